@@ -1,0 +1,520 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+Nothing here compares the oracle with itself: each check uses brute force on
+tiny inputs, a closed form, a hand-worked example (tests/golden), an invariant,
+or a library routine (torch's scaled_dot_product_attention in float64 on the
+CPU). ``test_oracle_mutations.py`` plants mistakes in copies of the oracle's
+functions and checks that these pins catch them.
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def load_counts():
+    rows = []
+    with open(os.path.join(GOLD, "eq5_counts.txt")) as fh:
+        for line in fh:
+            line = line.split("#")[0].strip()
+            if line:
+                M, s, nmin, nloc, n = line.split()
+                rows.append((int(M), float(s), int(nmin), int(nloc), int(n)))
+    return rows
+
+
+def worked():
+    with open(os.path.join(GOLD, "worked_example.json")) as fh:
+        return json.load(fh)
+
+
+# --------------------------------------------------------------------------
+# Pin helpers: each takes the function(s) under test and returns True/False,
+# so the mutation tests can run the same pins on planted mistakes.
+
+def pin_summaries_bruteforce(block_summaries, seed=0):
+    rng = np.random.default_rng(seed)
+    for L, b, D in [(37, 4, 3), (16, 16, 2), (5, 2, 2), (1, 8, 4), (33, 16, 5)]:
+        K = rng.integers(-9, 10, size=(L + 3, D)).astype(np.float64)
+        kmin, kmax = block_summaries(K, L, b)
+        M = -(-L // b)
+        if kmin.shape[0] != M:
+            return False
+        for m in range(M):
+            for j in range(D):
+                col = [K[t, j] for t in range(m * b, min(m * b + b, L))]
+                if kmin[m, j] != min(col) or kmax[m, j] != max(col):
+                    return False
+    return True
+
+
+def pin_worked_example(block_summaries, pooled_query, block_scores, num_selected,
+                       select_blocks):
+    ex = worked()
+    K = np.array(ex["K"], dtype=np.float64)
+    L, b = ex["seq_len"], ex["block_size"]
+    kmin, kmax = block_summaries(K, L, b)
+    if not (np.array_equal(kmin, ex["expect_kmin"]) and np.array_equal(kmax, ex["expect_kmax"])):
+        return False
+    qbar = pooled_query(np.array(ex["q_group"], dtype=np.float64))
+    if not np.array_equal(qbar, ex["expect_qbar"]):
+        return False
+    s = block_scores(qbar, kmin, kmax)
+    if not np.array_equal(s, ex["expect_scores"]):
+        return False
+    n = num_selected(3, ex["sparsity"], ex["min_blocks"], ex["n_local"])
+    if n != ex["expect_n"]:
+        return False
+    idx = select_blocks(s, n, ex["n_local"])
+    return list(idx) == ex["expect_idx"]
+
+
+def pin_eq5_table(num_selected):
+    return all(num_selected(M, s, nmin, nloc) == n for M, s, nmin, nloc, n in load_counts())
+
+
+def pin_eq5_closed_form(num_selected):
+    # ceil(M * (100 - k) / 100) in integer arithmetic, for s = k / 100.
+    for k in (0, 5, 10, 20, 50, 80, 90, 95, 98, 99):
+        s = k / 100
+        for M in list(range(0, 300)) + [4096, 4104, 16384, 65536, 1 << 20]:
+            keep = -(-(M * (100 - k)) // 100)
+            for nmin, nloc in ((0, 1), (16, 1), (64, 2), (0, 0)):
+                want = min(M, max(nmin, nloc, keep)) if M > 0 else 0
+                if num_selected(M, s, nmin, nloc) != want:
+                    return False
+    return True
+
+
+def pin_select_bruteforce(select_blocks, seed=0):
+    """The selected set is the unique n-subset whose every member beats every
+    non-member on (score desc, index asc); local blocks count as +inf."""
+    rng = np.random.default_rng(seed)
+    for trial in range(60):
+        M = int(rng.integers(1, 9))
+        n_local = int(rng.integers(0, min(M, 3) + 1))
+        n = int(rng.integers(max(n_local, 0), M + 1))
+        scores = rng.integers(-3, 4, size=M).astype(np.float64)  # many exact ties
+        eff = [math.inf if m >= M - n_local else scores[m] for m in range(M)]
+        winners = []
+        for S in itertools.combinations(range(M), n):
+            Sset = set(S)
+            ok = all((eff[a] > eff[c]) or (eff[a] == eff[c] and a < c)
+                     for a in Sset for c in range(M) if c not in Sset)
+            if ok:
+                winners.append(list(S))
+        if len(winners) != 1:
+            return False
+        got = select_blocks(scores, n, n_local)
+        if list(got) != winners[0]:
+            return False
+    return True
+
+
+def pin_quest_upper_bound(block_summaries, pooled_query, block_scores, seed=0):
+    """Eq. 4 bounds every in-block dot product: score_m >= max_t qbar . K_t."""
+    rng = np.random.default_rng(seed)
+    for L, b, D, g in [(64, 16, 8, 4), (50, 8, 16, 7), (9, 3, 4, 1)]:
+        K = rng.standard_normal((L, D))
+        q = rng.standard_normal((g, D))
+        kmin, kmax = block_summaries(K, L, b)
+        qbar = pooled_query(q)
+        s = block_scores(qbar, kmin, kmax)
+        for m in range(kmin.shape[0]):
+            best = max(float(np.dot(qbar, K[t])) for t in range(m * b, min(m * b + b, L)))
+            if s[m] < best - 1e-12:
+                return False
+    return True
+
+
+def pin_score_b1_is_dot(block_summaries, pooled_query, block_scores, seed=1):
+    """With one token per block, kmin = kmax = k and Eq. 4 is the plain dot product."""
+    rng = np.random.default_rng(seed)
+    K = rng.standard_normal((20, 6))
+    q = rng.standard_normal((3, 6))
+    kmin, kmax = block_summaries(K, 20, 1)
+    qbar = q.sum(axis=0) / 3
+    s = block_scores(pooled_query(q), kmin, kmax)
+    want = [math.fsum(qbar[j] * K[t, j] for j in range(6)) for t in range(20)]
+    return np.allclose(s, want, rtol=0, atol=1e-12)
+
+
+def pin_score_sign_split(block_scores, seed=2):
+    """score = sum_{q_j>=0} q_j kmax_j + sum_{q_j<0} q_j kmin_j (needs kmin <= kmax)."""
+    rng = np.random.default_rng(seed)
+    a = rng.standard_normal((12, 9))
+    c = rng.standard_normal((12, 9))
+    kmin, kmax = np.minimum(a, c), np.maximum(a, c)
+    qbar = rng.standard_normal(9)
+    s = block_scores(qbar, kmin, kmax)
+    for m in range(12):
+        want = math.fsum(qbar[j] * (kmax[m, j] if qbar[j] >= 0 else kmin[m, j]) for j in range(9))
+        if abs(s[m] - want) > 1e-12:
+            return False
+    return True
+
+
+def naive_attention(q, K, V, tokens, scale):
+    """Textbook softmax attention with Python loops and math.exp."""
+    out = []
+    lse = []
+    for qi in q:
+        z = [scale * math.fsum(qi[j] * K[t][j] for j in range(len(qi))) for t in tokens]
+        zm = max(z)
+        w = [math.exp(x - zm) for x in z]
+        den = math.fsum(w)
+        out.append([math.fsum(w[i] * V[t][d] for i, t in enumerate(tokens)) / den
+                    for d in range(len(V[0]))])
+        lse.append(zm + math.log(den))
+    return np.array(out), np.array(lse)
+
+
+def pin_attend_naive(attend, seed=3):
+    rng = np.random.default_rng(seed)
+    for T, D, g in [(7, 4, 2), (1, 3, 1), (20, 5, 4)]:
+        K = rng.standard_normal((T + 2, D))
+        V = rng.standard_normal((T + 2, D))
+        q = rng.standard_normal((g, D))
+        toks = sorted(rng.choice(T + 2, size=T, replace=False).tolist())
+        o, l = attend(q, K, V, toks, 0.37)
+        wo, wl = naive_attention(q, K, V, toks, 0.37)
+        if not (np.allclose(o, wo, rtol=0, atol=1e-12) and np.allclose(l, wl, rtol=0, atol=1e-12)):
+            return False
+    return True
+
+
+def pin_attend_sdpa(dense_attend, seed=4):
+    import torch
+    rng = np.random.default_rng(seed)
+    L, D, g = 45, 16, 4
+    K = rng.standard_normal((L, D))
+    V = rng.standard_normal((L, D))
+    q = rng.standard_normal((g, D))
+    o, _ = dense_attend(q, K, V, L, 1 / math.sqrt(D))
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q)[None, :, None, :], torch.from_numpy(K)[None, None].expand(1, g, L, D),
+        torch.from_numpy(V)[None, None].expand(1, g, L, D))[0, :, 0].numpy()
+    return np.allclose(o, ref, rtol=0, atol=1e-12)
+
+
+def pin_worked_attention(sparse_attend):
+    ex = worked()
+    K = np.array(ex["K"], dtype=np.float64)
+    V = np.array(ex["V"], dtype=np.float64)
+    q = np.array(ex["q_group"], dtype=np.float64)
+    o, l = sparse_attend(q, K, V, ex["seq_len"], ex["expect_idx"], ex["block_size"], ex["sm_scale"])
+    for h in range(2):
+        z = ex["expect_logits"][h]
+        e = [math.exp(x) for x in z]
+        den = sum(e)
+        want = [sum(e[i] * V[t][d] for i, t in enumerate(ex["expect_tokens"])) / den for d in range(2)]
+        if not np.allclose(o[h], want, rtol=0, atol=1e-13):
+            return False
+        if abs(l[h] - math.log(den)) > 1e-13:
+            return False
+    return True
+
+
+def pin_single_token(sparse_attend):
+    """A block holding a single valid token: output is that token's value."""
+    rng = np.random.default_rng(5)
+    K = rng.standard_normal((40, 4))
+    V = rng.standard_normal((40, 4))
+    q = rng.standard_normal((3, 4))
+    # L = 33, b = 8: block 4 holds only token 32.
+    o, l = sparse_attend(q, K, V, 33, [4], 8, 0.5)
+    return np.allclose(o, np.repeat(V[32][None], 3, axis=0), atol=1e-15) and \
+        np.allclose(l, 0.5 * (q @ K[32]), atol=1e-13)
+
+
+def pin_partition_merge(sparse_attend, merge_partials):
+    """Alg. 2: splitting the blocks into parts and LSE-merging equals one pass;
+    an empty part (lse = -inf) carries no weight."""
+    rng = np.random.default_rng(6)
+    K = rng.standard_normal((100, 8)) * 2
+    V = rng.standard_normal((100, 8))
+    q = rng.standard_normal((4, 8))
+    blocks = [0, 2, 3, 5, 7, 9, 12]
+    o, l = sparse_attend(q, K, V, 99, blocks, 8, 0.3)
+    parts = [blocks[:2], [], blocks[2:3], blocks[3:]]
+    outs, lses = zip(*[sparse_attend(q, K, V, 99, p, 8, 0.3) for p in parts])
+    mo, ml = merge_partials(np.array(outs), np.array(lses))
+    return np.allclose(mo, o, atol=1e-13) and np.allclose(ml, l, atol=1e-13)
+
+
+def textbook_causal(q, K, V, L, f, scale):
+    """Masked score matrix then row softmax (window row r is position L-f+r)."""
+    S = np.einsum("rd,td->rt", q, K[:L]) * scale
+    pos = np.arange(L)[None, :]
+    row = (L - f + np.arange(f))[:, None]
+    S = np.where(pos <= row, S, -np.inf)
+    P = np.exp(S - S.max(axis=1, keepdims=True))
+    P /= P.sum(axis=1, keepdims=True)
+    return P @ V[:L]
+
+
+def pin_rectify_textbook(rectify_group, block_summaries):
+    rng = np.random.default_rng(7)
+    for L, f, b, g, D in [(40, 8, 4, 3, 6), (17, 1, 16, 2, 4), (64, 32, 16, 4, 8), (12, 12, 5, 1, 3)]:
+        cap = L + 5
+        K = rng.standard_normal((cap, D))
+        V = rng.standard_normal((cap, D))
+        K0, V0 = K.copy(), V.copy()
+        mcap = -(-cap // b)
+        kmin = np.full((mcap, D), 7.0)
+        kmax = np.full((mcap, D), 7.0)
+        q = rng.standard_normal((g, f, D))
+        kf = rng.standard_normal((f, D))
+        vf = rng.standard_normal((f, D))
+        out, _ = rectify_group(q, K, V, kmin, kmax, L, f, b, 0.4, kf, vf)
+        Kw, Vw = K0.copy(), V0.copy()
+        Kw[L - f:L], Vw[L - f:L] = kf, vf
+        if not (np.array_equal(K, Kw) and np.array_equal(V, Vw)):
+            return False
+        for j in range(g):
+            if not np.allclose(out[j], textbook_causal(q[j], Kw, Vw, L, f, 0.4), atol=1e-12):
+                return False
+        rmin, rmax = block_summaries(Kw, L, b)
+        lo = (L - f) // b
+        M = -(-L // b)
+        if not (np.array_equal(kmin[lo:M], rmin[lo:M]) and np.array_equal(kmax[lo:M], rmax[lo:M])):
+            return False
+        if not (np.all(kmin[:lo] == 7.0) and np.all(kmin[M:] == 7.0)):
+            return False  # blocks without a rewritten row stay untouched
+    return True
+
+
+def pin_worked_rectify(rectify_group):
+    ex = worked()
+    r = ex["rectify"]
+    K = np.array(ex["K"], dtype=np.float64)
+    V = np.array(ex["V"], dtype=np.float64)
+    kmin = np.array(ex["expect_kmin"], dtype=np.float64)
+    kmax = np.array(ex["expect_kmax"], dtype=np.float64)
+    q = np.array(r["q_f"], dtype=np.float64)
+    out, _ = rectify_group(q, K, V, kmin, kmax, ex["seq_len"], r["f"], ex["block_size"], 1.0,
+                           np.array(r["k_f"], float), np.array(r["v_f"], float))
+    if not (np.array_equal(K, r["expect_K_after"]) and np.array_equal(kmin, r["expect_kmin_after"])
+            and np.array_equal(kmax, r["expect_kmax_after"])):
+        return False
+    for j in range(2):
+        for row, seen in enumerate(r["expect_rows_seen"]):
+            e = [math.exp(float(np.dot(q[j, row], K[t]))) for t in range(seen)]
+            want = [sum(e[t] * V[t][d] for t in range(seen)) / sum(e) for d in range(2)]
+            if not np.allclose(out[j, row], want, atol=1e-13):
+                return False
+    return True
+
+
+def pin_incremental_summary(update_summary, block_summaries, seed=8):
+    rng = np.random.default_rng(seed)
+    for b in (1, 4, 16):
+        D, L0, steps = 5, 13, 40
+        K = rng.integers(-20, 21, size=(L0 + steps, D)).astype(np.float64)
+        kmin, kmax = block_summaries(K, L0, b)
+        mcap = -(-(L0 + steps) // b)
+        # Slots past the current length hold stale values, as a reused cache does.
+        amin = np.full((mcap, D), -1e3)
+        amax = np.full((mcap, D), 1e3)
+        amin[:kmin.shape[0]], amax[:kmax.shape[0]] = kmin, kmax
+        for pos in range(L0, L0 + steps):
+            update_summary(amin, amax, pos, b, K[pos])
+            rmin, rmax = block_summaries(K, pos + 1, b)
+            M = rmin.shape[0]
+            if not (np.array_equal(amin[:M], rmin) and np.array_equal(amax[:M], rmax)):
+                return False
+    return True
+
+
+# ------------------------------------------------------------------- tests
+
+def test_bf16_widening_exact():
+    # IEEE bf16 patterns: 1.0, -2.0, 1 + 2^-7, smallest normal, largest finite.
+    bits = np.array([0x3F80, 0xC000, 0x3F81, 0x0080, 0x7F7F], dtype=np.uint16)
+    want = [1.0, -2.0, 1.0 + 2 ** -7, 2.0 ** -126, (2 - 2 ** -7) * 2.0 ** 127]
+    assert list(O.bf16_to_f64(bits)) == want
+    assert list(O.f64_to_bf16_exact(np.array(want))) == list(bits)
+    with pytest.raises(ValueError):
+        O.f64_to_bf16_exact(np.array([1.0 + 2 ** -9]))
+
+
+def test_generator_rounding_matches_definition():
+    # Round-to-nearest-even at the bf16 boundary, checked on hand-made halfway cases.
+    x = np.array([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -(1.0 + 2 ** -8), 1.0 + 2 ** -8 + 2 ** -20],
+                 dtype=np.float32)
+    got = O.bf16_to_f64(W.f32_to_bf16_bits(x))
+    assert list(got) == [1.0, 1.0 + 2 * 2 ** -7, -1.0, 1.0 + 2 ** -7]
+
+
+def test_summaries_bruteforce():
+    assert pin_summaries_bruteforce(O.block_summaries)
+
+
+def test_summary_bounds_and_union():
+    rng = np.random.default_rng(11)
+    K = rng.standard_normal((64, 8))
+    kmin, kmax = O.block_summaries(K, 64, 8)
+    for m in range(8):
+        assert np.all(kmin[m] <= K[m * 8:m * 8 + 8]) and np.all(K[m * 8:m * 8 + 8] <= kmax[m])
+    # Summary of a union of blocks = element-wise min/max of their summaries.
+    big_min, big_max = O.block_summaries(K, 64, 16)
+    assert np.array_equal(big_min, np.minimum(kmin[0::2], kmin[1::2]))
+    assert np.array_equal(big_max, np.maximum(kmax[0::2], kmax[1::2]))
+
+
+def test_incremental_summary():
+    assert pin_incremental_summary(O.update_summary, O.block_summaries)
+
+
+def test_worked_example_selection():
+    assert pin_worked_example(O.block_summaries, O.pooled_query, O.block_scores,
+                              O.num_selected, O.select_blocks)
+
+
+def test_worked_example_attention():
+    assert pin_worked_attention(O.sparse_attend)
+
+
+def test_worked_example_rectify():
+    assert pin_worked_rectify(O.rectify_group)
+
+
+def test_eq5_golden_counts():
+    assert pin_eq5_table(O.num_selected)
+
+
+def test_eq5_closed_form_grid():
+    assert pin_eq5_closed_form(O.num_selected)
+
+
+def test_select_bruteforce():
+    assert pin_select_bruteforce(O.select_blocks)
+
+
+def test_select_all_when_budget_covers():
+    s = np.array([3.0, -1.0, 2.0, 2.0, 0.5])
+    assert list(O.select_blocks(s, 5, 1)) == [0, 1, 2, 3, 4]
+    assert list(O.select_blocks(s, 2, 1)) == [0, 4]  # local block 4 is forced
+    assert list(O.select_blocks(s, 3, 0)) == [0, 2, 3]
+    assert list(O.select_blocks(s, 0, 0)) == []
+
+
+def test_quest_upper_bound():
+    assert pin_quest_upper_bound(O.block_summaries, O.pooled_query, O.block_scores)
+
+
+def test_score_b1_is_dot():
+    assert pin_score_b1_is_dot(O.block_summaries, O.pooled_query, O.block_scores)
+
+
+def test_score_sign_split():
+    assert pin_score_sign_split(O.block_scores)
+
+
+def test_attend_naive():
+    assert pin_attend_naive(O.attend)
+
+
+def test_attend_sdpa_f64():
+    assert pin_attend_sdpa(O.dense_attend)
+
+
+def test_single_token_block():
+    assert pin_single_token(O.sparse_attend)
+
+
+def test_partition_merge():
+    assert pin_partition_merge(O.sparse_attend, O.merge_partials)
+
+
+def test_sparse_equals_dense_when_all_blocks():
+    rng = np.random.default_rng(12)
+    K = rng.standard_normal((70, 16))
+    V = rng.standard_normal((70, 16))
+    q = rng.standard_normal((4, 16))
+    L, b = 61, 16
+    M = O.num_blocks(L, b)
+    so, sl = O.sparse_attend(q, K, V, L, range(M), b, 0.25)
+    do, dl = naive_attention(q, K, V, list(range(L)), 0.25)
+    assert np.allclose(so, do, atol=1e-12) and np.allclose(sl, dl, atol=1e-12)
+
+
+def test_garbage_beyond_length_ignored():
+    rng = np.random.default_rng(13)
+    K = rng.standard_normal((40, 8))
+    V = rng.standard_normal((40, 8))
+    q = rng.standard_normal((2, 8))
+    a = O.sparse_attend(q, K, V, 35, [0, 4], 8, 0.3)
+    K[35:] = 1e6
+    V[35:] = -1e6
+    b_ = O.sparse_attend(q, K, V, 35, [0, 4], 8, 0.3)
+    assert np.array_equal(a[0], b_[0]) and np.array_equal(a[1], b_[1])
+    kmin, _ = O.block_summaries(K, 35, 8)
+    assert np.all(kmin[4] < 1e5)
+
+
+def test_rectify_textbook():
+    assert pin_rectify_textbook(O.rectify_group, O.block_summaries)
+
+
+def test_rectify_f1_is_dense_decode():
+    rng = np.random.default_rng(14)
+    K = rng.standard_normal((30, 8))
+    V = rng.standard_normal((30, 8))
+    q = rng.standard_normal((3, 1, 8))
+    kf = rng.standard_normal((1, 8))
+    vf = rng.standard_normal((1, 8))
+    kmin = np.zeros((4, 8))
+    kmax = np.zeros((4, 8))
+    out, lse = O.rectify_group(q, K, V, kmin, kmax, 25, 1, 8, 0.3, kf, vf)
+    do, dl = naive_attention(q[:, 0], K, V, list(range(25)), 0.3)
+    assert np.allclose(out[:, 0], do, atol=1e-12) and np.allclose(lse[:, 0], dl, atol=1e-12)
+
+
+def test_planted_blocks_selected():
+    """With a strong planted direction (|u| = sqrt(d)) every planted block wins."""
+    w = W.TINY_4K.with_(plant_norm=math.sqrt(128), seed_tag="strong")
+    q = O.bf16_to_f64(W.decode_query(w))
+    g = w.group_size
+    for hi in range(w.num_kv_heads):
+        k, v = W.group_kv(w, 0, hi)
+        res = O.decode_group(q[0, hi * g:(hi + 1) * g], O.bf16_to_f64(k), O.bf16_to_f64(v),
+                             w.seq_len, w.block_size, w.sparsity, w.min_blocks, w.n_local,
+                             w.sm_scale)
+        planted = set(W.planted_blocks(w, 0, hi).tolist())
+        assert planted <= set(res["idx"].tolist())
+        assert res["n"] == 64 and (w.num_blocks - 1) in set(res["idx"].tolist())
+
+
+def test_decode_state_loop_consistent():
+    """Kernel-level Alg. 1 loop: after appends, the incrementally kept block keys
+    equal a recompute, and a rectification leaves them equal again."""
+    w = W.TINY_4K.with_(seq_len=100, batch=2, num_q_heads=4, num_kv_heads=2, head_dim=8,
+                        block_size=8, min_tokens=16, rectify_every=6, planted_per_head=2)
+    K, V = W.kv_cache(w, capacity=140)
+    st = O.DecodeState(O.bf16_to_f64(K), O.bf16_to_f64(V), [100, 93], w.block_size)
+    for step in range(12):
+        kn, vn = W.decode_kv(w, step)
+        st.append(O.bf16_to_f64(kn), O.bf16_to_f64(vn))
+        if (step + 1) % 6 == 0:
+            lastk = np.stack([np.stack([W.f32_to_bf16_bits(st.K[bi, hi, st.L[bi] - 6:st.L[bi]].astype(np.float32))
+                                        for hi in range(2)]) for bi in range(2)])
+            lastv = np.stack([np.stack([W.f32_to_bf16_bits(st.V[bi, hi, st.L[bi] - 6:st.L[bi]].astype(np.float32))
+                                        for hi in range(2)]) for bi in range(2)])
+            qf, kf, vf = W.rectify_inputs(w, step, lastk, lastv, 6)
+            st.rectify(O.bf16_to_f64(qf), O.bf16_to_f64(kf), O.bf16_to_f64(vf), 6, w.sm_scale)
+        for bi in range(2):
+            for hi in range(2):
+                rmin, rmax = O.block_summaries(st.K[bi, hi], st.L[bi], 8)
+                M = rmin.shape[0]
+                assert np.array_equal(st.kmin[bi, hi, :M], rmin)
+                assert np.array_equal(st.kmax[bi, hi, :M], rmax)
+    assert st.L == [112, 105]
