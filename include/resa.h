@@ -1,0 +1,220 @@
+/*
+ * resa.h - C ABI of the ReSA decode library for AMD Instinct MI355X (gfx950).
+ *
+ * Rectified Sparse Attention ("ReSA", arXiv 2506.04108) decodes with
+ * group block-sparse attention (Sec. 2.1) and periodically re-encodes the
+ * most recent f tokens densely (Sec. 2.2, Alg. 1). This library implements
+ * one attention layer's share of that loop on one GPU:
+ *
+ *   resa_block_summarize  Eq. 3   block key summaries (element-wise min/max)
+ *   resa_append_kv        Alg. 1  append one token, update its block summary
+ *   resa_select_blocks    Eq. 4-5 pooled-query Quest score + dynamic top-n
+ *   resa_sparse_decode    Eq. 2, Alg. 2  split flash-decoding over the
+ *                                 selected blocks with log-sum-exp combine
+ *   resa_dense_rectify    Sec. 2.2  rewrite the last f cache rows, dense
+ *                                 causal attention of their queries over the
+ *                                 whole cache, refresh the touched summaries
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Every tensor argument is a DEVICE pointer to caller-owned memory
+ *   (usually allocated by PyTorch). The library never allocates, frees or
+ *   synchronises; scratch comes from a caller workspace sized by the matching
+ *   resa_*_workspace_size() call.
+ * - Calls are asynchronous on the HIP stream passed as `stream` (a
+ *   hipStream_t; NULL is the default stream). A call returns once its kernels
+ *   are enqueued.
+ * - Return value: RESA_OK, or an error code; resa_last_error() then gives a
+ *   message (per host thread). Argument checks run before any HIP call, so a
+ *   rejected call touches neither the device nor the stream.
+ * - Data types: bf16 caches and queries (uint16 bit patterns), fp32 outputs,
+ *   int32 lengths and indices. All pointers must be 16-byte aligned.
+ * - Supported shapes: head_dim 128; block_size 16, 32 or 64; capacity a
+ *   multiple of block_size; 1 <= num_q_heads / num_kv_heads <= 8.
+ * - Layouts (row-major, last index fastest):
+ *     k, v        [batch, num_kv_heads, capacity, head_dim]
+ *     kmin, kmax  [batch, num_kv_heads, capacity / block_size, head_dim]
+ *     q           [batch, num_q_heads, head_dim]; query head h belongs to
+ *                 kv head h / g, g = num_q_heads / num_kv_heads (GQA, Eq. 1)
+ *     seq_lens    [batch] int32, current length L_b of each sequence
+ * - A block m of sequence b covers tokens [m*block_size, (m+1)*block_size)
+ *   cut at L_b; M_b = ceil(L_b / block_size) blocks exist.
+ */
+#ifndef RESA_H_
+#define RESA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RESA_HEAD_DIM 128
+#define RESA_MAX_GROUP 8
+
+typedef enum resa_status {
+  RESA_OK = 0,
+  RESA_ERR_INVALID_ARG = 1,  /* null/misaligned pointer, bad size or range */
+  RESA_ERR_UNSUPPORTED = 2,  /* valid in principle, not built (e.g. head_dim) */
+  RESA_ERR_WORKSPACE = 3,    /* workspace missing or too small */
+  RESA_ERR_CAPACITY = 4,     /* n_cap or cache capacity too small */
+  RESA_ERR_HIP = 5           /* a HIP runtime call or launch failed */
+} resa_status_t;
+
+/* The KV cache of one attention layer and its block-key cache. */
+typedef struct resa_kv_cache {
+  void* k;              /* bf16 [batch, num_kv_heads, capacity, head_dim] */
+  void* v;              /* bf16, same layout as k */
+  void* kmin;           /* bf16 [batch, num_kv_heads, capacity / block_size, head_dim] */
+  void* kmax;           /* bf16, same layout as kmin */
+  int32_t batch;
+  int32_t num_kv_heads;
+  int32_t head_dim;     /* 128 */
+  int32_t capacity;     /* rows per (batch, kv head); multiple of block_size */
+  int32_t block_size;   /* b: 16, 32 or 64 */
+} resa_kv_cache_t;
+
+/* Block-selection parameters (Sec. 2.1, Eq. 5). */
+typedef struct resa_select_params {
+  double sparsity;      /* s in [0, 1): share of blocks skipped; keep = 1 - s.
+                           Rounded to the nearest multiple of 1e-6. */
+  int32_t min_blocks;   /* n_min >= 0: minimum number of selected blocks */
+  int32_t n_local;      /* >= 0: most recent blocks always selected */
+} resa_select_params_t;
+
+/* Library version string ("major.minor.patch"). */
+const char* resa_version(void);
+
+/* Message of the last failed call on this host thread ("" if none). */
+const char* resa_last_error(void);
+
+/*
+ * Eq. 5 (Sec. 2.1), reading p as the kept fraction:
+ *   n = min(M, max(min_blocks, n_local, ceil(M * (1 - sparsity))))
+ * in exact integer arithmetic on sparsity rounded to 1e-6; 0 when M == 0.
+ * The device-side selection uses the same arithmetic. Host only, no device
+ * access. Returns -1 for invalid arguments (M < 0, sparsity outside [0, 1),
+ * negative min_blocks or n_local).
+ */
+int32_t resa_num_selected(int32_t num_blocks, double sparsity, int32_t min_blocks,
+                          int32_t n_local);
+
+/*
+ * Eq. 3 (Sec. 2.1, "Block Representation"): for every sequence b and kv head,
+ * kmin/kmax of blocks [blk_begin, blk_end) become the element-wise min/max
+ * of the block's valid keys (tokens < L_b). blk_end = -1 means "through the
+ * last block of each sequence"; blocks at or past M_b are left untouched.
+ * Exact: the min/max of bf16 values is a bf16 value. Reads c->k, writes
+ * c->kmin and c->kmax. Used after prefill and by resa_dense_rectify.
+ */
+int resa_block_summarize(const resa_kv_cache_t* c, const int32_t* seq_lens,
+                         int32_t blk_begin, int32_t blk_end, void* stream);
+
+/*
+ * Alg. 1, "Update KV cache / block key cache with t": for every sequence b,
+ * writes k_new[b], v_new[b] ([batch, num_kv_heads, head_dim] bf16) at row
+ * p = seq_lens[b] and folds the key into block p / block_size's summary
+ * (initialising it when p opens the block), then sets seq_lens[b] = p + 1
+ * in place. max_seq_len is a host-side upper bound of seq_lens before the
+ * call; it must be < capacity (RESA_ERR_CAPACITY otherwise). A sequence whose
+ * device length has reached capacity is left unchanged.
+ */
+int resa_append_kv(const resa_kv_cache_t* c, const void* k_new, const void* v_new,
+                   int32_t* seq_lens, int32_t max_seq_len, void* stream);
+
+/* Workspace bytes resa_select_blocks needs (0 if scores_out is given). */
+size_t resa_select_workspace_size(int32_t batch, int32_t num_kv_heads,
+                                  int32_t max_seq_len, int32_t block_size,
+                                  int32_t with_scores_out);
+
+/*
+ * Fig. 3 + Eq. 4 + Eq. 5 (Sec. 2.1, "Block Selection"), per (sequence b,
+ * kv head i):
+ *   qbar     = mean of the g query heads of group i             (fp32)
+ *   score_m  = sum_j max(qbar_j * kmax_mj, qbar_j * kmin_mj)     (fp32)
+ *   the last n_local blocks count as +inf; n = resa_num_selected(M_b, ...)
+ *   block_idx[b, i, :n] = the n best blocks by (score desc, id asc),
+ *                         written in ascending id order; the rest of the
+ *                         row up to n_cap is set to -1
+ *   num_sel[b, i] = n
+ * q: bf16 [batch, num_q_heads, head_dim]. block_idx: int32 [batch,
+ * num_kv_heads, n_cap]; num_sel: int32 [batch, num_kv_heads]. n_cap must be
+ * >= resa_num_selected(ceil(max_seq_len / block_size), ...) (else
+ * RESA_ERR_CAPACITY). scores_out (optional, may be NULL): fp32 [batch,
+ * num_kv_heads, ceil(max_seq_len / block_size)], receives the Eq. 4 scores
+ * before local forcing (entries past M_b are not written). When scores_out is
+ * NULL the scores live in the workspace.
+ */
+int resa_select_blocks(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
+                       const int32_t* seq_lens, int32_t max_seq_len,
+                       const resa_select_params_t* params, int32_t* block_idx,
+                       int32_t* num_sel, int32_t n_cap, float* scores_out,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* Split count resa_sparse_decode uses when num_splits = 0. */
+int32_t resa_decode_num_splits(int32_t batch, int32_t num_kv_heads, int32_t n_cap,
+                               int32_t block_size);
+
+/* Workspace bytes resa_sparse_decode needs for the given split count
+ * (0 = the automatic count). */
+size_t resa_decode_workspace_size(int32_t batch, int32_t num_kv_heads,
+                                  int32_t num_q_heads, int32_t n_cap,
+                                  int32_t block_size, int32_t num_splits);
+
+/*
+ * Eq. 2 with Alg. 2 (App. A): block-sparse flash-decoding. For every
+ * (sequence b, kv head i) the selected blocks block_idx[b, i, :num_sel[b, i]]
+ * (ids in [0, M_b); any order; as written by resa_select_blocks) are split
+ * into num_splits contiguous parts; each part runs an online softmax of the g
+ * query heads over its blocks' valid tokens (t < L_b; others are excluded)
+ * and the parts are merged by log-sum-exp. For query head h:
+ *   out[b, h, :] = sum_t softmax_t(q_h . K_t * sm_scale) V_t     (fp32)
+ *   lse[b, h]    = log sum_t exp(q_h . K_t * sm_scale)           (optional)
+ * With no token selected, out is 0 and lse is -inf. Passing every block id
+ * gives dense decoding. num_splits = 0 picks resa_decode_num_splits().
+ * The workspace holds split partials and one merge counter per group: it
+ * must be zero-filled before its first use (resa_workspace_clear) and every
+ * call leaves the counters at zero again. Calls that share a workspace must
+ * be ordered on one stream.
+ */
+int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
+                       const int32_t* seq_lens, const int32_t* block_idx,
+                       const int32_t* num_sel, int32_t n_cap, int32_t num_splits,
+                       float sm_scale, float* out, float* lse, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/* Workspace bytes resa_dense_rectify needs. */
+size_t resa_rectify_workspace_size(int32_t batch, int32_t num_kv_heads,
+                                   int32_t num_q_heads, int32_t f, int32_t max_seq_len);
+
+/*
+ * Dense rectification (Sec. 2.2; Alg. 1, "DenseForward" every f steps) of
+ * one layer. For every sequence b with length L = seq_lens[b] >= f:
+ *   1. rows [L - f, L) of k and v become k_f[b], v_f[b]
+ *      (bf16 [batch, num_kv_heads, f, head_dim]);
+ *   2. query row r of q_f[b, h] (bf16 [batch, num_q_heads, f, head_dim]) sits
+ *      at position L - f + r and attends causally to tokens t <= L - f + r:
+ *        out[b, h, r, :] = sum_t softmax_t(q . K_t * sm_scale) V_t   (fp32)
+ *        lse[b, h, r]    = log sum_t exp(...)            (optional, may be NULL)
+ *   3. if refresh_summaries, blocks floor((L - f) / b) .. M_b - 1 are
+ *      re-summarised (Eq. 3).
+ * 1 <= f <= 128 and f <= max_seq_len <= capacity. max_seq_len bounds every
+ * seq_lens[b] (host side, for launch sizing). The workspace holds split
+ * partials and merge counters: zero-fill it before first use; every call
+ * leaves the counters at zero.
+ */
+int resa_dense_rectify(const resa_kv_cache_t* c, const void* q_f, const void* k_f,
+                       const void* v_f, int32_t num_q_heads, int32_t f,
+                       const int32_t* seq_lens, int32_t max_seq_len, float sm_scale,
+                       float* out, float* lse, int32_t refresh_summaries,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* Zero-fills a workspace with a kernel (safe under stream capture). */
+int resa_workspace_clear(void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RESA_H_ */

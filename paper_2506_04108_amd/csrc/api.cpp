@@ -1,0 +1,378 @@
+// C ABI of the ReSA decode library: argument validation (before any HIP call),
+// workspace layout, launch configuration and error reporting.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "resa_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return RESA_OK;
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
+
+#define RESA_CHECK_PTR(p, align)                                                        \
+  do {                                                                                  \
+    if ((p) == nullptr) return fail(RESA_ERR_INVALID_ARG, "%s is NULL", #p);            \
+    if (!aligned((p), (align)))                                                         \
+      return fail(RESA_ERR_INVALID_ARG, "%s is not %d-byte aligned", #p, (int)(align)); \
+  } while (0)
+
+int check_cache(const resa_kv_cache_t* c) {
+  if (c == nullptr) return fail(RESA_ERR_INVALID_ARG, "cache descriptor is NULL");
+  RESA_CHECK_PTR(c->k, 16);
+  RESA_CHECK_PTR(c->v, 16);
+  RESA_CHECK_PTR(c->kmin, 16);
+  RESA_CHECK_PTR(c->kmax, 16);
+  if (c->head_dim != RESA_HEAD_DIM)
+    return fail(RESA_ERR_UNSUPPORTED, "head_dim %d unsupported (only 128)", c->head_dim);
+  if (c->block_size != 16 && c->block_size != 32 && c->block_size != 64)
+    return fail(RESA_ERR_UNSUPPORTED, "block_size %d unsupported (16, 32 or 64)", c->block_size);
+  if (c->batch < 1 || c->num_kv_heads < 1)
+    return fail(RESA_ERR_INVALID_ARG, "batch (%d) and num_kv_heads (%d) must be >= 1", c->batch,
+                c->num_kv_heads);
+  if ((int64_t)c->batch * c->num_kv_heads > 65535)
+    return fail(RESA_ERR_UNSUPPORTED, "batch * num_kv_heads = %lld exceeds 65535",
+                (long long)c->batch * c->num_kv_heads);
+  if (c->capacity < c->block_size || c->capacity % c->block_size != 0)
+    return fail(RESA_ERR_INVALID_ARG, "capacity %d must be a positive multiple of block_size %d",
+                c->capacity, c->block_size);
+  return RESA_OK;
+}
+
+resa::CacheArgs cache_args(const resa_kv_cache_t* c) {
+  resa::CacheArgs a;
+  a.k = static_cast<const uint16_t*>(c->k);
+  a.v = static_cast<const uint16_t*>(c->v);
+  a.kmin = static_cast<uint16_t*>(c->kmin);
+  a.kmax = static_cast<uint16_t*>(c->kmax);
+  a.batch = c->batch;
+  a.kv_heads = c->num_kv_heads;
+  a.capacity = c->capacity;
+  a.block_size = c->block_size;
+  a.max_blocks = c->capacity / c->block_size;
+  return a;
+}
+
+int check_heads(const resa_kv_cache_t* c, int32_t num_q_heads, int32_t* group) {
+  if (num_q_heads < 1 || num_q_heads % c->num_kv_heads != 0)
+    return fail(RESA_ERR_INVALID_ARG, "num_q_heads %d is not a positive multiple of num_kv_heads %d",
+                num_q_heads, c->num_kv_heads);
+  const int32_t g = num_q_heads / c->num_kv_heads;
+  if (g > RESA_MAX_GROUP)
+    return fail(RESA_ERR_UNSUPPORTED, "group size %d exceeds %d", g, RESA_MAX_GROUP);
+  *group = g;
+  return RESA_OK;
+}
+
+bool parse_sparsity(double s, int32_t* keep_ppm) {
+  if (!(s >= 0.0 && s <= 1.0)) return false;
+  const long long sp = llround(s * 1e6);
+  *keep_ppm = (int32_t)(1000000 - sp);
+  return true;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(RESA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+struct DecodeLayout {
+  size_t counters, lse, o, total;
+};
+
+DecodeLayout decode_layout(int32_t batch, int32_t kv_heads, int32_t group, int32_t splits) {
+  DecodeLayout d;
+  const size_t groups = (size_t)batch * kv_heads;
+  d.counters = 0;
+  d.lse = round256(groups * 4);
+  d.o = d.lse + round256(groups * splits * group * 4);
+  d.total = d.o + groups * splits * group * RESA_HEAD_DIM * 4;
+  return d;
+}
+
+struct RectifyLayout {
+  int32_t nq, chunk, splits;
+  size_t counters, lse, o, total;
+};
+
+RectifyLayout rectify_layout(int32_t batch, int32_t kv_heads, int32_t group, int32_t f,
+                             int32_t max_seq_len) {
+  RectifyLayout r;
+  r.nq = resa::rectify_num_qblocks(group, f);
+  r.chunk = resa::rectify_chunk(batch, kv_heads, r.nq, max_seq_len);
+  r.splits = (max_seq_len + r.chunk - 1) / r.chunk;
+  if (r.splits < 1) r.splits = 1;
+  const size_t groups = (size_t)batch * kv_heads;
+  const size_t rows = (size_t)group * f;
+  r.counters = 0;
+  r.lse = round256(groups * r.nq * 4);
+  r.o = r.lse + round256(groups * r.splits * rows * 4);
+  r.total = r.o + groups * r.splits * rows * RESA_HEAD_DIM * 4;
+  return r;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* resa_version(void) { return "0.1.0"; }
+
+const char* resa_last_error(void) { return g_err.c_str(); }
+
+int32_t resa_num_selected(int32_t num_blocks, double sparsity, int32_t min_blocks,
+                          int32_t n_local) {
+  int32_t keep = 0;
+  if (num_blocks < 0 || min_blocks < 0 || n_local < 0 || !parse_sparsity(sparsity, &keep)) {
+    fail(RESA_ERR_INVALID_ARG, "resa_num_selected: invalid argument");
+    return -1;
+  }
+  return resa::count_selected(num_blocks, keep, min_blocks, n_local);
+}
+
+int resa_block_summarize(const resa_kv_cache_t* c, const int32_t* seq_lens, int32_t blk_begin,
+                         int32_t blk_end, void* stream) {
+  if (int e = check_cache(c)) return e;
+  RESA_CHECK_PTR(seq_lens, 4);
+  const int32_t mb = c->capacity / c->block_size;
+  if (blk_begin < 0 || blk_begin > mb)
+    return fail(RESA_ERR_INVALID_ARG, "blk_begin %d outside [0, %d]", blk_begin, mb);
+  if (blk_end != -1 && (blk_end < blk_begin || blk_end > mb))
+    return fail(RESA_ERR_INVALID_ARG, "blk_end %d outside [blk_begin, %d] (or -1)", blk_end, mb);
+  hipError_t e = resa::launch_summarize(cache_args(c), seq_lens, blk_begin, blk_end,
+                                        static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "resa_block_summarize launch");
+  return ok();
+}
+
+int resa_append_kv(const resa_kv_cache_t* c, const void* k_new, const void* v_new,
+                   int32_t* seq_lens, int32_t max_seq_len, void* stream) {
+  if (int e = check_cache(c)) return e;
+  RESA_CHECK_PTR(k_new, 16);
+  RESA_CHECK_PTR(v_new, 16);
+  RESA_CHECK_PTR(seq_lens, 4);
+  if (max_seq_len < 0) return fail(RESA_ERR_INVALID_ARG, "max_seq_len %d < 0", max_seq_len);
+  if (max_seq_len >= c->capacity)
+    return fail(RESA_ERR_CAPACITY, "cache full: max_seq_len %d, capacity %d", max_seq_len,
+                c->capacity);
+  hipError_t e = resa::launch_append(cache_args(c), static_cast<const uint16_t*>(k_new),
+                                     static_cast<const uint16_t*>(v_new), seq_lens,
+                                     static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "resa_append_kv launch");
+  return ok();
+}
+
+size_t resa_select_workspace_size(int32_t batch, int32_t num_kv_heads, int32_t max_seq_len,
+                                  int32_t block_size, int32_t with_scores_out) {
+  if (with_scores_out || batch < 1 || num_kv_heads < 1 || max_seq_len < 0 || block_size < 1) return 0;
+  const size_t mseq = ((size_t)max_seq_len + block_size - 1) / block_size;
+  return (size_t)batch * num_kv_heads * mseq * sizeof(float);
+}
+
+int resa_select_blocks(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
+                       const int32_t* seq_lens, int32_t max_seq_len,
+                       const resa_select_params_t* params, int32_t* block_idx, int32_t* num_sel,
+                       int32_t n_cap, float* scores_out, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  if (int e = check_cache(c)) return e;
+  int32_t group = 0;
+  if (int e = check_heads(c, num_q_heads, &group)) return e;
+  RESA_CHECK_PTR(q, 16);
+  RESA_CHECK_PTR(seq_lens, 4);
+  RESA_CHECK_PTR(block_idx, 4);
+  RESA_CHECK_PTR(num_sel, 4);
+  if (params == nullptr) return fail(RESA_ERR_INVALID_ARG, "params is NULL");
+  int32_t keep = 0;
+  if (!parse_sparsity(params->sparsity, &keep))
+    return fail(RESA_ERR_INVALID_ARG, "sparsity %g outside [0, 1]", params->sparsity);
+  if (params->min_blocks < 0 || params->n_local < 0)
+    return fail(RESA_ERR_INVALID_ARG, "min_blocks (%d) and n_local (%d) must be >= 0",
+                params->min_blocks, params->n_local);
+  if (max_seq_len < 0 || max_seq_len > c->capacity)
+    return fail(RESA_ERR_INVALID_ARG, "max_seq_len %d outside [0, capacity %d]", max_seq_len,
+                c->capacity);
+  const int32_t mseq = (max_seq_len + c->block_size - 1) / c->block_size;
+  const int32_t need = resa::count_selected(mseq, keep, params->min_blocks, params->n_local);
+  if (n_cap < need)
+    return fail(RESA_ERR_CAPACITY, "n_cap %d < %d blocks selectable at max_seq_len %d", n_cap, need,
+                max_seq_len);
+  float* scores = scores_out;
+  if (scores_out != nullptr) {
+    RESA_CHECK_PTR(scores_out, 4);
+  } else {
+    const size_t want = resa_select_workspace_size(c->batch, c->num_kv_heads, max_seq_len,
+                                                   c->block_size, 0);
+    if (want > 0) {
+      if (workspace == nullptr || workspace_bytes < want)
+        return fail(RESA_ERR_WORKSPACE, "select workspace needs %zu bytes, got %zu", want,
+                    workspace == nullptr ? (size_t)0 : workspace_bytes);
+      if (!aligned(workspace, 16)) return fail(RESA_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
+    }
+    scores = static_cast<float*>(workspace);
+  }
+  resa::SelectArgs a;
+  a.c = cache_args(c);
+  a.q = static_cast<const uint16_t*>(q);
+  a.q_heads = num_q_heads;
+  a.group = group;
+  a.seq_lens = seq_lens;
+  a.max_blocks_seq = mseq;
+  a.keep_ppm = keep;
+  a.min_blocks = params->min_blocks;
+  a.n_local = params->n_local;
+  a.scores = scores;
+  a.block_idx = block_idx;
+  a.num_sel = num_sel;
+  a.n_cap = n_cap;
+  hipError_t e = resa::launch_select(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "resa_select_blocks launch");
+  return ok();
+}
+
+int32_t resa_decode_num_splits(int32_t batch, int32_t num_kv_heads, int32_t n_cap,
+                               int32_t block_size) {
+  if (batch < 1 || num_kv_heads < 1 || n_cap < 0 || block_size < 16) return 1;
+  return resa::decode_auto_splits(batch, num_kv_heads, n_cap, block_size);
+}
+
+size_t resa_decode_workspace_size(int32_t batch, int32_t num_kv_heads, int32_t num_q_heads,
+                                  int32_t n_cap, int32_t block_size, int32_t num_splits) {
+  if (batch < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || num_splits < 0) return 0;
+  const int32_t s = num_splits > 0 ? num_splits
+                                   : resa_decode_num_splits(batch, num_kv_heads, n_cap, block_size);
+  return decode_layout(batch, num_kv_heads, num_q_heads / num_kv_heads, s).total;
+}
+
+int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
+                       const int32_t* seq_lens, const int32_t* block_idx, const int32_t* num_sel,
+                       int32_t n_cap, int32_t num_splits, float sm_scale, float* out, float* lse,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+  if (int e = check_cache(c)) return e;
+  int32_t group = 0;
+  if (int e = check_heads(c, num_q_heads, &group)) return e;
+  RESA_CHECK_PTR(q, 16);
+  RESA_CHECK_PTR(seq_lens, 4);
+  RESA_CHECK_PTR(block_idx, 4);
+  RESA_CHECK_PTR(num_sel, 4);
+  RESA_CHECK_PTR(out, 4);
+  if (lse != nullptr && !aligned(lse, 4)) return fail(RESA_ERR_INVALID_ARG, "lse is not 4-byte aligned");
+  if (n_cap < 0) return fail(RESA_ERR_INVALID_ARG, "n_cap %d < 0", n_cap);
+  if (num_splits < 0 || num_splits > 65535)
+    return fail(RESA_ERR_INVALID_ARG, "num_splits %d outside [0, 65535]", num_splits);
+  if (!std::isfinite(sm_scale)) return fail(RESA_ERR_INVALID_ARG, "sm_scale is not finite");
+  const int32_t s = num_splits > 0 ? num_splits
+                                   : resa::decode_auto_splits(c->batch, c->num_kv_heads, n_cap,
+                                                              c->block_size);
+  const DecodeLayout lay = decode_layout(c->batch, c->num_kv_heads, group, s);
+  if (workspace == nullptr || workspace_bytes < lay.total)
+    return fail(RESA_ERR_WORKSPACE, "decode workspace needs %zu bytes, got %zu", lay.total,
+                workspace == nullptr ? (size_t)0 : workspace_bytes);
+  if (!aligned(workspace, 16)) return fail(RESA_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
+  char* ws = static_cast<char*>(workspace);
+  resa::DecodeArgs a;
+  a.c = cache_args(c);
+  a.q = static_cast<const uint16_t*>(q);
+  a.q_heads = num_q_heads;
+  a.group = group;
+  a.seq_lens = seq_lens;
+  a.block_idx = block_idx;
+  a.num_sel = num_sel;
+  a.n_cap = n_cap;
+  a.num_splits = s;
+  a.scale_log2 = sm_scale * 1.4426950408889634f;
+  a.out = out;
+  a.lse = lse;
+  a.counters = reinterpret_cast<uint32_t*>(ws + lay.counters);
+  a.part_lse = reinterpret_cast<float*>(ws + lay.lse);
+  a.part_o = reinterpret_cast<float*>(ws + lay.o);
+  hipError_t e = resa::launch_decode(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "resa_sparse_decode launch");
+  return ok();
+}
+
+size_t resa_rectify_workspace_size(int32_t batch, int32_t num_kv_heads, int32_t num_q_heads,
+                                   int32_t f, int32_t max_seq_len) {
+  if (batch < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || f < 1 || max_seq_len < 1)
+    return 0;
+  return rectify_layout(batch, num_kv_heads, num_q_heads / num_kv_heads, f, max_seq_len).total;
+}
+
+int resa_dense_rectify(const resa_kv_cache_t* c, const void* q_f, const void* k_f,
+                       const void* v_f, int32_t num_q_heads, int32_t f, const int32_t* seq_lens,
+                       int32_t max_seq_len, float sm_scale, float* out, float* lse,
+                       int32_t refresh_summaries, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  if (int e = check_cache(c)) return e;
+  int32_t group = 0;
+  if (int e = check_heads(c, num_q_heads, &group)) return e;
+  RESA_CHECK_PTR(q_f, 16);
+  RESA_CHECK_PTR(k_f, 16);
+  RESA_CHECK_PTR(v_f, 16);
+  RESA_CHECK_PTR(seq_lens, 4);
+  RESA_CHECK_PTR(out, 16);
+  if (lse != nullptr && !aligned(lse, 4)) return fail(RESA_ERR_INVALID_ARG, "lse is not 4-byte aligned");
+  if (f < 1 || f > 128) return fail(RESA_ERR_INVALID_ARG, "f %d outside [1, 128]", f);
+  if (max_seq_len < f || max_seq_len > c->capacity)
+    return fail(RESA_ERR_INVALID_ARG, "max_seq_len %d outside [f = %d, capacity %d]", max_seq_len,
+                f, c->capacity);
+  if (!std::isfinite(sm_scale)) return fail(RESA_ERR_INVALID_ARG, "sm_scale is not finite");
+  const RectifyLayout lay = rectify_layout(c->batch, c->num_kv_heads, group, f, max_seq_len);
+  if (workspace == nullptr || workspace_bytes < lay.total)
+    return fail(RESA_ERR_WORKSPACE, "rectify workspace needs %zu bytes, got %zu", lay.total,
+                workspace == nullptr ? (size_t)0 : workspace_bytes);
+  if (!aligned(workspace, 16)) return fail(RESA_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
+  char* ws = static_cast<char*>(workspace);
+  resa::RectifyArgs a;
+  a.c = cache_args(c);
+  a.q_f = static_cast<const uint16_t*>(q_f);
+  a.k_f = static_cast<const uint16_t*>(k_f);
+  a.v_f = static_cast<const uint16_t*>(v_f);
+  a.q_heads = num_q_heads;
+  a.group = group;
+  a.f = f;
+  a.seq_lens = seq_lens;
+  a.max_seq_len = max_seq_len;
+  a.chunk = lay.chunk;
+  a.num_splits = lay.splits;
+  a.scale_log2 = sm_scale * 1.4426950408889634f;
+  a.out = out;
+  a.lse = lse;
+  a.counters = reinterpret_cast<uint32_t*>(ws + lay.counters);
+  a.part_lse = reinterpret_cast<float*>(ws + lay.lse);
+  a.part_o = reinterpret_cast<float*>(ws + lay.o);
+  a.refresh = refresh_summaries ? 1 : 0;
+  hipError_t e = resa::launch_rectify(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "resa_dense_rectify launch");
+  return ok();
+}
+
+int resa_workspace_clear(void* workspace, size_t workspace_bytes, void* stream) {
+  if (workspace_bytes == 0) return ok();
+  RESA_CHECK_PTR(workspace, 16);
+  hipError_t e = resa::launch_clear(workspace, workspace_bytes, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "resa_workspace_clear launch");
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,98 @@
+// Internal interface between the C-ABI layer (api.cpp) and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/resa.h"
+
+namespace resa {
+
+// Eq. 5 (Sec. 2.1) in integer arithmetic; `keep_ppm` = round((1 - s) * 1e6).
+// n = min(M, max(min_blocks, n_local, ceil(M * keep_ppm / 1e6))); 0 if M <= 0.
+__host__ __device__ inline int32_t count_selected(int32_t M, int32_t keep_ppm,
+                                                  int32_t min_blocks, int32_t n_local) {
+  if (M <= 0) return 0;
+  int64_t n = ((int64_t)M * keep_ppm + 999999) / 1000000;
+  if (n < min_blocks) n = min_blocks;
+  if (n < n_local) n = n_local;
+  if (n > M) n = M;
+  return (int32_t)n;
+}
+
+// Plain-value view of a resa_kv_cache_t for kernel arguments.
+struct CacheArgs {
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* kmin;
+  uint16_t* kmax;
+  int32_t batch, kv_heads, capacity, block_size, max_blocks;  // max_blocks = capacity / b
+};
+
+struct SelectArgs {
+  CacheArgs c;
+  const uint16_t* q;
+  int32_t q_heads, group;      // group = q_heads / kv_heads
+  const int32_t* seq_lens;
+  int32_t max_blocks_seq;      // ceil(max_seq_len / b): row stride of the score array
+  int32_t keep_ppm, min_blocks, n_local;
+  float* scores;               // [B, Hkv, max_blocks_seq]
+  int32_t* block_idx;          // [B, Hkv, n_cap]
+  int32_t* num_sel;            // [B, Hkv]
+  int32_t n_cap;
+};
+
+struct DecodeArgs {
+  CacheArgs c;
+  const uint16_t* q;
+  int32_t q_heads, group;
+  const int32_t* seq_lens;
+  const int32_t* block_idx;
+  const int32_t* num_sel;
+  int32_t n_cap, num_splits;
+  float scale_log2;            // sm_scale * log2(e)
+  float* out;                  // [B, Hq, D]
+  float* lse;                  // [B, Hq] or null
+  float* part_o;               // [B, Hkv, S, G, D]
+  float* part_lse;             // [B, Hkv, S, G]
+  uint32_t* counters;          // [B, Hkv]
+};
+
+struct RectifyArgs {
+  CacheArgs c;
+  const uint16_t* q_f;         // [B, Hq, f, D]
+  const uint16_t* k_f;         // [B, Hkv, f, D]
+  const uint16_t* v_f;
+  int32_t q_heads, group, f;
+  const int32_t* seq_lens;
+  int32_t max_seq_len;
+  int32_t chunk;               // keys per split
+  int32_t num_splits;          // ceil(max_seq_len / chunk)
+  float scale_log2;
+  float* out;                  // [B, Hq, f, D]
+  float* lse;                  // [B, Hq, f] or null
+  float* part_o;               // [B, Hkv, S, G*f, D]
+  float* part_lse;             // [B, Hkv, S, G*f]
+  uint32_t* counters;          // [B, Hkv, ceil(G*f / 128)]
+  int32_t refresh;
+};
+
+// Launchers: enqueue on `stream`; return the hipError_t of the launch.
+hipError_t launch_summarize(const CacheArgs& c, const int32_t* seq_lens, int32_t blk_begin,
+                            int32_t blk_end, hipStream_t stream);
+hipError_t launch_summarize_tail(const CacheArgs& c, const int32_t* seq_lens, int32_t f,
+                                 hipStream_t stream);
+hipError_t launch_append(const CacheArgs& c, const uint16_t* k_new, const uint16_t* v_new,
+                         int32_t* seq_lens, hipStream_t stream);
+hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
+hipError_t launch_rectify(const RectifyArgs& a, hipStream_t stream);
+hipError_t launch_clear(void* p, size_t bytes, hipStream_t stream);
+
+// Split-count and chunk heuristics (host).
+int32_t decode_auto_splits(int32_t batch, int32_t kv_heads, int32_t n_cap, int32_t block_size);
+int32_t rectify_num_qblocks(int32_t group, int32_t f);
+int32_t rectify_chunk(int32_t batch, int32_t kv_heads, int32_t nqblk, int32_t max_seq_len);
+
+}  // namespace resa

@@ -1,0 +1,357 @@
+"""GPU parity of every step of the ReSA decode path against the CPU oracle.
+
+All calls go through the C ABI (via the ctypes binding). Bars: summaries and
+indices bit-exact (selection up to documented near-ties, |score - threshold|
+<= 1e-3), attention outputs and lse within 2e-3 absolute (bf16 in, fp32
+accumulate).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2506_04108_amd as R
+import workloads as W
+from gpu_util import SENTINEL, dev, down, i32, make_cache, oracle_summaries, padded_idx, up
+from oracle.compare import check_selection, max_abs_err
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-3
+
+
+def small(g=4, b=16, L=1000, cap=1024, B=2, H=2, tag="t", **kw):
+    return W.TINY_4K.with_(batch=B, num_kv_heads=H, num_q_heads=g * H, seq_len=L, block_size=b,
+                           seed_tag=f"{tag}-{g}-{b}-{L}", **kw), cap
+
+
+# ------------------------------------------------------------------ summaries
+
+@pytest.mark.parametrize("b", [16, 32, 64])
+def test_summarize_bitexact(b):
+    w, cap = small(b=b, tag="sum")
+    lens = [1000, 777]
+    K, V = W.kv_cache(w, capacity=cap)
+    cache = make_cache(K, V, b)
+    R.block_summarize(cache, i32(lens))
+    torch.cuda.synchronize()
+    gmin, gmax = down(cache.kmin), down(cache.kmax)
+    ref = oracle_summaries(O.bf16_to_f64(K), lens, b)
+    for (bi, hi), (mn, mx) in ref.items():
+        M = mn.shape[0]
+        assert np.array_equal(O.bf16_to_f64(gmin[bi, hi, :M]), mn)
+        assert np.array_equal(O.bf16_to_f64(gmax[bi, hi, :M]), mx)
+        assert np.all(gmin[bi, hi, M:] == SENTINEL) and np.all(gmax[bi, hi, M:] == SENTINEL)
+
+
+def test_summarize_range_only():
+    w, cap = small(tag="sumr")
+    lens = [1000, 100]
+    K, V = W.kv_cache(w, capacity=cap)
+    cache = make_cache(K, V, 16)
+    R.block_summarize(cache, i32(lens), 3, 10)
+    torch.cuda.synchronize()
+    gmin = down(cache.kmin)
+    ref = oracle_summaries(O.bf16_to_f64(K), lens, 16)
+    for bi, M in ((0, 63), (1, 7)):
+        mn = ref[bi, 0][0]
+        assert np.array_equal(O.bf16_to_f64(gmin[bi, 0, 3:min(10, M)]), mn[3:min(10, M)])
+        assert np.all(gmin[bi, 0, :3] == SENTINEL)
+        assert np.all(gmin[bi, 0, min(10, M):] == SENTINEL)
+
+
+# --------------------------------------------------------------------- append
+
+def test_append_incremental_summaries():
+    w, cap = small(L=100, cap=256, tag="app")
+    lens = [100, 93]
+    K, V = W.kv_cache(w, capacity=cap)
+    cache = make_cache(K, V, 16, sentinel=False)
+    lt = i32(lens)
+    R.block_summarize(cache, lt)
+    st = O.DecodeState(O.bf16_to_f64(K), O.bf16_to_f64(V), lens, 16)
+    for step in range(40):
+        kn, vn = W.decode_kv(w, step)
+        R.append_kv(cache, up(kn), up(vn), lt, max(st.L))
+        st.append(O.bf16_to_f64(kn), O.bf16_to_f64(vn))
+    torch.cuda.synchronize()
+    assert lt.cpu().tolist() == st.L == [140, 133]
+    assert np.array_equal(O.bf16_to_f64(down(cache.k)), st.K)
+    assert np.array_equal(O.bf16_to_f64(down(cache.v)), st.V)
+    gmin, gmax = O.bf16_to_f64(down(cache.kmin)), O.bf16_to_f64(down(cache.kmax))
+    for bi in range(2):
+        M = O.num_blocks(st.L[bi], 16)
+        assert np.array_equal(gmin[bi, :, :M], st.kmin[bi, :, :M])
+        assert np.array_equal(gmax[bi, :, :M], st.kmax[bi, :, :M])
+
+
+def test_append_full_cache_is_left_alone():
+    w, cap = small(L=64, cap=64, B=1, tag="full")
+    K, V = W.kv_cache(w, capacity=cap)
+    cache = make_cache(K, V, 16, sentinel=False)
+    lt = i32([64])
+    kn, vn = W.decode_kv(w, 0)
+    with pytest.raises(R.ResaError):
+        R.append_kv(cache, up(kn[:1]), up(vn[:1]), lt, 64)
+    # A host bound below the device length: the kernel itself refuses to write.
+    R.append_kv(cache, up(kn[:1]), up(vn[:1]), lt, 10)
+    torch.cuda.synchronize()
+    assert lt.cpu().tolist() == [64]
+    assert np.array_equal(down(cache.k), K)
+
+
+# ------------------------------------------------------------------ selection
+
+def run_select(w, cap, lens, q, scores=True, sparsity=None, min_blocks=None, K=None, V=None):
+    if K is None:
+        K, V = W.kv_cache(w, capacity=cap)
+    cache = make_cache(K, V, w.block_size)
+    lt = i32(lens)
+    R.block_summarize(cache, lt)
+    s = w.sparsity if sparsity is None else sparsity
+    nm = w.min_blocks if min_blocks is None else min_blocks
+    mseq = -(-max(lens) // w.block_size)
+    sc = torch.full((w.batch, w.num_kv_heads, mseq), float("nan"), device=dev()) if scores else None
+    idx, ns = R.select_blocks(cache, up(q), lt, max(lens), s, nm, w.n_local, scores_out=sc)
+    torch.cuda.synchronize()
+    st = O.DecodeState(O.bf16_to_f64(K), O.bf16_to_f64(V), lens, w.block_size)
+    ref_s, ref_i, ref_n = st.select(O.bf16_to_f64(q), s, nm, w.n_local)
+    return cache, idx.cpu().numpy(), ns.cpu().numpy(), (sc.cpu().numpy() if scores else None), \
+        ref_s, ref_i, ref_n, st
+
+
+@pytest.mark.parametrize("b", [16, 32, 64])
+def test_select_vs_oracle_tiny4k(b):
+    w = W.TINY_4K.with_(block_size=b, min_tokens=64 * b)
+    q = W.decode_query(w)
+    _, gi, gn, gs, rs, ri, rn, _ = run_select(w, 4096, [4096], q)
+    swaps = 0
+    for hi in range(w.num_kv_heads):
+        M = O.num_blocks(4096, b)
+        assert gn[0, hi] == rn[0, hi] == O.num_selected(M, w.sparsity, w.min_blocks, 1)
+        assert max_abs_err(gs[0, hi, :M], rs[0, hi]) <= 1e-3
+        swaps += check_selection(gi[0, hi, :gn[0, hi]], ri[0, hi], rs[0, hi], rn[0, hi], 1)
+        assert np.all(gi[0, hi, gn[0, hi]:] == -1)
+    assert swaps <= 2
+
+
+def test_select_ragged_batch_and_sparsities():
+    w, cap = small(g=7, L=3000, cap=3072, B=3, H=2, tag="selr")
+    lens = [3000, 17, 2049]
+    q = W.decode_query(w)
+    for s, nm in ((0.8, 4), (0.95, 0), (0.0, 0), (1.0, 2)):
+        _, gi, gn, gs, rs, ri, rn, _ = run_select(w, cap, lens, q, sparsity=s, min_blocks=nm)
+        for bi in range(3):
+            for hi in range(2):
+                M = O.num_blocks(lens[bi], 16)
+                assert gn[bi, hi] == rn[bi, hi]
+                assert max_abs_err(gs[bi, hi, :M], rs[bi, hi]) <= 1e-3
+                check_selection(gi[bi, hi, :gn[bi, hi]], ri[bi, hi], rs[bi, hi], rn[bi, hi], 1)
+
+
+def test_select_exact_ties():
+    """Small-integer keys and dyadic queries make every score exact in fp32 and
+    float64, with many exact ties: the sets must then match bit for bit,
+    including the lowest-id tie-break."""
+    w, cap = small(g=4, L=2000, cap=2048, B=2, H=2, tag="ties")
+    rng = np.random.default_rng(7)
+    Kf = rng.integers(-2, 3, size=(2, 2, cap, 128)).astype(np.float32)
+    Vf = rng.standard_normal((2, 2, cap, 128)).astype(np.float32)
+    qf = rng.integers(-1, 2, size=(2, 8, 128)).astype(np.float32)
+    K, V, q = W.f32_to_bf16_bits(Kf), W.f32_to_bf16_bits(Vf), W.f32_to_bf16_bits(qf)
+    lens = [2000, 1500]
+    _, gi, gn, gs, rs, ri, rn, _ = run_select(w, cap, lens, q, sparsity=0.9, min_blocks=3, K=K, V=V)
+    for bi in range(2):
+        for hi in range(2):
+            M = O.num_blocks(lens[bi], 16)
+            assert np.array_equal(gs[bi, hi, :M].astype(np.float64), rs[bi, hi])
+            assert len(set(rs[bi, hi].tolist())) < M // 2  # plenty of exact ties
+            assert list(gi[bi, hi, :gn[bi, hi]]) == list(ri[bi, hi])
+
+
+def test_select_planted_blocks_win():
+    w = W.TINY_4K.with_(plant_norm=math.sqrt(128), seed_tag="strong")
+    q = W.decode_query(w)
+    _, gi, gn, *_ = run_select(w, 4096, [4096], q, scores=False)
+    for hi in range(w.num_kv_heads):
+        planted = set(W.planted_blocks(w, 0, hi).tolist())
+        assert planted <= set(gi[0, hi, :gn[0, hi]].tolist())
+
+
+# --------------------------------------------------------------------- decode
+
+def oracle_select_idx(w, K64, lens, q, sparsity, min_blocks):
+    st = O.DecodeState(K64, K64, lens, w.block_size)  # values unused for selection
+    _, ri, rn = st.select(O.bf16_to_f64(q), sparsity, min_blocks, w.n_local)
+    return ri
+
+
+@pytest.mark.parametrize("g", [1, 4, 7, 8])
+@pytest.mark.parametrize("b", [16, 32, 64])
+@pytest.mark.parametrize("splits", [0, 1, 5])
+def test_decode_on_oracle_blocks(g, b, splits):
+    w, cap = small(g=g, b=b, tag="dec")
+    lens = [1000, 777]
+    K, V = W.kv_cache(w, capacity=cap)
+    q = W.decode_query(w)
+    K64, V64 = O.bf16_to_f64(K), O.bf16_to_f64(V)
+    ri = oracle_select_idx(w, K64, lens, q, 0.8, 4)
+    n_cap = max(len(v) for v in ri.values()) + 3
+    idx, ns = padded_idx(ri, 2, 2, n_cap)
+    cache = make_cache(K, V, b)
+    out, lse = R.sparse_decode(cache, up(q), i32(lens), i32(idx), i32(ns), num_splits=splits)
+    torch.cuda.synchronize()
+    st = O.DecodeState(K64, V64, lens, b)
+    ref_o, ref_l = st.attend(O.bf16_to_f64(q), ri, w.sm_scale)
+    assert max_abs_err(out.cpu().numpy(), ref_o) <= TOL
+    assert max_abs_err(lse.cpu().numpy(), ref_l) <= TOL
+
+
+def test_decode_all_blocks_is_dense():
+    w, cap = small(g=4, tag="dense")
+    lens = [1000, 777]
+    K, V = W.kv_cache(w, capacity=cap)
+    q = W.decode_query(w)
+    all_idx = {(bi, hi): list(range(O.num_blocks(lens[bi], 16))) for bi in range(2) for hi in range(2)}
+    idx, ns = padded_idx(all_idx, 2, 2, 63)
+    cache = make_cache(K, V, 16)
+    out, lse = R.sparse_decode(cache, up(q), i32(lens), i32(idx), i32(ns))
+    torch.cuda.synchronize()
+    K64, V64, q64 = O.bf16_to_f64(K), O.bf16_to_f64(V), O.bf16_to_f64(q)
+    for bi in range(2):
+        for hi in range(2):
+            ro, rl = O.dense_attend(q64[bi, 4 * hi:4 * hi + 4], K64[bi, hi], V64[bi, hi], lens[bi],
+                                    w.sm_scale)
+            assert max_abs_err(out[bi, 4 * hi:4 * hi + 4].cpu().numpy(), ro) <= TOL
+            assert max_abs_err(lse[bi, 4 * hi:4 * hi + 4].cpu().numpy(), rl) <= TOL
+
+
+def test_decode_edge_cases():
+    """Empty selection, a single valid token, unsorted ids, ids out of range,
+    and more splits than chunks (empty splits)."""
+    w, cap = small(g=4, L=40, cap=64, B=4, H=1, tag="edge")
+    lens = [40, 1, 33, 40]
+    K, V = W.kv_cache(w, capacity=cap, garbage=1e4)
+    q = W.decode_query(w)
+    ids = {(0, 0): [], (1, 0): [0], (2, 0): [2, 0], (3, 0): [1, 7, -1, 2]}
+    idx, ns = padded_idx(ids, 4, 1, 4)
+    cache = make_cache(K, V, 16)
+    out, lse = R.sparse_decode(cache, up(q), i32(lens), i32(idx), i32(ns), num_splits=9)
+    torch.cuda.synchronize()
+    o, l = out.cpu().numpy(), lse.cpu().numpy()
+    K64, V64, q64 = O.bf16_to_f64(K), O.bf16_to_f64(V), O.bf16_to_f64(q)
+    assert np.all(o[0] == 0) and np.all(np.isneginf(l[0]))
+    assert max_abs_err(o[1], np.repeat(V64[1, 0, :1], 4, axis=0)) <= 1e-6
+    ro, rl = O.sparse_attend(q64[2], K64[2, 0], V64[2, 0], 33, [0, 2], 16, w.sm_scale)
+    assert max_abs_err(o[2], ro) <= TOL and max_abs_err(l[2], rl) <= TOL
+    ro, rl = O.sparse_attend(q64[3], K64[3, 0], V64[3, 0], 40, [1, 2], 16, w.sm_scale)
+    assert max_abs_err(o[3], ro) <= TOL and max_abs_err(l[3], rl) <= TOL
+
+
+def test_decode_deterministic():
+    w, cap = small(g=4, tag="det")
+    lens = [1000, 999]
+    K, V = W.kv_cache(w, capacity=cap)
+    q = W.decode_query(w)
+    cache = make_cache(K, V, 16)
+    lt = i32(lens)
+    R.block_summarize(cache, lt)
+    idx, ns = R.select_blocks(cache, up(q), lt, 1000, 0.9, 4, 1)
+    a, la = R.sparse_decode(cache, up(q), lt, idx, ns)
+    idx2, ns2 = R.select_blocks(cache, up(q), lt, 1000, 0.9, 4, 1)
+    b, lb = R.sparse_decode(cache, up(q), lt, idx2, ns2)
+    torch.cuda.synchronize()
+    assert torch.equal(idx, idx2) and torch.equal(a, b) and torch.equal(la, lb)
+
+
+# -------------------------------------------------------------------- rectify
+
+@pytest.mark.parametrize("g,f", [(4, 16), (4, 1), (7, 32), (8, 32), (2, 64)])
+def test_rectify_vs_oracle(g, f):
+    w, cap = small(g=g, L=300, cap=320, tag="rect")
+    lens = [300, 257]
+    K, V = W.kv_cache(w, capacity=cap)
+    K0 = K.copy()
+    cache = make_cache(K, V, 16, sentinel=False)
+    lt = i32(lens)
+    R.block_summarize(cache, lt)
+    base_k = np.stack([np.stack([K[bi, hi, lens[bi] - f:lens[bi]] for hi in range(2)]) for bi in range(2)])
+    base_v = np.stack([np.stack([V[bi, hi, lens[bi] - f:lens[bi]] for hi in range(2)]) for bi in range(2)])
+    qf, kf, vf = W.rectify_inputs(w, 3, base_k, base_v, f)
+    out, lse = R.dense_rectify(cache, up(qf), up(kf), up(vf), lt, 300)
+    torch.cuda.synchronize()
+    st = O.DecodeState(O.bf16_to_f64(K), O.bf16_to_f64(V), lens, 16)
+    ro, rl = st.rectify(O.bf16_to_f64(qf), O.bf16_to_f64(kf), O.bf16_to_f64(vf), f, w.sm_scale)
+    assert max_abs_err(out.cpu().numpy(), ro) <= TOL
+    assert max_abs_err(lse.cpu().numpy(), rl) <= TOL
+    gk = down(cache.k)
+    for bi in range(2):
+        L = lens[bi]
+        assert np.array_equal(gk[bi, :, L - f:L], kf[bi])
+        assert np.array_equal(gk[bi, :, :L - f], K0[bi, :, :L - f])
+        assert np.array_equal(gk[bi, :, L:], K0[bi, :, L:])
+        M = O.num_blocks(L, 16)
+        assert np.array_equal(O.bf16_to_f64(down(cache.kmin)[bi, :, :M]), st.kmin[bi, :, :M])
+        assert np.array_equal(O.bf16_to_f64(down(cache.kmax)[bi, :, :M]), st.kmax[bi, :, :M])
+
+
+def test_rectify_tiny4k_full():
+    """The tiny 4K layer: f = 16 rows, causal over the whole 4096 cache."""
+    w = W.TINY_4K
+    K, V = W.kv_cache(w)
+    cache = make_cache(K, V, 16, sentinel=False)
+    lt = i32([4096])
+    R.block_summarize(cache, lt)
+    qf, kf, vf = W.rectify_inputs(w, 0, K[:, :, 4080:], V[:, :, 4080:], 16)
+    out, lse = R.dense_rectify(cache, up(qf), up(kf), up(vf), lt, 4096)
+    torch.cuda.synchronize()
+    st = O.DecodeState(O.bf16_to_f64(K), O.bf16_to_f64(V), [4096], 16)
+    ro, rl = st.rectify(O.bf16_to_f64(qf), O.bf16_to_f64(kf), O.bf16_to_f64(vf), 16, w.sm_scale)
+    assert max_abs_err(out.cpu().numpy(), ro) <= TOL
+    assert max_abs_err(lse.cpu().numpy(), rl) <= TOL
+
+
+# ---------------------------------------------------------------- decode loop
+
+def test_decode_loop_small():
+    """Kernel-level Alg. 1 loop (append, select, decode; rectify every f steps)
+    on a reduced copy of the 64K batch-8 workload (outlier key channels)."""
+    w = W.LONG_64K.with_(batch=2, num_q_heads=8, num_kv_heads=2, seq_len=600, min_tokens=64,
+                         seed_tag="loop")
+    f, steps, cap = 16, 40, 704
+    K, V = W.kv_cache(w, capacity=cap)
+    cache = make_cache(K, V, 16, sentinel=False)
+    lens = [600, 555]
+    lt = i32(lens)
+    R.block_summarize(cache, lt)
+    st = O.DecodeState(O.bf16_to_f64(K), O.bf16_to_f64(V), lens, 16)
+    swaps = 0
+    for step in range(steps):
+        kn, vn = W.decode_kv(w, step)
+        q = W.decode_query(w, step)
+        R.append_kv(cache, up(kn), up(vn), lt, max(st.L))
+        st.append(O.bf16_to_f64(kn), O.bf16_to_f64(vn))
+        idx, ns = R.select_blocks(cache, up(q), lt, max(st.L), w.sparsity, w.min_blocks, 1)
+        out, _ = R.sparse_decode(cache, up(q), lt, idx, ns)
+        rs, ri, rn = st.select(O.bf16_to_f64(q), w.sparsity, w.min_blocks, 1)
+        ro, _ = st.attend(O.bf16_to_f64(q), ri, w.sm_scale)
+        gi, gn, go = idx.cpu().numpy(), ns.cpu().numpy(), out.cpu().numpy()
+        for bi in range(2):
+            for hi in range(2):
+                s = check_selection(gi[bi, hi, :gn[bi, hi]], ri[bi, hi], rs[bi, hi], rn[bi, hi], 1)
+                swaps += s
+                if s == 0:
+                    assert max_abs_err(go[bi, 4 * hi:4 * hi + 4], ro[bi, 4 * hi:4 * hi + 4]) <= TOL
+        if (step + 1) % f == 0:
+            # The window is the f rows appended since the last rectification.
+            rows = [W.decode_kv(w, s) for s in range(step - f + 1, step + 1)]
+            lastk = np.stack([r[0] for r in rows], axis=2)
+            lastv = np.stack([r[1] for r in rows], axis=2)
+            qf, kf, vf = W.rectify_inputs(w, step, lastk, lastv, f)
+            rout, _ = R.dense_rectify(cache, up(qf), up(kf), up(vf), lt, max(st.L))
+            rr, _ = st.rectify(O.bf16_to_f64(qf), O.bf16_to_f64(kf), O.bf16_to_f64(vf), f, w.sm_scale)
+            assert max_abs_err(rout.cpu().numpy(), rr) <= TOL
+    torch.cuda.synchronize()
+    assert lt.cpu().tolist() == st.L
+    assert swaps <= 4
