@@ -1,0 +1,332 @@
+"""Benchmark of the ReSA decode hot path on one MI355X.
+
+A step is one decode token of one attention layer for the whole batch:
+append the token's K/V (online block-summary update), select blocks (pooled
+query, Quest score, top-n) and run block-sparse flash-decoding; every f-th
+step of a layer also runs the dense rectification of its last f rows. The
+default workload is the 64K batch-8 decode loop (32 query / 8 kv heads,
+head_dim 128, block 16, sparsity 0.9 with a 2048-token minimum, f = 32,
+LogNormal(0, 0.5) key channels). Steps cycle through `--layers` independent
+layer caches, as a model's layers do, so data reused from one step to the
+next cannot be served by the 256 MB last-level cache.
+
+Prints one JSON line. Per-phase kernel times come from HIP events recorded on
+the launch stream; the sparse-decode roofline uses the bytes of the selected
+K/V blocks per launch.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import hashlib
+import json
+import math
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "sparse decode µs/step + achieved HBM GB/s (% roofline) at 64K/256K ctx"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=128)
+    p.add_argument("--warmup", type=int, default=32)
+    p.add_argument("--workload", default="long_64k",
+                   choices=["long_64k", "extreme_256k", "qwen7b_32k", "tiny_4k", "sweep_64k"])
+    p.add_argument("--layers", type=int, default=4)
+    p.add_argument("--block-size", type=int, default=None)
+    p.add_argument("--sparsity", type=float, default=None)
+    p.add_argument("--rectify-every", type=int, default=None)
+    p.add_argument("--dense", action="store_true", help="dense baseline: decode over every block")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work")
+    return p.parse_args()
+
+
+def workload_of(args):
+    import workloads as W
+    w = W.WORKLOADS[args.workload]
+    kw = {}
+    if args.block_size:
+        kw["block_size"] = args.block_size
+    if args.sparsity is not None:
+        kw["sparsity"] = args.sparsity
+    if args.rectify_every:
+        kw["rectify_every"] = args.rectify_every
+    return w.with_(**kw) if kw else w
+
+
+def describe(w, layers, dense):
+    return (f"{w.name}: batch {w.batch}, {w.num_q_heads} query / {w.num_kv_heads} kv heads, "
+            f"head_dim {w.head_dim}, context {w.seq_len} growing by one token per step, "
+            f"block {w.block_size}, " + ("dense (all blocks)" if dense else
+                                          f"sparsity {w.sparsity} with a {w.min_tokens}-token minimum, ")
+            + f"rectify every {w.rectify_every} steps, {layers} layer caches in rotation")
+
+
+def traffic_from_profile(kernel_src: str):
+    """HBM bytes per decode launch measured by rocprofv3 PMC counters, if the
+    committed profile was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "sparse_decode_long64k_pmc.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"source_sha256:\s*([0-9a-f]{64})", text)
+    t = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m or not t:
+        return None
+    cur = hashlib.sha256(open(kernel_src, "rb").read()).hexdigest()
+    return float(t.group(1)) if m.group(1) == cur else None
+
+
+def cpu_baseline(w, budget_s):
+    """The oracle timed on host cores on a bounded sample of the same workload."""
+    import numpy as np
+    import oracle as O
+    import workloads as W
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = 1
+    groups = w.batch * w.num_kv_heads
+    g = w.group_size
+    f = w.rectify_every
+    t_step = []
+    t_rect = []
+    t0 = time.perf_counter()
+    sampled = 0
+    for gi in range(groups):
+        bi, hi = divmod(gi, w.num_kv_heads)
+        k, v = W.group_kv(w, bi, hi)
+        cap = w.seq_len + f + 1
+        K = np.zeros((1, 1, cap, w.head_dim))
+        V = np.zeros((1, 1, cap, w.head_dim))
+        K[0, 0, :w.seq_len] = O.bf16_to_f64(k)
+        V[0, 0, :w.seq_len] = O.bf16_to_f64(v)
+        st = O.DecodeState(K, V, [w.seq_len], w.block_size)
+        q = O.bf16_to_f64(W.decode_query(w, 0))[bi:bi + 1, hi * g:(hi + 1) * g]
+        kn, vn = W.decode_kv(w, 0)
+        a = time.perf_counter()
+        st.append(O.bf16_to_f64(kn)[bi:bi + 1, hi:hi + 1], O.bf16_to_f64(vn)[bi:bi + 1, hi:hi + 1])
+        _, idx, _ = st.select(q, w.sparsity, w.min_blocks, w.n_local)
+        st.attend(q, idx, w.sm_scale)
+        t_step.append(time.perf_counter() - a)
+        if gi == 0:
+            qf = np.random.default_rng(0).standard_normal((1, g, f, w.head_dim))
+            kf = st.K[0:1, 0:1, st.L[0] - f:st.L[0]]
+            a = time.perf_counter()
+            st.rectify(qf, kf, st.V[0:1, 0:1, st.L[0] - f:st.L[0]], f, w.sm_scale)
+            t_rect.append(time.perf_counter() - a)
+        sampled += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    per_group_step = sum(t_step) / len(t_step)
+    per_group_rect = sum(t_rect) / len(t_rect)
+    us = (per_group_step + per_group_rect / f) * groups * 1e6
+    return {"value": round(us, 1), "unit": "us/step", "cores": cores, "kind": "oracle",
+            "sample": (f"{sampled} of {groups} (batch, kv-head) groups at full context: one decode "
+                       f"step each (append, select, sparse attend) plus one rectification of "
+                       f"{f} rows amortised over {f} steps, scaled to all {groups} groups")}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no "
+              "multi-GPU path.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2506_04108_amd as R
+    from paper_2506_04108_amd._lib import KVCacheDesc, SelectParams, check, lib
+    import workloads.device as WD
+
+    w = workload_of(args)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    L0, B, H, Hq, D, b = w.seq_len, w.batch, w.num_kv_heads, w.num_q_heads, w.head_dim, w.block_size
+    f = w.rectify_every
+    nlay = max(1, args.layers)
+    total = args.warmup + args.steps
+    per_layer = -(-total // nlay)
+    cap = L0 + per_layer + b
+    cap = -(-cap // b) * b
+    stream = torch.cuda.current_stream()
+    sptr = stream.cuda_stream
+    lb = lib()
+
+    log(f"[bench] {describe(w, nlay, args.dense)}; capacity {cap}")
+    t_gen = time.perf_counter()
+    layers = []
+    for li in range(nlay):
+        K, V, scale = WD.caches(w, cap, li, dev)
+        mb = cap // b
+        cache = R.KVCache(K, V, torch.empty((B, H, mb, D), dtype=torch.bfloat16, device=dev),
+                          torch.empty((B, H, mb, D), dtype=torch.bfloat16, device=dev), b)
+        lens = torch.full((B,), L0, dtype=torch.int32, device=dev)
+        R.block_summarize(cache, lens)
+        q, k, v = WD.step_inputs(w, per_layer, li, scale, dev)
+        layers.append(dict(cache=cache, desc=cache.desc(), lens=lens, q=q, k=k, v=v, steps=0))
+    torch.cuda.synchronize()
+    log(f"[bench] inputs ready in {time.perf_counter() - t_gen:.1f}s")
+
+    mcap = cap // b
+    if args.dense:
+        n_cap = mcap
+    else:
+        n_cap = R.num_selected(mcap, w.sparsity, w.min_blocks, w.n_local)
+    idx = torch.empty((B, H, n_cap), dtype=torch.int32, device=dev)
+    nsel = torch.empty((B, H), dtype=torch.int32, device=dev)
+    out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
+    lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+    splits = R.decode_num_splits(B, H, n_cap, b)
+    ws_sel = torch.zeros(max(lb.resa_select_workspace_size(B, H, cap, b, 0), 256), dtype=torch.uint8,
+                         device=dev)
+    ws_dec = torch.zeros(lb.resa_decode_workspace_size(B, H, Hq, n_cap, b, splits), dtype=torch.uint8,
+                         device=dev)
+    ws_rec = torch.zeros(lb.resa_rectify_workspace_size(B, H, Hq, f, cap), dtype=torch.uint8, device=dev)
+    rout = torch.empty((B, Hq, f, D), dtype=torch.float32, device=dev)
+    params = SelectParams(w.sparsity, w.min_blocks, w.n_local)
+    sm = 1.0 / math.sqrt(D)
+
+    # Dense baseline: every block id in order, count = M (decode only).
+    if args.dense:
+        all_idx = torch.arange(n_cap, dtype=torch.int32, device=dev).repeat(B, H, 1).contiguous()
+
+    # Rectification rows are prepared ahead (inputs, not timed work).
+    rect_inputs = {}
+    for li, ly in enumerate(layers):
+        for s in range(f, per_layer + 1, f):
+            lo = s - f
+            k_last = ly["k"][lo:s].permute(1, 2, 0, 3).contiguous()
+            v_last = ly["v"][lo:s].permute(1, 2, 0, 3).contiguous()
+            rect_inputs[li, s] = WD.rectify_rows(w, k_last, v_last, f, 100 * li + s, dev)
+    torch.cuda.synchronize()
+
+    ev = {k: [] for k in ("append", "select", "decode", "rectify")}
+
+    def mark(name):
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        ev[name].append(e)
+
+    def step(timed: bool):
+        li = step.count % nlay
+        step.count += 1
+        ly = layers[li]
+        s = ly["steps"]
+        Lcur = L0 + s
+        d = C.byref(ly["desc"])
+        if timed:
+            mark("append")
+        check(lb.resa_append_kv(d, ly["k"][s].data_ptr(), ly["v"][s].data_ptr(), ly["lens"].data_ptr(),
+                                Lcur, sptr))
+        if timed:
+            mark("append")
+        if args.dense:
+            M = -(-(Lcur + 1) // b)
+            nsel.fill_(M)
+            ids = all_idx
+        else:
+            if timed:
+                mark("select")
+            check(lb.resa_select_blocks(d, ly["q"][s].data_ptr(), Hq, ly["lens"].data_ptr(), Lcur + 1,
+                                        C.byref(params), idx.data_ptr(), nsel.data_ptr(), n_cap, None,
+                                        ws_sel.data_ptr(), ws_sel.numel(), sptr))
+            if timed:
+                mark("select")
+            ids = idx
+        if timed:
+            mark("decode")
+        check(lb.resa_sparse_decode(d, ly["q"][s].data_ptr(), Hq, ly["lens"].data_ptr(), ids.data_ptr(),
+                                    nsel.data_ptr(), n_cap, splits, sm, out.data_ptr(), lse.data_ptr(),
+                                    ws_dec.data_ptr(), ws_dec.numel(), sptr))
+        if timed:
+            mark("decode")
+        ly["steps"] = s + 1
+        if not args.dense and (s + 1) % f == 0:
+            qf, kf, vf = rect_inputs[li, s + 1]
+            if timed:
+                mark("rectify")
+            check(lb.resa_dense_rectify(d, qf.data_ptr(), kf.data_ptr(), vf.data_ptr(), Hq, f,
+                                        ly["lens"].data_ptr(), Lcur + 1, sm, rout.data_ptr(), None, 1,
+                                        ws_rec.data_ptr(), ws_rec.numel(), sptr))
+            if timed:
+                mark("rectify")
+        return Lcur + 1
+
+    step.count = 0
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    lens_seen = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        lens_seen.append(step(True))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    def durations(name):
+        e = ev[name]
+        return [e[i].elapsed_time(e[i + 1]) * 1e3 for i in range(0, len(e), 2)]  # us
+
+    ph = {k: durations(k) for k in ev}
+    # Algorithmic bytes of each decode launch: the selected blocks' K and V rows.
+    bytes_dec = []
+    for L in lens_seen:
+        M = -(-L // b)
+        n = M if args.dense else R.num_selected(M, w.sparsity, w.min_blocks, w.n_local)
+        bytes_dec.append(B * H * n * b * D * 2 * 2)
+    dec_us = ph["decode"]
+    avg_dec_us = sum(dec_us) / len(dec_us)
+    avg_bytes = sum(bytes_dec) / len(bytes_dec)
+    achieved = avg_bytes / (avg_dec_us * 1e-6) / 1e9
+    kernel_src = os.path.join(ROOT, "paper_2506_04108_amd", "csrc", "decode.hip")
+    traffic = traffic_from_profile(kernel_src)
+    ms_per_step = wall * 1e3 / args.steps
+    phase_us = {k: round(sum(v) / args.steps, 2) for k, v in ph.items() if v}
+    res = {
+        "metric": METRIC,
+        "value": round(ms_per_step * 1e3, 2),
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": describe(w, nlay, args.dense), "batch": B, "q_heads": Hq, "kv_heads": H,
+                   "head_dim": D, "context_start": L0, "block_size": b,
+                   "sparsity": None if args.dense else w.sparsity, "min_tokens": w.min_tokens,
+                   "rectify_every": f, "decode_splits": splits, "layers_rotated": nlay},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "kernel": "k_decode",
+                     "avg_launch_us": round(avg_dec_us, 3), "bytes_per_launch": int(avg_bytes)},
+        "phases_us_per_step": phase_us,
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        res["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -28,7 +28,8 @@
  *   message (per host thread). Argument checks run before any HIP call, so a
  *   rejected call touches neither the device nor the stream.
  * - Data types: bf16 caches and queries (uint16 bit patterns), fp32 outputs,
- *   int32 lengths and indices. All pointers must be 16-byte aligned.
+ *   int32 lengths and indices. bf16 tensors, workspaces and the rectify
+ *   output must be 16-byte aligned; other int32/fp32 arrays 4-byte aligned.
  * - Supported shapes: head_dim 128; block_size 16, 32 or 64; capacity a
  *   multiple of block_size; 1 <= num_q_heads / num_kv_heads <= 8.
  * - Layouts (row-major, last index fastest):
@@ -77,7 +78,7 @@ typedef struct resa_kv_cache {
 
 /* Block-selection parameters (Sec. 2.1, Eq. 5). */
 typedef struct resa_select_params {
-  double sparsity;      /* s in [0, 1): share of blocks skipped; keep = 1 - s.
+  double sparsity;      /* s in [0, 1]: share of blocks skipped; keep = 1 - s.
                            Rounded to the nearest multiple of 1e-6. */
   int32_t min_blocks;   /* n_min >= 0: minimum number of selected blocks */
   int32_t n_local;      /* >= 0: most recent blocks always selected */
@@ -94,7 +95,7 @@ const char* resa_last_error(void);
  *   n = min(M, max(min_blocks, n_local, ceil(M * (1 - sparsity))))
  * in exact integer arithmetic on sparsity rounded to 1e-6; 0 when M == 0.
  * The device-side selection uses the same arithmetic. Host only, no device
- * access. Returns -1 for invalid arguments (M < 0, sparsity outside [0, 1),
+ * access. Returns -1 for invalid arguments (M < 0, sparsity outside [0, 1],
  * negative min_blocks or n_local).
  */
 int32_t resa_num_selected(int32_t num_blocks, double sparsity, int32_t min_blocks,
@@ -172,11 +173,12 @@ size_t resa_decode_workspace_size(int32_t batch, int32_t num_kv_heads,
  *   out[b, h, :] = sum_t softmax_t(q_h . K_t * sm_scale) V_t     (fp32)
  *   lse[b, h]    = log sum_t exp(q_h . K_t * sm_scale)           (optional)
  * With no token selected, out is 0 and lse is -inf. Passing every block id
- * gives dense decoding. num_splits = 0 picks resa_decode_num_splits().
- * The workspace holds split partials and one merge counter per group: it
- * must be zero-filled before its first use (resa_workspace_clear) and every
- * call leaves the counters at zero again. Calls that share a workspace must
- * be ordered on one stream.
+ * gives dense decoding. num_splits = 0 picks resa_decode_num_splits();
+ * explicit counts must lie in [1, 256].
+ * Runs as two kernels: the split kernel writes per-split partials into the
+ * workspace, then a combine kernel merges them (one split: one kernel). The
+ * workspace needs no initialisation; calls sharing one must be ordered on a
+ * single stream.
  */
 int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
                        const int32_t* seq_lens, const int32_t* block_idx,
@@ -200,9 +202,9 @@ size_t resa_rectify_workspace_size(int32_t batch, int32_t num_kv_heads,
  *   3. if refresh_summaries, blocks floor((L - f) / b) .. M_b - 1 are
  *      re-summarised (Eq. 3).
  * 1 <= f <= 128 and f <= max_seq_len <= capacity. max_seq_len bounds every
- * seq_lens[b] (host side, for launch sizing). The workspace holds split
- * partials and merge counters: zero-fill it before first use; every call
- * leaves the counters at zero.
+ * seq_lens[b] (host side, for launch sizing). A sequence with
+ * seq_lens[b] < f is left untouched and its out rows are 0 (lse -inf). The
+ * workspace holds split partials and needs no initialisation.
  */
 int resa_dense_rectify(const resa_kv_cache_t* c, const void* q_f, const void* k_f,
                        const void* v_f, int32_t num_q_heads, int32_t f,
@@ -210,7 +212,7 @@ int resa_dense_rectify(const resa_kv_cache_t* c, const void* q_f, const void* k_
                        float* out, float* lse, int32_t refresh_summaries,
                        void* workspace, size_t workspace_bytes, void* stream);
 
-/* Zero-fills a workspace with a kernel (safe under stream capture). */
+/* Zero-fills a workspace with a kernel (a convenience; no call requires it). */
 int resa_workspace_clear(void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus

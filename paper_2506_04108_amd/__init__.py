@@ -96,12 +96,8 @@ class KVCache:
 
 
 class Workspace:
-    """A zero-initialised device scratch buffer that grows on demand.
-
-    The decode and rectify kernels keep merge counters in their workspace and
-    leave them at zero after every call, so a buffer is cleared only when it
-    is (re)allocated.
-    """
+    """A device scratch buffer that grows on demand (one per operation kind;
+    calls sharing one must be ordered on a single stream)."""
 
     def __init__(self, device="cuda"):
         self.device = device

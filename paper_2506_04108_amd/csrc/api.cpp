@@ -99,22 +99,21 @@ int hip_fail(hipError_t e, const char* what) {
 }
 
 struct DecodeLayout {
-  size_t counters, lse, o, total;
+  size_t lse, o, total;
 };
 
 DecodeLayout decode_layout(int32_t batch, int32_t kv_heads, int32_t group, int32_t splits) {
   DecodeLayout d;
   const size_t groups = (size_t)batch * kv_heads;
-  d.counters = 0;
-  d.lse = round256(groups * 4);
-  d.o = d.lse + round256(groups * splits * group * 4);
+  d.lse = 0;
+  d.o = round256(groups * splits * group * 4);
   d.total = d.o + groups * splits * group * RESA_HEAD_DIM * 4;
   return d;
 }
 
 struct RectifyLayout {
   int32_t nq, chunk, splits;
-  size_t counters, lse, o, total;
+  size_t lse, o, total;
 };
 
 RectifyLayout rectify_layout(int32_t batch, int32_t kv_heads, int32_t group, int32_t f,
@@ -126,9 +125,8 @@ RectifyLayout rectify_layout(int32_t batch, int32_t kv_heads, int32_t group, int
   if (r.splits < 1) r.splits = 1;
   const size_t groups = (size_t)batch * kv_heads;
   const size_t rows = (size_t)group * f;
-  r.counters = 0;
-  r.lse = round256(groups * r.nq * 4);
-  r.o = r.lse + round256(groups * r.splits * rows * 4);
+  r.lse = 0;
+  r.o = round256(groups * r.splits * rows * 4);
   r.total = r.o + groups * r.splits * rows * RESA_HEAD_DIM * 4;
   return r;
 }
@@ -278,8 +276,8 @@ int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_he
   RESA_CHECK_PTR(out, 4);
   if (lse != nullptr && !aligned(lse, 4)) return fail(RESA_ERR_INVALID_ARG, "lse is not 4-byte aligned");
   if (n_cap < 0) return fail(RESA_ERR_INVALID_ARG, "n_cap %d < 0", n_cap);
-  if (num_splits < 0 || num_splits > 65535)
-    return fail(RESA_ERR_INVALID_ARG, "num_splits %d outside [0, 65535]", num_splits);
+  if (num_splits < 0 || num_splits > 256)
+    return fail(RESA_ERR_INVALID_ARG, "num_splits %d outside [0, 256]", num_splits);
   if (!std::isfinite(sm_scale)) return fail(RESA_ERR_INVALID_ARG, "sm_scale is not finite");
   const int32_t s = num_splits > 0 ? num_splits
                                    : resa::decode_auto_splits(c->batch, c->num_kv_heads, n_cap,
@@ -303,7 +301,6 @@ int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_he
   a.scale_log2 = sm_scale * 1.4426950408889634f;
   a.out = out;
   a.lse = lse;
-  a.counters = reinterpret_cast<uint32_t*>(ws + lay.counters);
   a.part_lse = reinterpret_cast<float*>(ws + lay.lse);
   a.part_o = reinterpret_cast<float*>(ws + lay.o);
   hipError_t e = resa::launch_decode(a, static_cast<hipStream_t>(stream));
@@ -358,7 +355,6 @@ int resa_dense_rectify(const resa_kv_cache_t* c, const void* q_f, const void* k_
   a.scale_log2 = sm_scale * 1.4426950408889634f;
   a.out = out;
   a.lse = lse;
-  a.counters = reinterpret_cast<uint32_t*>(ws + lay.counters);
   a.part_lse = reinterpret_cast<float*>(ws + lay.lse);
   a.part_o = reinterpret_cast<float*>(ws + lay.o);
   a.refresh = refresh_summaries ? 1 : 0;

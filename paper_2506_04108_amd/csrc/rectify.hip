@@ -16,8 +16,8 @@
 //   high part and a bf16 low part (p - hi) so the product keeps ~16 bits
 //   O^T += V^T . P^T     (dims x queries; the contraction index is ordered so
 //                          that P^T is already in the B-operand layout)
-// Splits are merged by log-sum-exp in the last workgroup to finish (ticket),
-// like the decode combine (Alg. 2).
+// A second kernel merges the splits by log-sum-exp (Alg. 2, "Combine"),
+// spread over many workgroups.
 #include "resa_device.h"
 #include "resa_internal.h"
 
@@ -33,6 +33,7 @@ constexpr int kRowsPerWg = 128;
 constexpr int kKeyTile = 32;
 constexpr int kKStride = kHeadDim + 8;  // bf16 per K row in LDS (272 B, 16-B aligned)
 constexpr int kVStride = kKeyTile + 4;  // bf16 per transposed V row in LDS (72 B)
+constexpr int kMaxRectSplits = 1024;     // splits per group (bounded by the host)
 
 __device__ __forceinline__ f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -55,11 +56,9 @@ __global__ __launch_bounds__(256) void k_rectify_rows(RectifyArgs a) {
   }
 }
 
-__global__ __launch_bounds__(256) void k_rectify_attn(RectifyArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_rectify_attn(RectifyArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t sK[kKeyTile * kKStride];
   __shared__ __attribute__((aligned(16))) uint16_t sV[kHeadDim * kVStride];
-  __shared__ uint32_t s_ticket;
-
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int split = blockIdx.x, qblk = blockIdx.y, grp = blockIdx.z;
   const int bb = grp / a.c.kv_heads, hk = grp % a.c.kv_heads;
@@ -220,36 +219,29 @@ __global__ __launch_bounds__(256) void k_rectify_attn(RectifyArgs a) {
     }
   }
 
-  __threadfence();
-  __syncthreads();
-  const size_t ctr = (size_t)grp * gridDim.y + qblk;
-  if (tid == 0) s_ticket = atomicAdd(&a.counters[ctr], 1u);
-  __syncthreads();
-  if (s_ticket != (uint32_t)(S - 1)) return;
-  __threadfence();
+}
 
-  const int r0 = qblk * kRowsPerWg;
-  const int nrows = min(R - r0, kRowsPerWg);
-  for (int o2 = tid; o2 < nrows * kHeadDim; o2 += 256) {
-    const int rho = r0 + o2 / kHeadDim, d = o2 % kHeadDim;
-    const float* pl = a.part_lse + (size_t)grp * S * R + rho;
-    float mx = ninf;
-    for (int s = 0; s < S; ++s) mx = fmaxf(mx, pl[(size_t)s * R]);
-    float wsum = 0.f, x = 0.f;
-    if (mx != ninf) {
-      for (int s = 0; s < S; ++s) {
-        const float ls = pl[(size_t)s * R];
-        const float w = ls == ninf ? 0.f : fast_exp2(ls - mx);
-        wsum += w;
-        x = fmaf(w, a.part_o[(((size_t)grp * S + s) * R + rho) * kHeadDim + d], x);
-      }
-    }
-    const int h = rho % G, r = rho / G;
-    const size_t orow = ((size_t)bb * a.q_heads + (size_t)hk * G + h) * f + r;
-    a.out[orow * kHeadDim + d] = wsum > 0.f ? x / wsum : 0.f;
-    if (d == 0 && a.lse) a.lse[orow] = wsum > 0.f ? (mx + fast_log2(wsum)) * kLn2 : ninf;
-  }
-  if (tid == 0) a.counters[ctr] = 0u;
+// Log-sum-exp merge of the splits (Alg. 2, "Combine") spread over many
+// workgroups: each takes kCombineRows query rows of one group.
+constexpr int kCombineRows = 2;
+
+__global__ __launch_bounds__(256) void k_rectify_combine(RectifyArgs a) {
+  __shared__ float s_w[kMaxRectSplits * kCombineRows];
+  __shared__ f4_t s_red[256];
+  const int grp = blockIdx.y;
+  const int bb = grp / a.c.kv_heads, hk = grp % a.c.kv_heads;
+  const int G = a.group, f = a.f, R = G * f, S = a.num_splits;
+  const int rho0 = blockIdx.x * kCombineRows;
+  const int rows = min(kCombineRows, R - rho0);
+  if (rows <= 0) return;
+  auto out_index = [&](int r) {
+    const int rho = rho0 + r;
+    return ((size_t)bb * a.q_heads + (size_t)hk * G + rho % G) * f + rho / G;
+  };
+  merge_splits(a.part_o + ((size_t)grp * S * R + rho0) * kHeadDim, (size_t)R * kHeadDim,
+               a.part_lse + (size_t)grp * S * R + rho0, (size_t)R, S, rows, s_w, s_red,
+               [&](int r) { return a.out + out_index(r) * kHeadDim; },
+               [&](int r, float v) { if (a.lse) a.lse[out_index(r)] = v; });
 }
 
 }  // namespace
@@ -265,6 +257,9 @@ int32_t rectify_chunk(int32_t batch, int32_t kv_heads, int32_t nqblk, int32_t ma
   int64_t chunk = (max_seq_len + target - 1) / target;
   chunk = (chunk + kKeyTile - 1) / kKeyTile * kKeyTile;
   if (chunk < 512) chunk = 512;
+  // At most kMaxRectSplits splits, so the combine's weights fit in LDS.
+  const int64_t least = ((int64_t)max_seq_len + kMaxRectSplits - 1) / kMaxRectSplits;
+  if (chunk < least) chunk = (least + kKeyTile - 1) / kKeyTile * kKeyTile;
   return (int32_t)chunk;
 }
 
@@ -279,6 +274,11 @@ hipError_t launch_rectify(const RectifyArgs& a, hipStream_t stream) {
   const int32_t nq = rectify_num_qblocks(a.group, a.f);
   hipLaunchKernelGGL(k_rectify_attn, dim3(a.num_splits, nq, a.c.batch * a.c.kv_heads), dim3(256), 0,
                      stream, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int32_t rows = a.group * a.f;
+  hipLaunchKernelGGL(k_rectify_combine, dim3((rows + kCombineRows - 1) / kCombineRows,
+                     a.c.batch * a.c.kv_heads), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -91,4 +91,65 @@ __device__ __forceinline__ uint32_t order_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Log-sum-exp merge of split partials (Alg. 2, "Combine"), for one workgroup.
+//
+// Split s holds `rows` normalised rows of 128 floats at po + s * o_stride +
+// row * 128 and their log2-domain lse at pl + s * l_stride + row. Row r of the
+// result is written to out_row(r) (128 floats) and its natural-log lse is
+// passed to lse_out(r, value). LDS: `w` holds S * rows floats, `red` blockDim.x
+// float4. Every float4 column of the output gets blockDim.x / (32 * rows)
+// threads, each summing a strided subset of the splits, so the partial reads
+// are spread over the whole workgroup instead of one dependent chain per
+// output.
+typedef float f4_t __attribute__((ext_vector_type(4)));
+
+template <typename OutRow, typename LseOut>
+__device__ void merge_splits(const float* po, size_t o_stride, const float* pl, size_t l_stride,
+                             int S, int rows, float* w, f4_t* red, OutRow out_row, LseOut lse_out) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const float ninf = -__builtin_inff();
+  for (int i = tid; i < S * rows; i += nt) w[i] = pl[(size_t)(i / rows) * l_stride + i % rows];
+  __syncthreads();
+  for (int r = tid; r < rows; r += nt) {
+    float mx = ninf;
+    for (int s = 0; s < S; ++s) mx = fmaxf(mx, w[s * rows + r]);
+    float sum = 0.f;
+    for (int s = 0; s < S; ++s) {
+      const float l = w[s * rows + r];
+      const float e = (l == ninf) ? 0.f : fast_exp2(l - mx);
+      w[s * rows + r] = e;
+      sum += e;
+    }
+    const float inv = sum > 0.f ? 1.f / sum : 0.f;
+    for (int s = 0; s < S; ++s) w[s * rows + r] *= inv;
+    lse_out(r, sum > 0.f ? (mx + fast_log2(sum)) * kLn2 : ninf);
+  }
+  __syncthreads();
+  const int U = rows * (kHeadDim / 4);          // float4 columns
+  const int T = U >= nt ? 1 : nt / U;           // threads per column
+  for (int base = 0; base < U; base += nt) {
+    const int u = base + (tid % (U < nt ? U : nt));
+    const int phase = U < nt ? tid / U : 0;
+    const bool active = phase < T && u < U;
+    const int r = active ? u / (kHeadDim / 4) : 0;
+    const int c4 = active ? u % (kHeadDim / 4) : 0;
+    f4_t acc = {0.f, 0.f, 0.f, 0.f};
+    if (active) {
+      const float* src = po + (size_t)r * kHeadDim + 4 * c4;
+#pragma unroll 8
+      for (int s = phase; s < S; s += T)
+        acc += w[s * rows + r] * *reinterpret_cast<const f4_t*>(src + (size_t)s * o_stride);
+    }
+    if (T > 1) {
+      red[tid] = acc;
+      __syncthreads();
+      if (active && phase == 0) {
+        for (int k = 1; k < T; ++k) acc += red[tid + k * U];
+      }
+      __syncthreads();
+    }
+    if (active && phase == 0) *reinterpret_cast<f4_t*>(out_row(r) + 4 * c4) = acc;
+  }
+}
+
 }  // namespace resa

@@ -56,7 +56,6 @@ struct DecodeArgs {
   float* lse;                  // [B, Hq] or null
   float* part_o;               // [B, Hkv, S, G, D]
   float* part_lse;             // [B, Hkv, S, G]
-  uint32_t* counters;          // [B, Hkv]
 };
 
 struct RectifyArgs {
@@ -74,7 +73,6 @@ struct RectifyArgs {
   float* lse;                  // [B, Hq, f] or null
   float* part_o;               // [B, Hkv, S, G*f, D]
   float* part_lse;             // [B, Hkv, S, G*f]
-  uint32_t* counters;          // [B, Hkv, ceil(G*f / 128)]
   int32_t refresh;
 };
 
