@@ -175,10 +175,11 @@ size_t resa_decode_workspace_size(int32_t batch, int32_t num_kv_heads,
  * With no token selected, out is 0 and lse is -inf. Passing every block id
  * gives dense decoding. num_splits = 0 picks resa_decode_num_splits();
  * explicit counts must lie in [1, 256].
- * Runs as two kernels: the split kernel writes per-split partials into the
- * workspace, then a combine kernel merges them (one split: one kernel). The
- * workspace needs no initialisation; calls sharing one must be ordered on a
- * single stream.
+ * One kernel: each split writes a partial into the workspace and the last
+ * split of a group to finish merges them. The workspace starts with one merge
+ * counter per group: zero-fill it before its first use (resa_workspace_clear
+ * or any zeroing allocator); every call leaves the counters at zero again.
+ * Calls sharing a workspace must be ordered on one stream.
  */
 int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
                        const int32_t* seq_lens, const int32_t* block_idx,
@@ -212,7 +213,7 @@ int resa_dense_rectify(const resa_kv_cache_t* c, const void* q_f, const void* k_
                        float* out, float* lse, int32_t refresh_summaries,
                        void* workspace, size_t workspace_bytes, void* stream);
 
-/* Zero-fills a workspace with a kernel (a convenience; no call requires it). */
+/* Zero-fills a workspace with a kernel (safe under stream capture). */
 int resa_workspace_clear(void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus

@@ -96,8 +96,13 @@ class KVCache:
 
 
 class Workspace:
-    """A device scratch buffer that grows on demand (one per operation kind;
-    calls sharing one must be ordered on a single stream)."""
+    """A zero-initialised device scratch buffer that grows on demand.
+
+    Use one per operation kind. The decode kernel keeps one merge counter per
+    group at the start of its workspace and leaves it at zero after every
+    call, so the buffer is cleared only when it is (re)allocated. Calls that
+    share a workspace must be ordered on one stream.
+    """
 
     def __init__(self, device="cuda"):
         self.device = device

@@ -99,14 +99,15 @@ int hip_fail(hipError_t e, const char* what) {
 }
 
 struct DecodeLayout {
-  size_t lse, o, total;
+  size_t counters, lse, o, total;
 };
 
 DecodeLayout decode_layout(int32_t batch, int32_t kv_heads, int32_t group, int32_t splits) {
   DecodeLayout d;
   const size_t groups = (size_t)batch * kv_heads;
-  d.lse = 0;
-  d.o = round256(groups * splits * group * 4);
+  d.counters = 0;
+  d.lse = round256(groups * 4);
+  d.o = d.lse + round256(groups * splits * group * 4);
   d.total = d.o + groups * splits * group * RESA_HEAD_DIM * 4;
   return d;
 }
@@ -301,6 +302,7 @@ int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_he
   a.scale_log2 = sm_scale * 1.4426950408889634f;
   a.out = out;
   a.lse = lse;
+  a.counters = reinterpret_cast<uint32_t*>(ws + lay.counters);
   a.part_lse = reinterpret_cast<float*>(ws + lay.lse);
   a.part_o = reinterpret_cast<float*>(ws + lay.o);
   hipError_t e = resa::launch_decode(a, static_cast<hipStream_t>(stream));

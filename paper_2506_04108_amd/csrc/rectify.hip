@@ -238,7 +238,7 @@ __global__ __launch_bounds__(256) void k_rectify_combine(RectifyArgs a) {
     const int rho = rho0 + r;
     return ((size_t)bb * a.q_heads + (size_t)hk * G + rho % G) * f + rho / G;
   };
-  merge_splits(a.part_o + ((size_t)grp * S * R + rho0) * kHeadDim, (size_t)R * kHeadDim,
+  merge_splits<false>(a.part_o + ((size_t)grp * S * R + rho0) * kHeadDim, (size_t)R * kHeadDim,
                a.part_lse + (size_t)grp * S * R + rho0, (size_t)R, S, rows, s_w, s_red,
                [&](int r) { return a.out + out_index(r) * kHeadDim; },
                [&](int r, float v) { if (a.lse) a.lse[out_index(r)] = v; });

@@ -59,15 +59,37 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
                                          __builtin_bit_cast(bf16x2_t, b), c, false);
 }
 
-// DPP lane moves inside a row of 16 lanes.
+// DPP lane moves inside a row of 16 lanes. Every pattern used here reads a
+// lane of the same row, so bound_ctrl (out-of-row reads give 0) never applies
+// and the destination needs no initial value.
 template <int kCtrl>
 __device__ __forceinline__ float dpp(float x) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), kCtrl, 0xf, 0xf, false));
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), kCtrl, 0xf, 0xf, true));
 }
 constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
 constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
 constexpr int kDppHalfMirror = 0x141; // lane i <-> 7 - i within each half row
 constexpr int kDppMirror = 0x140;     // lane i <-> 15 - i within the row
+constexpr int kDppXor3 = 0x1B;        // quad_perm [3,2,1,0]
+constexpr int kDppRor4 = 0x124;       // rotate the row by 4 lanes
+constexpr int kDppRor8 = 0x128;       // rotate the row by 8 lanes
+constexpr int kDppBcast0 = 0x150;     // + k: every lane of the row reads lane k
+
+// Transpose-reduce of 16 values across the 16 lanes of a row. Lane c enters
+// with v[s] holding the lane's partial of value n = s ^ c; it leaves with
+// v[0] = the full 16-lane sum of value n = c. Each step pairs lanes that
+// differ in one more bit of c (partners c ^ 15, c ^ 7, c ^ 3, c ^ 1), keeps
+// the half of its values whose bit matches its own, and receives the
+// partner's partial of that half: 8 + 4 + 2 + 1 adds instead of 4 * 16.
+__device__ __forceinline__ void transpose_reduce16(float* v) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) v[j] += dpp<kDppMirror>(v[15 - j]);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) v[j] += dpp<kDppHalfMirror>(v[7 - j]);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) v[j] += dpp<kDppXor3>(v[3 - j]);
+  v[0] += dpp<kDppXor1>(v[1]);
+}
 
 // Sum over the 16 lanes of a row; every lane of the row receives the total.
 __device__ __forceinline__ float row16_sum(float x) {
@@ -91,6 +113,8 @@ __device__ __forceinline__ uint32_t order_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+typedef float f4_t __attribute__((ext_vector_type(4)));
+
 // Log-sum-exp merge of split partials (Alg. 2, "Combine"), for one workgroup.
 //
 // Split s holds `rows` normalised rows of 128 floats at po + s * o_stride +
@@ -103,12 +127,28 @@ __device__ __forceinline__ uint32_t order_key(float f) {
 // output.
 typedef float f4_t __attribute__((ext_vector_type(4)));
 
-template <typename OutRow, typename LseOut>
+// Loads of partials written by other workgroups of the same kernel use agent
+// scope (coherent across the chip's L2 slices); plain loads otherwise.
+template <bool kCoherent>
+__device__ __forceinline__ float ld_part(const float* p) {
+  if constexpr (kCoherent) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else return *p;
+}
+template <bool kCoherent>
+__device__ __forceinline__ f4_t ld_part4(const float* p) {
+  if constexpr (kCoherent) {
+    return f4_t{ld_part<true>(p), ld_part<true>(p + 1), ld_part<true>(p + 2), ld_part<true>(p + 3)};
+  } else {
+    return *reinterpret_cast<const f4_t*>(p);
+  }
+}
+
+template <bool kCoherent, typename OutRow, typename LseOut>
 __device__ void merge_splits(const float* po, size_t o_stride, const float* pl, size_t l_stride,
                              int S, int rows, float* w, f4_t* red, OutRow out_row, LseOut lse_out) {
   const int tid = threadIdx.x, nt = blockDim.x;
   const float ninf = -__builtin_inff();
-  for (int i = tid; i < S * rows; i += nt) w[i] = pl[(size_t)(i / rows) * l_stride + i % rows];
+  for (int i = tid; i < S * rows; i += nt) w[i] = ld_part<kCoherent>(pl + (size_t)(i / rows) * l_stride + i % rows);
   __syncthreads();
   for (int r = tid; r < rows; r += nt) {
     float mx = ninf;
@@ -138,7 +178,7 @@ __device__ void merge_splits(const float* po, size_t o_stride, const float* pl, 
       const float* src = po + (size_t)r * kHeadDim + 4 * c4;
 #pragma unroll 8
       for (int s = phase; s < S; s += T)
-        acc += w[s * rows + r] * *reinterpret_cast<const f4_t*>(src + (size_t)s * o_stride);
+        acc += w[s * rows + r] * ld_part4<kCoherent>(src + (size_t)s * o_stride);
     }
     if (T > 1) {
       red[tid] = acc;

@@ -5,7 +5,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
-#include "../../include/resa.h"
+#include "resa.h"
 
 namespace resa {
 
@@ -56,6 +56,7 @@ struct DecodeArgs {
   float* lse;                  // [B, Hq] or null
   float* part_o;               // [B, Hkv, S, G, D]
   float* part_lse;             // [B, Hkv, S, G]
+  uint32_t* counters;          // [B, Hkv], zero between calls
 };
 
 struct RectifyArgs {

@@ -249,6 +249,35 @@ def test_decode_edge_cases():
     assert max_abs_err(o[3], ro) <= TOL and max_abs_err(l[3], rl) <= TOL
 
 
+def test_decode_reused_workspace_many_splits():
+    """Consecutive calls on one workspace with different queries, block sets
+    and split counts: each call's last split must merge only its own partials
+    and leave the merge counters at zero for the next call."""
+    w, cap = small(g=4, L=2000, cap=2048, tag="reuse")
+    lens = [2000, 1985]
+    K, V = W.kv_cache(w, capacity=cap)
+    K64, V64 = O.bf16_to_f64(K), O.bf16_to_f64(V)
+    cache = make_cache(K, V, 16)
+    ws = R.Workspace(dev())
+    st = O.DecodeState(K64, V64, lens, 16)
+    calls = []
+    for step, (s, S) in enumerate([(0.5, 7), (0.9, 32), (0.8, 64), (0.95, 3), (0.5, 128), (0.9, 1),
+                                   (0.8, 33)]):
+        q = W.decode_query(w, step)
+        ri = oracle_select_idx(w, K64, lens, q, s, 4)
+        idx, ns = padded_idx(ri, 2, 2, 125)
+        out, lse = R.sparse_decode(cache, up(q), i32(lens), i32(idx), i32(ns), num_splits=S,
+                                   workspace=ws)
+        calls.append((out.clone(), lse.clone(), q, ri))
+    torch.cuda.synchronize()
+    for out, lse, q, ri in calls:
+        ro, rl = st.attend(O.bf16_to_f64(q), ri, w.sm_scale)
+        assert max_abs_err(out.cpu().numpy(), ro) <= TOL
+        assert max_abs_err(lse.cpu().numpy(), rl) <= TOL
+    counters = ws.buf[:16].view(torch.int32).cpu().numpy()
+    assert np.all(counters[:4] == 0)
+
+
 def test_decode_deterministic():
     w, cap = small(g=4, tag="det")
     lens = [1000, 999]
