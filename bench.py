@@ -194,7 +194,7 @@ def main():
     out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
     lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
     splits = R.decode_num_splits(B, H, n_cap, b)
-    ws_sel = torch.zeros(max(lb.resa_select_workspace_size(B, H, cap, b, 0), 256), dtype=torch.uint8,
+    ws_sel = torch.zeros(max(lb.resa_select_workspace_size(B, H, cap, b), 256), dtype=torch.uint8,
                          device=dev)
     ws_dec = torch.zeros(lb.resa_decode_workspace_size(B, H, Hq, n_cap, b, splits), dtype=torch.uint8,
                          device=dev)

@@ -124,10 +124,9 @@ int resa_block_summarize(const resa_kv_cache_t* c, const int32_t* seq_lens,
 int resa_append_kv(const resa_kv_cache_t* c, const void* k_new, const void* v_new,
                    int32_t* seq_lens, int32_t max_seq_len, void* stream);
 
-/* Workspace bytes resa_select_blocks needs (0 if scores_out is given). */
+/* Workspace bytes resa_select_blocks needs. */
 size_t resa_select_workspace_size(int32_t batch, int32_t num_kv_heads,
-                                  int32_t max_seq_len, int32_t block_size,
-                                  int32_t with_scores_out);
+                                  int32_t max_seq_len, int32_t block_size);
 
 /*
  * Fig. 3 + Eq. 4 + Eq. 5 (Sec. 2.1, "Block Selection"), per (sequence b,
@@ -144,8 +143,13 @@ size_t resa_select_workspace_size(int32_t batch, int32_t num_kv_heads,
  * >= resa_num_selected(ceil(max_seq_len / block_size), ...) (else
  * RESA_ERR_CAPACITY). scores_out (optional, may be NULL): fp32 [batch,
  * num_kv_heads, ceil(max_seq_len / block_size)], receives the Eq. 4 scores
- * before local forcing (entries past M_b are not written). When scores_out is
- * NULL the scores live in the workspace.
+ * before local forcing (entries past M_b are not written); the scores are
+ * also kept in the workspace either way.
+ * One kernel scores the blocks and, in the last workgroup of each group to
+ * finish, selects them (groups of more than 32768 blocks use a second
+ * kernel). The workspace starts with one ticket per group: zero-fill it
+ * before its first use (resa_workspace_clear); every call leaves the tickets
+ * at zero again. Calls sharing a workspace must be ordered on one stream.
  */
 int resa_select_blocks(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
                        const int32_t* seq_lens, int32_t max_seq_len,

@@ -170,14 +170,11 @@ def select_blocks(cache: KVCache, q: torch.Tensor, seq_lens: torch.Tensor, max_s
         num_sel = torch.empty((B, Hkv), dtype=torch.int32, device=q.device)
     _need(block_idx, "block_idx", torch.int32, (B, Hkv, n_cap))
     _need(num_sel, "num_sel", torch.int32, (B, Hkv))
-    ws_ptr, ws_bytes = None, 0
     if scores_out is not None:
         _need(scores_out, "scores_out", torch.float32, (B, Hkv, mseq))
-    else:
-        ws_bytes = lib().resa_select_workspace_size(B, Hkv, max_seq_len, cache.block_size, 0)
-        if ws_bytes:
-            ws = (workspace or Workspace(q.device)).get(ws_bytes)
-            ws_ptr = ws.data_ptr()
+    ws_bytes = lib().resa_select_workspace_size(B, Hkv, max_seq_len, cache.block_size)
+    ws = (workspace or Workspace(q.device)).get(ws_bytes)
+    ws_ptr, ws_bytes = ws.data_ptr(), ws.numel()
     params = SelectParams(float(sparsity), int(min_blocks), int(n_local))
     d = cache.desc()
     check(lib().resa_select_blocks(C.byref(d), q.data_ptr(), hq, seq_lens.data_ptr(), max_seq_len,

@@ -46,7 +46,7 @@ SIGNATURES = {
     "resa_num_selected": (_I, [_I, _D, _I, _I]),
     "resa_block_summarize": (C.c_int, [_CACHE, _P, _I, _I, _P]),
     "resa_append_kv": (C.c_int, [_CACHE, _P, _P, _P, _I, _P]),
-    "resa_select_workspace_size": (_Z, [_I, _I, _I, _I, _I]),
+    "resa_select_workspace_size": (_Z, [_I, _I, _I, _I]),
     "resa_select_blocks": (C.c_int, [_CACHE, _P, _I, _P, _I, C.POINTER(SelectParams), _P, _P, _I,
                                      _P, _P, _Z, _P]),
     "resa_decode_num_splits": (_I, [_I, _I, _I, _I]),

@@ -98,6 +98,23 @@ int hip_fail(hipError_t e, const char* what) {
   return fail(RESA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+struct SelectLayout {
+  size_t counters, hist, scores, total;
+};
+
+// Workspace of resa_select_blocks: one ticket per group (zero between calls),
+// per-workgroup key-digit counts, and the scores (rows padded to 4 floats).
+SelectLayout select_layout(int32_t batch, int32_t kv_heads, int32_t max_seq_len, int32_t block_size) {
+  SelectLayout l;
+  const size_t groups = (size_t)batch * kv_heads;
+  const size_t mseq = ((size_t)max_seq_len + block_size - 1) / block_size;
+  l.counters = 0;
+  l.hist = round256(groups * 4);
+  l.scores = l.hist + round256(groups * (size_t)resa::select_hist_words(batch, kv_heads, (int32_t)mseq) * 4);
+  l.total = l.scores + groups * ((mseq + 3) & ~size_t(3)) * sizeof(float);
+  return l;
+}
+
 struct DecodeLayout {
   size_t counters, lse, o, total;
 };
@@ -183,10 +200,9 @@ int resa_append_kv(const resa_kv_cache_t* c, const void* k_new, const void* v_ne
 }
 
 size_t resa_select_workspace_size(int32_t batch, int32_t num_kv_heads, int32_t max_seq_len,
-                                  int32_t block_size, int32_t with_scores_out) {
-  if (with_scores_out || batch < 1 || num_kv_heads < 1 || max_seq_len < 0 || block_size < 1) return 0;
-  const size_t mseq = ((size_t)max_seq_len + block_size - 1) / block_size;
-  return (size_t)batch * num_kv_heads * mseq * sizeof(float);
+                                  int32_t block_size) {
+  if (batch < 1 || num_kv_heads < 1 || max_seq_len < 0 || block_size < 1) return 0;
+  return select_layout(batch, num_kv_heads, max_seq_len, block_size).total;
 }
 
 int resa_select_blocks(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
@@ -216,20 +232,13 @@ int resa_select_blocks(const resa_kv_cache_t* c, const void* q, int32_t num_q_he
   if (n_cap < need)
     return fail(RESA_ERR_CAPACITY, "n_cap %d < %d blocks selectable at max_seq_len %d", n_cap, need,
                 max_seq_len);
-  float* scores = scores_out;
-  if (scores_out != nullptr) {
-    RESA_CHECK_PTR(scores_out, 4);
-  } else {
-    const size_t want = resa_select_workspace_size(c->batch, c->num_kv_heads, max_seq_len,
-                                                   c->block_size, 0);
-    if (want > 0) {
-      if (workspace == nullptr || workspace_bytes < want)
-        return fail(RESA_ERR_WORKSPACE, "select workspace needs %zu bytes, got %zu", want,
-                    workspace == nullptr ? (size_t)0 : workspace_bytes);
-      if (!aligned(workspace, 16)) return fail(RESA_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
-    }
-    scores = static_cast<float*>(workspace);
-  }
+  if (scores_out != nullptr) RESA_CHECK_PTR(scores_out, 4);
+  const SelectLayout lay = select_layout(c->batch, c->num_kv_heads, max_seq_len, c->block_size);
+  if (workspace == nullptr || workspace_bytes < lay.total)
+    return fail(RESA_ERR_WORKSPACE, "select workspace needs %zu bytes, got %zu", lay.total,
+                workspace == nullptr ? (size_t)0 : workspace_bytes);
+  if (!aligned(workspace, 16)) return fail(RESA_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
+  char* ws = static_cast<char*>(workspace);
   resa::SelectArgs a;
   a.c = cache_args(c);
   a.q = static_cast<const uint16_t*>(q);
@@ -240,10 +249,16 @@ int resa_select_blocks(const resa_kv_cache_t* c, const void* q, int32_t num_q_he
   a.keep_ppm = keep;
   a.min_blocks = params->min_blocks;
   a.n_local = params->n_local;
-  a.scores = scores;
+  a.scores = reinterpret_cast<float*>(ws + lay.scores);
+  a.score_stride = (mseq + 3) & ~3;
+  a.scores_out = scores_out;
   a.block_idx = block_idx;
   a.num_sel = num_sel;
   a.n_cap = n_cap;
+  a.counters = reinterpret_cast<uint32_t*>(ws + lay.counters);
+  a.hist = reinterpret_cast<uint32_t*>(ws + lay.hist);
+  a.blocks_per_wg = resa::select_blocks_per_wg(c->batch, c->num_kv_heads, mseq);
+  a.fused = mseq <= resa::select_fused_max_blocks() ? 1 : 0;
   hipError_t e = resa::launch_select(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "resa_select_blocks launch");
   return ok();

@@ -37,10 +37,16 @@ struct SelectArgs {
   const int32_t* seq_lens;
   int32_t max_blocks_seq;      // ceil(max_seq_len / b): row stride of the score array
   int32_t keep_ppm, min_blocks, n_local;
-  float* scores;               // [B, Hkv, max_blocks_seq]
+  float* scores;               // workspace [B, Hkv, score_stride], 16-byte aligned rows
+  int32_t score_stride;        // max_blocks_seq rounded up to a multiple of 4
+  float* scores_out;           // optional [B, Hkv, max_blocks_seq]
   int32_t* block_idx;          // [B, Hkv, n_cap]
   int32_t* num_sel;            // [B, Hkv]
   int32_t n_cap;
+  uint32_t* hist;              // [B, Hkv, workgroups, 256] per-workgroup key-digit counts
+  uint32_t* counters;          // [B, Hkv], zero between calls
+  int32_t blocks_per_wg;
+  int32_t fused;               // top-n in the scoring kernel's last workgroup
 };
 
 struct DecodeArgs {
@@ -90,6 +96,9 @@ hipError_t launch_rectify(const RectifyArgs& a, hipStream_t stream);
 hipError_t launch_clear(void* p, size_t bytes, hipStream_t stream);
 
 // Split-count and chunk heuristics (host).
+int32_t select_fused_max_blocks();
+int32_t select_blocks_per_wg(int32_t batch, int32_t kv_heads, int32_t max_blocks_seq);
+int32_t select_hist_words(int32_t batch, int32_t kv_heads, int32_t max_blocks_seq);
 int32_t decode_auto_splits(int32_t batch, int32_t kv_heads, int32_t n_cap, int32_t block_size);
 int32_t rectify_num_qblocks(int32_t group, int32_t f);
 int32_t rectify_chunk(int32_t batch, int32_t kv_heads, int32_t nqblk, int32_t max_seq_len);

@@ -6,82 +6,27 @@
 namespace resa {
 namespace {
 
-constexpr int kScoreBlocksPerWg = 256;  // 4 waves x 64 blocks
+constexpr int kSelThreads = 1024;                 // 16 waves
+constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kTopnThreads = 1024;
+constexpr int kBins1 = 256;                       // first digit: key bits 31..24
+constexpr int kBins2 = 4096;                      // next digits: bits 23..12, then 11..0
+constexpr int kKeysPerLane = 32;                  // fused top-n: M <= 16 waves x 64 lanes x 32
+constexpr int kMaxBlocksPerWg = 4096;             // scores staged in LDS per workgroup
+constexpr int kBufWord3 = 0x00020000;             // raw buffer resource, 32-bit data format
+constexpr int kSc1 = 16;                          // cache policy: agent-scope coherent
 
-// Scores stream the summaries once: lane (r, c) handles dims [8c, 8c + 8) of
-// block base + 4 * it + r, so each wave-wide load is four whole 256-byte
-// summary rows. Per dimension the larger of q*kmax and q*kmin is the product
-// with kmax when q >= 0 and with kmin otherwise (exactly, as fp32 rounding is
-// monotone), so the kernel selects the summary row before multiplying.
-template <int BS>
-__global__ __launch_bounds__(256) void k_score(SelectArgs a) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int hk = blockIdx.y, bb = blockIdx.z;
-  const int L = a.seq_lens[bb];
-  // Lengths beyond max_seq_len are clamped so every access stays in bounds.
-  const int M = min(min((L + BS - 1) / BS, a.max_blocks_seq), a.c.max_blocks);
-  const int base = blockIdx.x * kScoreBlocksPerWg + wave * 64;
-  if (base >= M) return;  // uniform per wave
-  const int r = lane >> 4, col = (lane & 15) * 8;
+__device__ __forceinline__ uint32_t block_key(int m, int forced_from, float s) {
+  return m >= forced_from ? 0xFFFFFFFFu : order_key(s);
+}
 
-  // Pooled query (Fig. 3: average over the g heads of the group), fp32.
-  float qb[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) qb[j] = 0.f;
-  for (int h = 0; h < a.group; ++h) {
-    const U4 qv = ld16(a.q + ((size_t)bb * a.q_heads + (size_t)hk * a.group + h) * kHeadDim + col);
-    const uint32_t w[4] = {qv.x, qv.y, qv.z, qv.w};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      qb[2 * j] += bf_lo(w[j]);
-      qb[2 * j + 1] += bf_hi(w[j]);
-    }
-  }
-  const float inv_g = 1.0f / (float)a.group;
-  bool use_max[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    qb[j] *= inv_g;
-    use_max[j] = qb[j] >= 0.f;
-  }
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, kBufWord3);
+}
 
-  const size_t grp = (size_t)bb * a.c.kv_heads + hk;
-  const uint16_t* kmin = a.c.kmin + grp * a.c.max_blocks * kHeadDim + col;
-  const uint16_t* kmax = a.c.kmax + grp * a.c.max_blocks * kHeadDim + col;
-  float* out = a.scores + grp * a.max_blocks_seq;
-
-  constexpr int kUnroll = 4;
-  for (int it = 0; it < 16; it += kUnroll) {
-    U4 lo[kUnroll], hi[kUnroll];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int m = base + (it + u) * 4 + r;
-      if (m < M) {
-        lo[u] = ld16(kmin + (size_t)m * kHeadDim);
-        hi[u] = ld16(kmax + (size_t)m * kHeadDim);
-      } else {
-        lo[u] = U4{0, 0, 0, 0};
-        hi[u] = U4{0, 0, 0, 0};
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const uint32_t wl[4] = {lo[u].x, lo[u].y, lo[u].z, lo[u].w};
-      const uint32_t wh[4] = {hi[u].x, hi[u].y, hi[u].z, hi[u].w};
-      float s = 0.f;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float a0 = use_max[2 * j] ? bf_lo(wh[j]) : bf_lo(wl[j]);
-        const float a1 = use_max[2 * j + 1] ? bf_hi(wh[j]) : bf_hi(wl[j]);
-        s = fmaf(qb[2 * j], a0, s);
-        s = fmaf(qb[2 * j + 1], a1, s);
-      }
-      s = row16_sum(s);
-      const int m = base + (it + u) * 4 + r;
-      if ((lane & 15) == 0 && m < M) out[m] = s;
-    }
-  }
+// Number of set bits of `mask` in lanes below this one.
+__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
 // Exclusive prefix sum over the 1024 threads of the workgroup; returns the
@@ -134,7 +79,7 @@ __global__ __launch_bounds__(kTopnThreads) void k_topn(SelectArgs a) {
     for (int i = tid; i < a.n_cap; i += kTopnThreads) out[i] = i < n ? i : -1;
     return;
   }
-  const float* sc = a.scores + grp * a.max_blocks_seq;
+  const float* sc = a.scores + grp * a.score_stride;
   const int forced_from = M - a.n_local;
   const int E = (M + kTopnThreads - 1) / kTopnThreads;
   const int lo = min(tid * E, M), hi = min(lo + E, M);
@@ -223,22 +168,321 @@ __global__ __launch_bounds__(kTopnThreads) void k_topn(SelectArgs a) {
   for (int i = n + tid; i < a.n_cap; i += kTopnThreads) out[i] = -1;
 }
 
+
+// Among `nbins` counted digits (a larger digit is a larger key), finds the
+// digit holding the k-th largest key, with the 1024 threads of the group.
+// Leaves {digit, rank within the digit, count of the digit} in misc[0..2].
+__device__ void find_digit(const uint32_t* hist, int nbins, uint32_t k, uint32_t* lds32,
+                           uint32_t* misc) {
+  const int tid = threadIdx.x;
+  const int per = nbins >= kSelThreads ? nbins / kSelThreads : 1;
+  const int owners = nbins / per;
+  uint32_t cnt[kBins2 / kSelThreads];
+  uint32_t sum = 0;
+#pragma unroll
+  for (int j = 0; j < kBins2 / kSelThreads; ++j) {
+    cnt[j] = (tid < owners && j < per) ? hist[nbins - 1 - (tid * per + j)] : 0u;
+    sum += cnt[j];
+  }
+  uint32_t tot;
+  uint32_t cum = block_exclusive_scan(sum, lds32, &tot);
+#pragma unroll
+  for (int j = 0; j < kBins2 / kSelThreads; ++j) {
+    if (tid < owners && j < per && cum < k && cum + cnt[j] >= k) {
+      misc[0] = nbins - 1 - (tid * per + j);
+      misc[1] = k - cum;
+      misc[2] = cnt[j];
+    }
+    cum += cnt[j];
+  }
+  __syncthreads();
+}
+
+// Exact top-n of one group by its last workgroup (M <= 16 * 64 * 32). Keys
+// are lane-major: wave w holds ids [w R, (w + 1) R) and lane l of it ids
+// w R + 64 j + l, so loads are coalesced and id order is (wave, j, lane).
+// s_hist enters holding the counts of the keys' 8 high bits; while the
+// threshold digit holds more keys than are wanted, the next 12 bits, then
+// the last 12, are counted over the keys of that digit, pinning the n-th
+// largest key T. Blocks above T are kept, of the blocks equal to T the lowest
+// ids; output positions and ranks among T-equal keys come from wave ballots
+// and one scan over the 16 wave totals, so the ids leave in ascending order.
+__device__ void select_tail(const SelectArgs& a, size_t grp, int M, int forced_from,
+                            uint32_t* s_hist, uint32_t* lds32, uint32_t* misc) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = count_selected(M, a.keep_ppm, a.min_blocks, a.n_local);
+  int32_t* out = a.block_idx + grp * a.n_cap;
+  if (tid == 0) a.num_sel[grp] = n;
+  if (n == 0 || n >= M) {
+    for (int i = tid; i < a.n_cap; i += kSelThreads) out[i] = i < n ? i : -1;
+    return;
+  }
+  const int R = ((M + kSelWaves - 1) / kSelWaves + 63) & ~63;
+  const int base = wave * R;
+  const __amdgpu_buffer_rsrc_t rs = buf_rsrc(a.scores + grp * a.score_stride, (uint32_t)M * 4);
+  uint32_t key[kKeysPerLane];
+#pragma unroll
+  for (int j = 0; j < kKeysPerLane; ++j) {
+    // Ids past M read 0 (buffer bounds) and are never used.
+    const int id = base + 64 * j + lane;
+    const float v = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, id * 4, 0, kSc1));
+    key[j] = block_key(id, forced_from, v);
+  }
+  auto valid = [&](int j) { return 64 * j < R && base + 64 * j + lane < M; };
+
+  uint32_t prefix, pmask, k = (uint32_t)n;
+  find_digit(s_hist, kBins1, k, lds32, misc);
+  prefix = misc[0] << 24;
+  pmask = 0xFFu << 24;
+  k = misc[1];
+#pragma unroll 1
+  for (int shift = 12; shift >= 0 && misc[2] != k; shift -= 12) {
+    for (int i = tid; i < kBins2; i += kSelThreads) s_hist[i] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kKeysPerLane; ++j)
+      if (valid(j) && (key[j] & pmask) == prefix) atomicAdd(&s_hist[(key[j] >> shift) & 0xFFFu], 1u);
+    __syncthreads();
+    find_digit(s_hist, kBins2, k, lds32, misc);
+    prefix |= misc[0] << shift;
+    pmask |= 0xFFFu << shift;
+    k = misc[1];
+  }
+
+  // Wave totals of keys above T and equal to T, then each wave's offsets.
+  uint32_t eq_w = 0, gt_w = 0;
+#pragma unroll
+  for (int j = 0; j < kKeysPerLane; ++j) {
+    const bool v = valid(j);
+    const uint32_t km = key[j] & pmask;
+    eq_w += __popcll(__ballot(v && km == prefix));
+    gt_w += __popcll(__ballot(v && km > prefix));
+  }
+  uint32_t* s_eq = lds32;        // 16 entries
+  uint32_t* s_gt = lds32 + 16;   // 16 entries
+  __syncthreads();
+  if (lane == 0) {
+    s_eq[wave] = eq_w;
+    s_gt[wave] = gt_w;
+  }
+  __syncthreads();
+  uint32_t run_eq = 0, run_sel = 0;
+  for (int w = 0; w < wave; ++w) {
+    const uint32_t e = s_eq[w];
+    const uint32_t taken = run_eq < k ? min(e, k - run_eq) : 0u;
+    run_sel += s_gt[w] + taken;
+    run_eq += e;
+  }
+#pragma unroll
+  for (int j = 0; j < kKeysPerLane; ++j) {
+    const bool v = valid(j);
+    const uint32_t km = key[j] & pmask;
+    const bool eq = v && km == prefix;
+    const uint64_t beq = __ballot(eq);
+    const bool take = (v && km > prefix) || (eq && run_eq + lanes_below(beq) < k);
+    const uint64_t bt = __ballot(take);
+    const uint32_t pos = run_sel + lanes_below(bt);
+    if (take && pos < (uint32_t)a.n_cap) out[pos] = base + 64 * j + lane;  // never past the row
+    run_eq += __popcll(beq);
+    run_sel += __popcll(bt);
+  }
+  for (int i = n + tid; i < a.n_cap; i += kSelThreads) out[i] = -1;
+}
+
+// Pooled query (Fig. 3), Quest scores (Eq. 4) and, when `fused`, the top-n
+// (Eq. 5) in one kernel. Grid (ceil(max_blocks_seq / blocks_per_wg), kv
+// heads, batch), about one 16-wave workgroup per CU. Each workgroup streams
+// the summaries of its block range: lane (r, c) handles dims [8c, 8c + 8) of
+// 16-block tiles, so each wave-wide load is four whole 256-byte summary rows,
+// and the next tile's loads are in flight while one is scored. Per dimension
+// the larger of q*kmax and q*kmin is the product with kmax when q >= 0 and
+// with kmin otherwise (exactly, as fp32 rounding is monotone), so the
+// summary row is selected before the multiply. Scores are staged in LDS and
+// written out coalesced; with `fused`, the workgroup also counts its keys' 8
+// high bits into its own histogram slot, and the last workgroup of the group
+// to finish (ticket) sums the slots and runs select_tail. Scores, slots and
+// ticket use agent scope (write-through stores, coherent loads, a relaxed
+// atomic after the stores are acknowledged), so no cache writeback is needed
+// between workgroups.
+template <int BS>
+__global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
+  __shared__ uint32_t s_hist[kBins2];
+  __shared__ __attribute__((aligned(16))) float s_score[kMaxBlocksPerWg];
+  __shared__ uint32_t s_lds32[32];
+  __shared__ uint32_t s_misc[4];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int hk = blockIdx.y, bb = blockIdx.z;
+  const size_t grp = (size_t)bb * a.c.kv_heads + hk;
+  const int L = a.seq_lens[bb];
+  // Lengths beyond max_seq_len are clamped so every access stays in bounds.
+  const int M = max(0, min(min((L + BS - 1) / BS, a.max_blocks_seq), a.c.max_blocks));
+  const int forced_from = M - a.n_local;
+  const int b0 = blockIdx.x * a.blocks_per_wg;
+  const int b1 = min(b0 + a.blocks_per_wg, M);
+  const int r = lane >> 4, c = lane & 15, col = c * 8;
+
+  if (a.fused) {
+    for (int i = tid; i < kBins1; i += kSelThreads) s_hist[i] = 0;
+    __syncthreads();
+  }
+  if (b0 < b1) {
+    float qb[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) qb[j] = 0.f;
+    for (int h = 0; h < a.group; ++h) {
+      const U4 qv = ld16(a.q + ((size_t)bb * a.q_heads + (size_t)hk * a.group + h) * kHeadDim + col);
+      const uint32_t w[4] = {qv.x, qv.y, qv.z, qv.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        qb[2 * j] += bf_lo(w[j]);
+        qb[2 * j + 1] += bf_hi(w[j]);
+      }
+    }
+    const float inv_g = 1.0f / (float)a.group;
+    bool use_max[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      qb[j] *= inv_g;
+      use_max[j] = qb[j] >= 0.f;
+    }
+    const uint16_t* kmin = a.c.kmin + grp * a.c.max_blocks * kHeadDim + col;
+    const uint16_t* kmax = a.c.kmax + grp * a.c.max_blocks * kHeadDim + col;
+    const int ntiles = (b1 - b0 + 15) / 16;
+    // Rows past b1 read the last valid block (in bounds) and are ignored.
+    auto load_tile = [&](int t, U4 (&lo4)[4], U4 (&hi4)[4]) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int m = min(b0 + 16 * t + 4 * u + r, b1 - 1);
+        lo4[u] = ld16_stream(kmin + (size_t)m * kHeadDim);
+        hi4[u] = ld16_stream(kmax + (size_t)m * kHeadDim);
+      }
+    };
+    U4 lo4[4], hi4[4], nlo[4], nhi[4];
+    int t = wave;
+    load_tile(min(t, ntiles - 1), lo4, hi4);
+    while (t < ntiles) {
+      load_tile(min(t + kSelWaves, ntiles - 1), nlo, nhi);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t wl[4] = {lo4[u].x, lo4[u].y, lo4[u].z, lo4[u].w};
+        const uint32_t wh[4] = {hi4[u].x, hi4[u].y, hi4[u].z, hi4[u].w};
+        float s = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float a0 = use_max[2 * j] ? bf_lo(wh[j]) : bf_lo(wl[j]);
+          const float a1 = use_max[2 * j + 1] ? bf_hi(wh[j]) : bf_hi(wl[j]);
+          s = fmaf(qb[2 * j], a0, s);
+          s = fmaf(qb[2 * j + 1], a1, s);
+        }
+        s = row16_sum(s);
+        const int m = b0 + 16 * t + 4 * u + r;
+        if (c == 0 && m < b1) {
+          s_score[m - b0] = s;
+          if (a.fused) atomicAdd(&s_hist[block_key(m, forced_from, s) >> 24], 1u);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        lo4[u] = nlo[u];
+        hi4[u] = nhi[u];
+      }
+      t += kSelWaves;
+    }
+  }
+  __syncthreads();
+  // Coalesced write-out of this range's scores: to the workspace rows (16-byte
+  // aligned, write-through at agent scope) and, if asked, to scores_out.
+  const int nb = max(b1 - b0, 0);
+  if (nb > 0) {
+    const __amdgpu_buffer_rsrc_t rs = buf_rsrc(a.scores + grp * a.score_stride + b0, (uint32_t)nb * 4);
+    for (int i = 4 * tid; i < nb; i += 4 * kSelThreads) {
+      const f4_t v = *reinterpret_cast<const f4_t*>(&s_score[i]);
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned, v),
+                                             rs, i * 4, 0, kSc1);
+    }
+    if (a.scores_out != nullptr) {
+      float* so = a.scores_out + grp * a.max_blocks_seq + b0;
+      for (int i = tid; i < nb; i += kSelThreads) so[i] = s_score[i];
+    }
+  }
+  if (!a.fused) return;
+  // This workgroup's digit counts go to its own slot: no shared counters.
+  uint32_t* slot = a.hist + (grp * gridDim.x + blockIdx.x) * kBins1;
+  for (int i = tid; i < kBins1; i += kSelThreads)
+    __hip_atomic_store(slot + i, s_hist[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (tid == 0)
+    s_misc[3] = __hip_atomic_fetch_add(a.counters + grp, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  if (s_misc[3] != gridDim.x - 1) return;
+  {
+    // Sum the group's slots: digit d gets 4 threads, each summing every 4th
+    // slot with independent loads (16 per round).
+    const uint32_t* slots = a.hist + grp * gridDim.x * kBins1;
+    const int W = gridDim.x, d = tid & (kBins1 - 1), part = tid / kBins1;
+    constexpr int kParts = kSelThreads / kBins1;
+    if (tid < kBins1) s_hist[tid] = 0;
+    __syncthreads();
+    uint32_t sum = 0;
+    for (int w0 = part; w0 < W; w0 += 16 * kParts) {
+      uint32_t v[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int w = w0 + j * kParts;
+        v[j] = w < W ? __hip_atomic_load(slots + w * kBins1 + d, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+      }
+#pragma unroll
+      for (int j = 0; j < 16; ++j) sum += v[j];
+    }
+    atomicAdd(&s_hist[d], sum);
+  }
+  __syncthreads();
+  select_tail(a, grp, M, forced_from, s_hist, s_lds32, s_misc);
+  if (tid == 0) __hip_atomic_store(a.counters + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 }  // namespace
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
-  dim3 sgrid((a.max_blocks_seq + kScoreBlocksPerWg - 1) / kScoreBlocksPerWg, a.c.kv_heads, a.c.batch);
   if (a.max_blocks_seq > 0) {
+    dim3 grid((a.max_blocks_seq + a.blocks_per_wg - 1) / a.blocks_per_wg, a.c.kv_heads, a.c.batch);
     switch (a.c.block_size) {
-      case 16: hipLaunchKernelGGL(k_score<16>, sgrid, dim3(256), 0, stream, a); break;
-      case 32: hipLaunchKernelGGL(k_score<32>, sgrid, dim3(256), 0, stream, a); break;
-      case 64: hipLaunchKernelGGL(k_score<64>, sgrid, dim3(256), 0, stream, a); break;
+      case 16: hipLaunchKernelGGL(k_select<16>, grid, dim3(kSelThreads), 0, stream, a); break;
+      case 32: hipLaunchKernelGGL(k_select<32>, grid, dim3(kSelThreads), 0, stream, a); break;
+      case 64: hipLaunchKernelGGL(k_select<64>, grid, dim3(kSelThreads), 0, stream, a); break;
       default: return hipErrorInvalidValue;
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (a.fused) return hipSuccess;
   }
   hipLaunchKernelGGL(k_topn, dim3(a.c.kv_heads, a.c.batch), dim3(kTopnThreads), 0, stream, a);
   return hipGetLastError();
+}
+
+int32_t select_fused_max_blocks() { return kSelThreads * kKeysPerLane; }
+
+int32_t select_blocks_per_wg(int32_t batch, int32_t kv_heads, int32_t max_blocks_seq) {
+  // About one 16-wave workgroup per CU (256 CUs) in all, split evenly within
+  // a group, in multiples of 256 blocks (one 16-block tile per wave).
+  const int64_t groups = (int64_t)batch * kv_heads;
+  int64_t per_group = (256 + groups - 1) / groups;
+  int64_t bpw = ((int64_t)max_blocks_seq + per_group - 1) / per_group;
+  bpw = (bpw + 255) / 256 * 256;
+  if (bpw < 256) bpw = 256;
+  if (bpw > kMaxBlocksPerWg) bpw = kMaxBlocksPerWg;
+  return (int32_t)bpw;
+}
+
+int32_t select_hist_words(int32_t batch, int32_t kv_heads, int32_t max_blocks_seq) {
+  const int32_t bpw = select_blocks_per_wg(batch, kv_heads, max_blocks_seq);
+  const int32_t wgs = (max_blocks_seq + bpw - 1) / bpw;
+  return wgs * kBins1;
 }
 
 }  // namespace resa

@@ -146,8 +146,8 @@ def test_rectify_validation():
 
 def test_workspace_sizes():
     lib = L.lib()
-    assert lib.resa_select_workspace_size(8, 8, 65536, 16, 0) == 8 * 8 * 4096 * 4
-    assert lib.resa_select_workspace_size(8, 8, 65536, 16, 1) == 0
+    full = lib.resa_select_workspace_size(8, 8, 65536, 16)
+    assert full >= 8 * 8 * (4096 + 256 + 1) * 4     # scores, digit counts, tickets
     s = lib.resa_decode_num_splits(8, 8, 410, 16)
     assert 1 <= s <= 256
     assert lib.resa_decode_workspace_size(8, 8, 32, 410, 16, s) >= 64 * s * 4 * 128 * 4

@@ -170,6 +170,45 @@ def test_select_exact_ties():
             assert list(gi[bi, hi, :gn[bi, hi]]) == list(ri[bi, hi])
 
 
+@pytest.mark.parametrize("M", [16400, 32800])
+def test_select_large_groups(M):
+    """16400 blocks run the fused selection near its 32768-key budget; 32800
+    blocks exceed it, so scoring and the standalone top-n kernel run instead."""
+    w = W.TINY_4K.with_(batch=1, num_q_heads=4, num_kv_heads=1, seq_len=M * 16 - 5,
+                        min_tokens=0, seed_tag=f"large{M}")
+    cap = M * 16
+    q = W.decode_query(w)
+    _, gi, gn, gs, rs, ri, rn, _ = run_select(w, cap, [w.seq_len], q, sparsity=0.97)
+    assert O.num_blocks(w.seq_len, 16) == M
+    assert gn[0, 0] == rn[0, 0] == O.num_selected(M, 0.97, 0, 1)
+    assert max_abs_err(gs[0, 0, :M], rs[0, 0]) <= 1e-3
+    check_selection(gi[0, 0, :gn[0, 0]], ri[0, 0], rs[0, 0], rn[0, 0], 1)
+
+
+def test_select_reused_workspace():
+    """Consecutive selections on one workspace (tickets and key histograms must
+    return to zero after each call)."""
+    w, cap = small(g=4, L=3000, cap=3072, B=2, H=2, tag="selws")
+    lens = [3000, 2500]
+    K, V = W.kv_cache(w, capacity=cap)
+    cache = make_cache(K, V, 16)
+    lt = i32(lens)
+    R.block_summarize(cache, lt)
+    ws = R.Workspace(dev())
+    st = O.DecodeState(O.bf16_to_f64(K), O.bf16_to_f64(V), lens, 16)
+    for step, s_ in enumerate([0.9, 0.5, 0.95, 0.8]):
+        q = W.decode_query(w, step)
+        idx, ns = R.select_blocks(cache, up(q), lt, 3000, s_, 4, 1, workspace=ws)
+        rs, ri, rn = st.select(O.bf16_to_f64(q), s_, 4, 1)
+        gi, gn = idx.cpu().numpy(), ns.cpu().numpy()
+        for bi in range(2):
+            for hi in range(2):
+                assert gn[bi, hi] == rn[bi, hi]
+                check_selection(gi[bi, hi, :gn[bi, hi]], ri[bi, hi], rs[bi, hi], rn[bi, hi], 1)
+    tickets = ws.buf[:16].view(torch.int32).cpu().numpy()
+    assert np.all(tickets == 0)
+
+
 def test_select_planted_blocks_win():
     w = W.TINY_4K.with_(plant_norm=math.sqrt(128), seed_tag="strong")
     q = W.decode_query(w)
