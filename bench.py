@@ -10,9 +10,12 @@ LogNormal(0, 0.5) key channels). Steps cycle through `--layers` independent
 layer caches, as a model's layers do, so data reused from one step to the
 next cannot be served by the 256 MB last-level cache.
 
-Prints one JSON line. Per-phase kernel times come from HIP events recorded on
-the launch stream; the sparse-decode roofline uses the bytes of the selected
-K/V blocks per launch.
+Prints one JSON line. `value` is the GPU time of the timed steps (HIP events
+on the launch stream around the whole loop, host launches included). The
+per-kernel figures come from a second pass that replays every launch of one
+kernel from the timed loop back to back between two events; the sparse-decode
+roofline divides the bytes of the selected K/V blocks per launch by that
+average duration.
 """
 from __future__ import annotations
 
@@ -51,6 +54,8 @@ def parse():
     p.add_argument("--dense", action="store_true", help="dense baseline: decode over every block")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work")
+    p.add_argument("--copy-probe", type=int, default=0,
+                   help="bytes of one plain device copy before the timed steps (counter reference)")
     return p.parse_args()
 
 
@@ -163,7 +168,7 @@ def main():
     nlay = max(1, args.layers)
     total = args.warmup + args.steps
     per_layer = -(-total // nlay)
-    cap = L0 + per_layer + b
+    cap = L0 + 2 * per_layer + b  # room for the append replay
     cap = -(-cap // b) * b
     stream = torch.cuda.current_stream()
     sptr = stream.cuda_stream
@@ -217,88 +222,114 @@ def main():
             rect_inputs[li, s] = WD.rectify_rows(w, k_last, v_last, f, 100 * li + s, dev)
     torch.cuda.synchronize()
 
-    ev = {k: [] for k in ("append", "select", "decode", "rectify")}
+    # Per-step selections are kept so the per-kernel timing pass below can
+    # replay each launch with the arguments it had in the timed loop.
+    idx_all = torch.empty((args.steps, B, H, n_cap), dtype=torch.int32, device=dev)
+    nsel_all = torch.empty((args.steps, B, H), dtype=torch.int32, device=dev)
+    calls = []  # (phase, layer, step-in-layer, timed-step, Lcur)
 
-    def mark(name):
-        e = torch.cuda.Event(enable_timing=True)
-        e.record(stream)
-        ev[name].append(e)
+    def launch(phase, li, s, t, Lcur):
+        ly = layers[li]
+        d = C.byref(ly["desc"])
+        ids, ns = (idx_all[t], nsel_all[t]) if t >= 0 else (idx, nsel)
+        if phase == "append":
+            check(lb.resa_append_kv(d, ly["k"][s].data_ptr(), ly["v"][s].data_ptr(),
+                                    ly["lens"].data_ptr(), Lcur, sptr))
+        elif phase == "select":
+            check(lb.resa_select_blocks(d, ly["q"][s].data_ptr(), Hq, ly["lens"].data_ptr(), Lcur + 1,
+                                        C.byref(params), ids.data_ptr(), ns.data_ptr(), n_cap, None,
+                                        ws_sel.data_ptr(), ws_sel.numel(), sptr))
+        elif phase == "decode":
+            if args.dense:
+                ids = all_idx
+            check(lb.resa_sparse_decode(d, ly["q"][s].data_ptr(), Hq, ly["lens"].data_ptr(),
+                                        ids.data_ptr(), ns.data_ptr(), n_cap, splits, sm, out.data_ptr(),
+                                        lse.data_ptr(), ws_dec.data_ptr(), ws_dec.numel(), sptr))
+        else:
+            qf, kf, vf = rect_inputs[li, s + 1]
+            check(lb.resa_dense_rectify(d, qf.data_ptr(), kf.data_ptr(), vf.data_ptr(), Hq, f,
+                                        ly["lens"].data_ptr(), Lcur + 1, sm, rout.data_ptr(), None, 1,
+                                        ws_rec.data_ptr(), ws_rec.numel(), sptr))
 
-    def step(timed: bool):
+    def step(t):
+        """One decode step (t >= 0: timed step t, its selection kept)."""
         li = step.count % nlay
         step.count += 1
         ly = layers[li]
         s = ly["steps"]
         Lcur = L0 + s
-        d = C.byref(ly["desc"])
-        if timed:
-            mark("append")
-        check(lb.resa_append_kv(d, ly["k"][s].data_ptr(), ly["v"][s].data_ptr(), ly["lens"].data_ptr(),
-                                Lcur, sptr))
-        if timed:
-            mark("append")
-        if args.dense:
-            M = -(-(Lcur + 1) // b)
-            nsel.fill_(M)
-            ids = all_idx
-        else:
-            if timed:
-                mark("select")
-            check(lb.resa_select_blocks(d, ly["q"][s].data_ptr(), Hq, ly["lens"].data_ptr(), Lcur + 1,
-                                        C.byref(params), idx.data_ptr(), nsel.data_ptr(), n_cap, None,
-                                        ws_sel.data_ptr(), ws_sel.numel(), sptr))
-            if timed:
-                mark("select")
-            ids = idx
-        if timed:
-            mark("decode")
-        check(lb.resa_sparse_decode(d, ly["q"][s].data_ptr(), Hq, ly["lens"].data_ptr(), ids.data_ptr(),
-                                    nsel.data_ptr(), n_cap, splits, sm, out.data_ptr(), lse.data_ptr(),
-                                    ws_dec.data_ptr(), ws_dec.numel(), sptr))
-        if timed:
-            mark("decode")
-        ly["steps"] = s + 1
+        seq = ["append", "decode"] if args.dense else ["append", "select", "decode"]
         if not args.dense and (s + 1) % f == 0:
-            qf, kf, vf = rect_inputs[li, s + 1]
-            if timed:
-                mark("rectify")
-            check(lb.resa_dense_rectify(d, qf.data_ptr(), kf.data_ptr(), vf.data_ptr(), Hq, f,
-                                        ly["lens"].data_ptr(), Lcur + 1, sm, rout.data_ptr(), None, 1,
-                                        ws_rec.data_ptr(), ws_rec.numel(), sptr))
-            if timed:
-                mark("rectify")
+            seq.append("rectify")
+        if args.dense:
+            (nsel_all[t] if t >= 0 else nsel).fill_(-(-(Lcur + 1) // b))
+        for ph in seq:
+            launch(ph, li, s, t, Lcur)
+            if t >= 0:
+                calls.append((ph, li, s, t, Lcur))
+        ly["steps"] = s + 1
         return Lcur + 1
 
     step.count = 0
     for _ in range(args.warmup):
-        step(False)
+        step(-1)
+    if args.copy_probe:
+        # One plain device copy of known size: the reference that scales the
+        # FETCH_SIZE / WRITE_SIZE counters in a rocprofv3 --pmc run.
+        src = torch.empty(args.copy_probe // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        del src, dst
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     lens_seen = []
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        lens_seen.append(step(True))
+    e0.record(stream)
+    for t in range(args.steps):
+        lens_seen.append(step(t))
+    e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    gpu_ms = e0.elapsed_time(e1)
 
-    def durations(name):
-        e = ev[name]
-        return [e[i].elapsed_time(e[i + 1]) * 1e3 for i in range(0, len(e), 2)]  # us
+    # Per-kernel timing: every launch of one phase from the timed loop is
+    # replayed back to back, bracketed by two events on the launch stream, so
+    # the average is the kernel's own duration (no host launch gaps and no
+    # event packets between launches). Select, decode and rectify only read
+    # the cache (rectify rewrites the rows it was given); the append replay
+    # appends the same tokens once more into the capacity kept for it.
+    phase_us = {}
+    for ph in ("select", "decode", "rectify", "append"):
+        cs = [c for c in calls if c[0] == ph]
+        if not cs:
+            continue
+        a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _, li, s, t, _ in cs:
+            # The host length bound must hold for the cache as it is now.
+            n = layers[li]["steps"]
+            launch(ph, li, s, t, L0 + (n if ph == "append" else n - 1))
+            if ph == "append":
+                layers[li]["steps"] = n + 1
+        z.record(stream)
+        torch.cuda.synchronize()
+        phase_us[ph] = a.elapsed_time(z) * 1e3 / len(cs)
 
-    ph = {k: durations(k) for k in ev}
     # Algorithmic bytes of each decode launch: the selected blocks' K and V rows.
     bytes_dec = []
     for L in lens_seen:
         M = -(-L // b)
         n = M if args.dense else R.num_selected(M, w.sparsity, w.min_blocks, w.n_local)
         bytes_dec.append(B * H * n * b * D * 2 * 2)
-    dec_us = ph["decode"]
-    avg_dec_us = sum(dec_us) / len(dec_us)
+    avg_dec_us = phase_us["decode"]
     avg_bytes = sum(bytes_dec) / len(bytes_dec)
     achieved = avg_bytes / (avg_dec_us * 1e-6) / 1e9
     kernel_src = os.path.join(ROOT, "paper_2506_04108_amd", "csrc", "decode.hip")
     traffic = traffic_from_profile(kernel_src)
-    ms_per_step = wall * 1e3 / args.steps
-    phase_us = {k: round(sum(v) / args.steps, 2) for k, v in ph.items() if v}
+    ms_per_step = gpu_ms / args.steps
+    n_calls = {ph: sum(1 for c in calls if c[0] == ph) for ph in phase_us}
     res = {
         "metric": METRIC,
         "value": round(ms_per_step * 1e3, 2),
@@ -320,7 +351,9 @@ def main():
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "kernel": "k_decode",
                      "avg_launch_us": round(avg_dec_us, 3), "bytes_per_launch": int(avg_bytes)},
-        "phases_us_per_step": phase_us,
+        "kernel_us_per_launch": {k: round(v, 2) for k, v in phase_us.items()},
+        "kernel_us_per_step": {k: round(v * n_calls[k] / args.steps, 2) for k, v in phase_us.items()},
+        "wall_us_per_step": round(wall * 1e6 / args.steps, 2),
     }
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
