@@ -178,13 +178,13 @@ def main():
     t_gen = time.perf_counter()
     layers = []
     for li in range(nlay):
-        K, V, scale = WD.caches(w, cap, li, dev)
+        K, V, scale, plant = WD.caches(w, cap, li, dev)
         mb = cap // b
         cache = R.KVCache(K, V, torch.empty((B, H, mb, D), dtype=torch.bfloat16, device=dev),
                           torch.empty((B, H, mb, D), dtype=torch.bfloat16, device=dev), b)
         lens = torch.full((B,), L0, dtype=torch.int32, device=dev)
         R.block_summarize(cache, lens)
-        q, k, v = WD.step_inputs(w, per_layer, li, scale, dev)
+        q, k, v = WD.step_inputs(w, per_layer, li, scale, plant, dev)
         layers.append(dict(cache=cache, desc=cache.desc(), lens=lens, q=q, k=k, v=v, steps=0))
     torch.cuda.synchronize()
     log(f"[bench] inputs ready in {time.perf_counter() - t_gen:.1f}s")

@@ -11,7 +11,7 @@ constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kTopnThreads = 1024;
 constexpr int kBins1 = 256;                       // first digit: key bits 31..24
 constexpr int kBins2 = 4096;                      // next digits: bits 23..12, then 11..0
-constexpr int kKeysPerLane = 32;                  // fused top-n: M <= 16 waves x 64 lanes x 32
+constexpr int kKeysPerLane = 32;                  // fused top-n: M <= 1024 threads x 32
 constexpr int kMaxBlocksPerWg = 4096;             // scores staged in LDS per workgroup
 constexpr int kBufWord3 = 0x00020000;             // raw buffer resource, 32-bit data format
 constexpr int kSc1 = 16;                          // cache policy: agent-scope coherent
@@ -22,11 +22,6 @@ __device__ __forceinline__ uint32_t block_key(int m, int forced_from, float s) {
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, kBufWord3);
-}
-
-// Number of set bits of `mask` in lanes below this one.
-__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
-  return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
 // Exclusive prefix sum over the 1024 threads of the workgroup; returns the
@@ -198,19 +193,23 @@ __device__ void find_digit(const uint32_t* hist, int nbins, uint32_t k, uint32_t
   __syncthreads();
 }
 
-// Exact top-n of one group by its last workgroup (M <= 16 * 64 * 32). Keys
-// are lane-major: wave w holds ids [w R, (w + 1) R) and lane l of it ids
-// w R + 64 j + l, so loads are coalesced and id order is (wave, j, lane).
-// s_hist enters holding the counts of the keys' 8 high bits; while the
-// threshold digit holds more keys than are wanted, the next 12 bits, then
-// the last 12, are counted over the keys of that digit, pinning the n-th
-// largest key T. Blocks above T are kept, of the blocks equal to T the lowest
-// ids; output positions and ranks among T-equal keys come from wave ballots
-// and one scan over the 16 wave totals, so the ids leave in ascending order.
-__device__ void select_tail(const SelectArgs& a, size_t grp, int M, int forced_from,
+// Exact top-n of one group by its last workgroup (M <= 1024 * NJ). Thread t
+// holds the keys of ids [t NJ, t NJ + NJ) in registers, so id order is
+// thread order. The key loads are issued first; while they are in flight the
+// workgroup sums the group's slots into the counts of the keys' 8 high bits.
+// While the threshold digit holds more keys than are wanted, the next 12
+// bits, then the last 12, are counted over the keys of that digit, pinning
+// the n-th largest key T. Blocks above T are kept and, of the blocks equal to
+// T, the lowest ids: one scan of the packed per-thread counts (above T in the
+// high half, equal to T in the low half) gives every thread its first output
+// position, so the ids leave in ascending order. NJ (a multiple of 4) is the
+// smallest instantiation that covers M, so the unrolled per-thread loops do
+// no more work than the group needs.
+template <int NJ>
+__device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int M, int forced_from, int W,
                             uint32_t* s_hist, uint32_t* lds32, uint32_t* misc) {
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  static_assert(NJ % 4 == 0, "keys are loaded four at a time");
+  const int tid = threadIdx.x;
   const int n = count_selected(M, a.keep_ppm, a.min_blocks, a.n_local);
   int32_t* out = a.block_idx + grp * a.n_cap;
   if (tid == 0) a.num_sel[grp] = n;
@@ -218,18 +217,48 @@ __device__ void select_tail(const SelectArgs& a, size_t grp, int M, int forced_f
     for (int i = tid; i < a.n_cap; i += kSelThreads) out[i] = i < n ? i : -1;
     return;
   }
-  const int R = ((M + kSelWaves - 1) / kSelWaves + 63) & ~63;
-  const int base = wave * R;
-  const __amdgpu_buffer_rsrc_t rs = buf_rsrc(a.scores + grp * a.score_stride, (uint32_t)M * 4);
-  uint32_t key[kKeysPerLane];
+  const int id0 = tid * NJ;
+  // The row is padded to a multiple of 4 scores, so each 16-byte load is
+  // wholly inside the row or wholly past it (then it reads 0); ids past M
+  // are never used.
+  const __amdgpu_buffer_rsrc_t rs = buf_rsrc(a.scores + grp * a.score_stride, (uint32_t)((M + 3) & ~3) * 4);
+  f4_t raw[NJ / 4];
 #pragma unroll
-  for (int j = 0; j < kKeysPerLane; ++j) {
-    // Ids past M read 0 (buffer bounds) and are never used.
-    const int id = base + 64 * j + lane;
-    const float v = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, id * 4, 0, kSc1));
-    key[j] = block_key(id, forced_from, v);
+  for (int i = 0; i < NJ / 4; ++i)
+    raw[i] = __builtin_bit_cast(f4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (id0 + 4 * i) * 4, 0, kSc1));
+
+  {
+    // Sum the group's W slots: digit d gets 4 threads, each summing every 4th
+    // slot with independent loads (16 per round).
+    const uint32_t* slots = a.hist + grp * W * kBins1;
+    const int d = tid & (kBins1 - 1), part = tid / kBins1;
+    constexpr int kParts = kSelThreads / kBins1;
+    if (tid < kBins1) s_hist[tid] = 0;
+    __syncthreads();
+    uint32_t sum = 0;
+    for (int w0 = part; w0 < W; w0 += 16 * kParts) {
+      uint32_t v[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int w = w0 + j * kParts;
+        v[j] = w < W ? __hip_atomic_load(slots + w * kBins1 + d, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+      }
+#pragma unroll
+      for (int j = 0; j < 16; ++j) sum += v[j];
+    }
+    atomicAdd(&s_hist[d], sum);
+    __syncthreads();
   }
-  auto valid = [&](int j) { return 64 * j < R && base + 64 * j + lane < M; };
+
+  uint32_t key[NJ];
+#pragma unroll
+  for (int i = 0; i < NJ / 4; ++i) {
+    key[4 * i + 0] = block_key(id0 + 4 * i + 0, forced_from, raw[i].x);
+    key[4 * i + 1] = block_key(id0 + 4 * i + 1, forced_from, raw[i].y);
+    key[4 * i + 2] = block_key(id0 + 4 * i + 2, forced_from, raw[i].z);
+    key[4 * i + 3] = block_key(id0 + 4 * i + 3, forced_from, raw[i].w);
+  }
+  const int nv = min(max(M - id0, 0), NJ);  // this thread's valid keys: j < nv
 
   uint32_t prefix, pmask, k = (uint32_t)n;
   find_digit(s_hist, kBins1, k, lds32, misc);
@@ -241,8 +270,8 @@ __device__ void select_tail(const SelectArgs& a, size_t grp, int M, int forced_f
     for (int i = tid; i < kBins2; i += kSelThreads) s_hist[i] = 0;
     __syncthreads();
 #pragma unroll
-    for (int j = 0; j < kKeysPerLane; ++j)
-      if (valid(j) && (key[j] & pmask) == prefix) atomicAdd(&s_hist[(key[j] >> shift) & 0xFFFu], 1u);
+    for (int j = 0; j < NJ; ++j)
+      if (j < nv && (key[j] & pmask) == prefix) atomicAdd(&s_hist[(key[j] >> shift) & 0xFFFu], 1u);
     __syncthreads();
     find_digit(s_hist, kBins2, k, lds32, misc);
     prefix |= misc[0] << shift;
@@ -250,42 +279,32 @@ __device__ void select_tail(const SelectArgs& a, size_t grp, int M, int forced_f
     k = misc[1];
   }
 
-  // Wave totals of keys above T and equal to T, then each wave's offsets.
-  uint32_t eq_w = 0, gt_w = 0;
+  // Per-thread counts above T and equal to T (each <= NJ, totals <= M < 2^16).
+  uint32_t gt = 0, eq = 0;
 #pragma unroll
-  for (int j = 0; j < kKeysPerLane; ++j) {
-    const bool v = valid(j);
+  for (int j = 0; j < NJ; ++j) {
     const uint32_t km = key[j] & pmask;
-    eq_w += __popcll(__ballot(v && km == prefix));
-    gt_w += __popcll(__ballot(v && km > prefix));
+    gt += (j < nv && km > prefix);
+    eq += (j < nv && km == prefix);
   }
-  uint32_t* s_eq = lds32;        // 16 entries
-  uint32_t* s_gt = lds32 + 16;   // 16 entries
-  __syncthreads();
-  if (lane == 0) {
-    s_eq[wave] = eq_w;
-    s_gt[wave] = gt_w;
-  }
-  __syncthreads();
-  uint32_t run_eq = 0, run_sel = 0;
-  for (int w = 0; w < wave; ++w) {
-    const uint32_t e = s_eq[w];
-    const uint32_t taken = run_eq < k ? min(e, k - run_eq) : 0u;
-    run_sel += s_gt[w] + taken;
-    run_eq += e;
-  }
+  uint32_t tot;
+  const uint32_t before = block_exclusive_scan((gt << 16) | eq, lds32, &tot);
+  uint32_t e = before & 0xFFFFu;
+  uint32_t pos = (before >> 16) + min(e, k);
 #pragma unroll
-  for (int j = 0; j < kKeysPerLane; ++j) {
-    const bool v = valid(j);
+  for (int j = 0; j < NJ; ++j) {
     const uint32_t km = key[j] & pmask;
-    const bool eq = v && km == prefix;
-    const uint64_t beq = __ballot(eq);
-    const bool take = (v && km > prefix) || (eq && run_eq + lanes_below(beq) < k);
-    const uint64_t bt = __ballot(take);
-    const uint32_t pos = run_sel + lanes_below(bt);
-    if (take && pos < (uint32_t)a.n_cap) out[pos] = base + 64 * j + lane;  // never past the row
-    run_eq += __popcll(beq);
-    run_sel += __popcll(bt);
+    bool take = false;
+    if (j < nv && km > prefix) {
+      take = true;
+    } else if (j < nv && km == prefix) {
+      take = e < k;
+      ++e;
+    }
+    if (take) {
+      if (pos < (uint32_t)a.n_cap) out[pos] = id0 + j;  // never past the row
+      ++pos;
+    }
   }
   for (int i = n + tid; i < a.n_cap; i += kSelThreads) out[i] = -1;
 }
@@ -305,7 +324,7 @@ __device__ void select_tail(const SelectArgs& a, size_t grp, int M, int forced_f
 // ticket use agent scope (write-through stores, coherent loads, a relaxed
 // atomic after the stores are acknowledged), so no cache writeback is needed
 // between workgroups.
-template <int BS>
+template <int NJ>
 __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
   __shared__ uint32_t s_hist[kBins2];
   __shared__ __attribute__((aligned(16))) float s_score[kMaxBlocksPerWg];
@@ -317,7 +336,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
   const size_t grp = (size_t)bb * a.c.kv_heads + hk;
   const int L = a.seq_lens[bb];
   // Lengths beyond max_seq_len are clamped so every access stays in bounds.
-  const int M = max(0, min(min((L + BS - 1) / BS, a.max_blocks_seq), a.c.max_blocks));
+  const int M = max(0, min(min((L + a.c.block_size - 1) / a.c.block_size, a.max_blocks_seq), a.c.max_blocks));
   const int forced_from = M - a.n_local;
   const int b0 = blockIdx.x * a.blocks_per_wg;
   const int b1 = min(b0 + a.blocks_per_wg, M);
@@ -420,29 +439,8 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
     s_misc[3] = __hip_atomic_fetch_add(a.counters + grp, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
   if (s_misc[3] != gridDim.x - 1) return;
-  {
-    // Sum the group's slots: digit d gets 4 threads, each summing every 4th
-    // slot with independent loads (16 per round).
-    const uint32_t* slots = a.hist + grp * gridDim.x * kBins1;
-    const int W = gridDim.x, d = tid & (kBins1 - 1), part = tid / kBins1;
-    constexpr int kParts = kSelThreads / kBins1;
-    if (tid < kBins1) s_hist[tid] = 0;
-    __syncthreads();
-    uint32_t sum = 0;
-    for (int w0 = part; w0 < W; w0 += 16 * kParts) {
-      uint32_t v[16];
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int w = w0 + j * kParts;
-        v[j] = w < W ? __hip_atomic_load(slots + w * kBins1 + d, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
-      }
-#pragma unroll
-      for (int j = 0; j < 16; ++j) sum += v[j];
-    }
-    atomicAdd(&s_hist[d], sum);
-  }
-  __syncthreads();
-  select_tail(a, grp, M, forced_from, s_hist, s_lds32, s_misc);
+  const int W = gridDim.x;
+  select_tail<NJ>(a, grp, M, forced_from, W, s_hist, s_lds32, s_misc);
   if (tid == 0) __hip_atomic_store(a.counters + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -451,12 +449,21 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   if (a.max_blocks_seq > 0) {
     dim3 grid((a.max_blocks_seq + a.blocks_per_wg - 1) / a.blocks_per_wg, a.c.kv_heads, a.c.batch);
-    switch (a.c.block_size) {
-      case 16: hipLaunchKernelGGL(k_select<16>, grid, dim3(kSelThreads), 0, stream, a); break;
-      case 32: hipLaunchKernelGGL(k_select<32>, grid, dim3(kSelThreads), 0, stream, a); break;
-      case 64: hipLaunchKernelGGL(k_select<64>, grid, dim3(kSelThreads), 0, stream, a); break;
-      default: return hipErrorInvalidValue;
-    }
+    // Keys per thread of the fused top-n: the smallest instantiation that
+    // holds the longest group (every group's M <= max_blocks_seq).
+    const int per = (a.max_blocks_seq + kSelThreads - 1) / kSelThreads;
+    if (per <= 4)
+      hipLaunchKernelGGL(k_select<4>, grid, dim3(kSelThreads), 0, stream, a);
+    else if (per <= 8)
+      hipLaunchKernelGGL(k_select<8>, grid, dim3(kSelThreads), 0, stream, a);
+    else if (per <= 12)
+      hipLaunchKernelGGL(k_select<12>, grid, dim3(kSelThreads), 0, stream, a);
+    else if (per <= 16)
+      hipLaunchKernelGGL(k_select<16>, grid, dim3(kSelThreads), 0, stream, a);
+    else if (per <= 24)
+      hipLaunchKernelGGL(k_select<24>, grid, dim3(kSelThreads), 0, stream, a);
+    else
+      hipLaunchKernelGGL(k_select<kKeysPerLane>, grid, dim3(kSelThreads), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (a.fused) return hipSuccess;

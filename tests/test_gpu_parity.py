@@ -170,9 +170,10 @@ def test_select_exact_ties():
             assert list(gi[bi, hi, :gn[bi, hi]]) == list(ri[bi, hi])
 
 
-@pytest.mark.parametrize("M", [16400, 32800])
+@pytest.mark.parametrize("M", [4097, 8193, 12000, 16400, 20000, 28000, 32768, 32800])
 def test_select_large_groups(M):
-    """16400 blocks run the fused selection near its 32768-key budget; 32800
+    """Group sizes that take each per-thread key count of the fused selection
+    (4097 just past 4 keys per thread, up to its 32768-key budget); 32800
     blocks exceed it, so scoring and the standalone top-n kernel run instead."""
     w = W.TINY_4K.with_(batch=1, num_q_heads=4, num_kv_heads=1, seq_len=M * 16 - 5,
                         min_tokens=0, seed_tag=f"large{M}")

@@ -20,12 +20,15 @@ def _gen(seed: int, device) -> torch.Generator:
 
 
 def caches(w: Workload, capacity: int, layer: int, device="cuda"):
-    """K, V bf16 ``[B, Hkv, capacity, 128]`` for one layer; rows >= L are zero."""
+    """K, V bf16 ``[B, Hkv, capacity, 128]`` for one layer (rows >= L are zero),
+    the key channel scale ``[Hkv, 128]`` (or None) and the planted directions
+    ``[B, Hkv, 128]`` (or None), which the decode queries of the layer carry too."""
     B, H, D, L = w.batch, w.num_kv_heads, w.head_dim, w.seq_len
     g = _gen(4108 * 1000 + 17 * layer + w.tag() % 997, device)
     K = torch.zeros((B, H, capacity, D), dtype=torch.bfloat16, device=device)
     V = torch.zeros_like(K)
     scale = None
+    plant = torch.zeros((B, H, D), device=device) if w.planted_per_head > 0 else None
     if w.key_scale_sigma > 0:
         scale = torch.empty((H, D), device=device).log_normal_(0.0, w.key_scale_sigma, generator=g)
     for bi in range(B):
@@ -37,17 +40,19 @@ def caches(w: Workload, capacity: int, layer: int, device="cuda"):
             for hi in range(H):
                 u = torch.randn(D, generator=g, device=device)
                 u *= w.plant_norm / u.norm()
+                plant[bi, hi] = u
                 blocks = torch.randperm(max(M - 1, 1), generator=g, device=device)[:w.planted_per_head]
                 rows = (blocks[:, None] * w.block_size + torch.arange(w.block_size, device=device)).reshape(-1)
                 rows = rows[rows < L]
                 k[hi, rows] += w.plant_gain * u
         K[bi, :, :L] = k.to(torch.bfloat16)
         V[bi, :, :L] = torch.randn((H, L, D), generator=g, device=device).to(torch.bfloat16)
-    return K, V, scale
+    return K, V, scale, plant
 
 
-def step_inputs(w: Workload, steps: int, layer: int, scale=None, device="cuda"):
-    """Per-step decode rows: q ``[steps, B, Hq, 128]``, k, v ``[steps, B, Hkv, 128]`` (bf16)."""
+def step_inputs(w: Workload, steps: int, layer: int, scale=None, plant=None, device="cuda"):
+    """Per-step decode rows: q ``[steps, B, Hq, 128]``, k, v ``[steps, B, Hkv, 128]`` (bf16).
+    Each query head of kv group i gets that group's planted direction added."""
     B, H, D = w.batch, w.num_kv_heads, w.head_dim
     g = _gen(4108 * 2000 + 17 * layer + w.tag() % 997, device)
     q = torch.randn((steps, B, w.num_q_heads, D), generator=g, device=device)
@@ -55,6 +60,8 @@ def step_inputs(w: Workload, steps: int, layer: int, scale=None, device="cuda"):
     v = torch.randn((steps, B, H, D), generator=g, device=device)
     if scale is not None:
         k *= scale[None, None]
+    if plant is not None:
+        q += plant.repeat_interleave(w.group_size, dim=1)[None]
     return q.to(torch.bfloat16), k.to(torch.bfloat16), v.to(torch.bfloat16)
 
 
