@@ -8,16 +8,22 @@
 //
 // Grid (num_splits, ceil(R / 128), batch * kv_heads); 4 waves per workgroup,
 // each owning 32 query rows (two 16-row tiles). A workgroup walks its key
-// range in tiles of 32 keys staged through LDS (K row-major, V transposed).
-// Per tile and wave:
+// range in tiles of 64 keys: K and V rows go from registers (loaded one tile
+// ahead) into one of two LDS buffers, row-major, so one barrier per tile
+// separates filling a buffer from reading it. Per tile and wave:
 //   S^T = K . Q^T        (keys x queries; lane l holds query l % 16 and keys
 //                          16 kt + 4 (l / 16) + i)
 //   online softmax per query row in the log2 domain; P is split into a bf16
 //   high part and a bf16 low part (p - hi) so the product keeps ~16 bits
 //   O^T += V^T . P^T     (dims x queries; the contraction index is ordered so
-//                          that P^T is already in the B-operand layout)
-// A second kernel merges the splits by log-sum-exp (Alg. 2, "Combine"),
-// spread over many workgroups.
+//                          that P^T is already in the B-operand layout, and
+//                          V^T comes from the row-major V tile through the
+//                          LDS transpose read)
+// Masking (causal cut, end of the split) is only evaluated on the tiles that
+// reach it. A second kernel merges the splits by log-sum-exp (Alg. 2,
+// "Combine"), spread over many workgroups.
+#include <type_traits>
+
 #include "resa_device.h"
 #include "resa_internal.h"
 
@@ -26,17 +32,29 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kRowsPerWave = 32;
 constexpr int kRowsPerWg = 128;
-constexpr int kKeyTile = 32;
-constexpr int kKStride = kHeadDim + 8;  // bf16 per K row in LDS (272 B, 16-B aligned)
-constexpr int kVStride = kKeyTile + 4;  // bf16 per transposed V row in LDS (72 B)
+constexpr int kKeyTile = 64;
+constexpr int kStride = kHeadDim + 8;    // bf16 per K or V row in LDS (272 B, 16-B aligned)
+constexpr int kTileElems = kKeyTile * kStride;
 constexpr int kMaxRectSplits = 1024;     // splits per group (bounded by the host)
 
 __device__ __forceinline__ f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// LDS transpose read of a 4-key x 16-dim bf16 block by each 16-lane group:
+// lane c of the group passes the address of key kbase + c / 4, dims
+// dbase + 4 (c % 4) .. + 4; lane i of the group receives dim dbase + i of
+// keys kbase .. kbase + 3.
+__device__ __forceinline__ bf16x4_t lds_read_tr(const uint16_t* p) {
+  typedef __attribute__((address_space(3))) i16x4_t lds_i16x4;
+  const i16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_i16x4*)(const_cast<uint16_t*>(p)));
+  return __builtin_bit_cast(bf16x4_t, v);
 }
 
 // Writes the re-encoded rows k_f, v_f over cache rows [L - f, L).
@@ -57,8 +75,8 @@ __global__ __launch_bounds__(256) void k_rectify_rows(RectifyArgs a) {
 }
 
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_rectify_attn(RectifyArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t sK[kKeyTile * kKStride];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[kHeadDim * kVStride];
+  __shared__ __attribute__((aligned(16))) uint16_t sK[2][kTileElems];
+  __shared__ __attribute__((aligned(16))) uint16_t sV[2][kTileElems];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int split = blockIdx.x, qblk = blockIdx.y, grp = blockIdx.z;
   const int bb = grp / a.c.kv_heads, hk = grp % a.c.kv_heads;
@@ -71,6 +89,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int j = lane >> 4, lq = lane & 15;
   const int row_base = qblk * kRowsPerWg + wave * kRowsPerWave;
   const float ninf = -__builtin_inff();
+  const float c = a.scale_log2;
 
   // Q^T operand (B of the S^T product): lane holds query row lq of each tile,
   // dims 32 s + 8 j .. + 8 for k-step s.
@@ -91,6 +110,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       for (int s = 0; s < 4; ++s) qb[qt][s] = __builtin_bit_cast(bf16x8_t, U4{0, 0, 0, 0});
     }
   }
+  // Keys at or past `cut` need the mask: the causal cut of the first row of
+  // this wave (the smallest limit) or the end of the split.
+  const int cut = min(k1, L - f + row_base / G);
 
   f32x4_t o[8][2];
 #pragma unroll
@@ -99,13 +121,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     for (int qt = 0; qt < 2; ++qt) o[dt][qt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m[2] = {ninf, ninf}, l[2] = {0.f, 0.f};
 
+  // Thread tid moves 16-byte pieces tid + 256 e (e < 4) of a tile's K and V:
+  // key (tid + 256 e) / 16, dims 8 (tid % 16) .. + 8.
   const size_t gbase = (size_t)grp * a.c.capacity * kHeadDim;
-  U4 rk[2], rv[2];
+  const int part = tid & 15;
+  U4 rk[4], rv[4];
   auto gload = [&](int t0) {
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int seg = tid + 256 * e, key = seg >> 4, part = seg & 15;
-      const int kk = t0 + key;
+    for (int e = 0; e < 4; ++e) {
+      const int kk = t0 + (tid >> 4) + 16 * e;
       if (kk < k1) {
         rk[e] = ld16_stream(a.c.k + gbase + (size_t)kk * kHeadDim + part * 8);
         rv[e] = ld16_stream(a.c.v + gbase + (size_t)kk * kHeadDim + part * 8);
@@ -115,89 +139,115 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       }
     }
   };
-  auto lstore = [&]() {
+  auto lstore = [&](int buf) {
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int seg = tid + 256 * e, key = seg >> 4, part = seg & 15;
-      st16(&sK[key * kKStride + part * 8], rk[e]);
-      const uint32_t w[4] = {rv[e].x, rv[e].y, rv[e].z, rv[e].w};
-#pragma unroll
-      for (int d = 0; d < 4; ++d) {
-        sV[(part * 8 + 2 * d) * kVStride + key] = (uint16_t)(w[d] & 0xffffu);
-        sV[(part * 8 + 2 * d + 1) * kVStride + key] = (uint16_t)(w[d] >> 16);
-      }
+    for (int e = 0; e < 4; ++e) {
+      const int off = ((tid >> 4) + 16 * e) * kStride + part * 8;
+      st16(&sK[buf][off], rk[e]);
+      st16(&sV[buf][off], rv[e]);
     }
   };
 
-  if (k0 < k1) gload(k0);
-  for (int t0 = k0; t0 < k1; t0 += kKeyTile) {
-    __syncthreads();
-    lstore();
-    __syncthreads();
-    if (t0 + kKeyTile < k1) gload(t0 + kKeyTile);
-
-    f32x4_t sacc[2][2];
+  // One tile: scores, softmax update, P.V. kMasked evaluates the causal cut
+  // and the split end per key.
+  auto tile = [&](int t0, int buf, auto masked) {
+    constexpr bool kMasked = decltype(masked)::value;
+    const uint16_t* tk = sK[buf];
+    const uint16_t* tv = sV[buf];
+    f32x4_t sacc[4][2];
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) sacc[kt][qt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(&sK[(16 * kt + lq) * kKStride + 32 * s + 8 * j]);
+      for (int kt = 0; kt < 4; ++kt) {
+        const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(&tk[(16 * kt + lq) * kStride + 32 * s + 8 * j]);
 #pragma unroll
         for (int qt = 0; qt < 2; ++qt) sacc[kt][qt] = mfma16(ka, qb[qt][s], sacc[kt][qt]);
       }
     }
 
-    bf16x8_t phi[2], plo[2];
+    bf16x8_t phi[2][2], plo[2][2];  // [qt][32-key step]
 #pragma unroll
     for (int qt = 0; qt < 2; ++qt) {
-      float x[8];
+      float x[16];
       float tmax = ninf;
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int key = t0 + 16 * kt + 4 * j + i;
-          float y = sacc[kt][qt][i] * a.scale_log2;
-          y = (key > lim[qt] || key >= k1) ? ninf : y;
+          float y = sacc[kt][qt][i];
+          if constexpr (kMasked) {
+            const int key = t0 + 16 * kt + 4 * j + i;
+            y = (key > lim[qt] || key >= k1) ? ninf : y;
+          }
           x[4 * kt + i] = y;
           tmax = fmaxf(tmax, y);
         }
       tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
       tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-      const float mn = fmaxf(m[qt], tmax);
+      // Raw scores times c are log2-domain logits; c > 0 keeps the maximum.
+      const float mn = fmaxf(m[qt], tmax * c);
       const float mref = mn == ninf ? 0.f : mn;
       const float alpha = fast_exp2(m[qt] - mref);
       m[qt] = mn;
       float ps = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float p = fast_exp2(x[e] - mref);
-        ps += p;
-        const __bf16 hi = (__bf16)p;
-        phi[qt][e] = hi;
-        plo[qt][e] = (__bf16)(p - (float)hi);
+      for (int e = 0; e < 16; ++e) {
+        const float pe = fast_exp2(fmaf(x[e], c, -mref));
+        ps += pe;
+        const __bf16 hi = (__bf16)pe;
+        phi[qt][e >> 3][e & 7] = hi;
+        plo[qt][e >> 3][e & 7] = (__bf16)(pe - (float)hi);
       }
       l[qt] = fmaf(l[qt], alpha, ps);
+      if (__any(alpha != 1.f)) {
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) o[dt][qt] *= alpha;
-    }
-
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
-      const uint16_t* vr = &sV[(16 * dt + lq) * kVStride];
-      const bf16x4_t v0 = *reinterpret_cast<const bf16x4_t*>(vr + 4 * j);
-      const bf16x4_t v1 = *reinterpret_cast<const bf16x4_t*>(vr + 16 + 4 * j);
-      const bf16x8_t va = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
-#pragma unroll
-      for (int qt = 0; qt < 2; ++qt) {
-        o[dt][qt] = mfma16(va, phi[qt], o[dt][qt]);
-        o[dt][qt] = mfma16(va, plo[qt], o[dt][qt]);
+        for (int dt = 0; dt < 8; ++dt) o[dt][qt] *= alpha;
       }
     }
+
+    // P^T for 32-key step ks: lane keys 32 ks + 4 j + (0..3) then
+    // 32 ks + 16 + 4 j + (0..3) (S^T tiles kt = 2 ks, 2 ks + 1); V^T rows of
+    // the same keys come from two transpose reads.
+    const int tr_key = 4 * j + (lq >> 2), tr_dim = 4 * (lq & 3);
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) {
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const bf16x4_t v0 = lds_read_tr(&tv[(32 * ks + tr_key) * kStride + 16 * dt + tr_dim]);
+        const bf16x4_t v1 = lds_read_tr(&tv[(32 * ks + 16 + tr_key) * kStride + 16 * dt + tr_dim]);
+        const bf16x8_t va = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+          o[dt][qt] = mfma16(va, phi[qt][ks], o[dt][qt]);
+          o[dt][qt] = mfma16(va, plo[qt][ks], o[dt][qt]);
+        }
+      }
+    }
+  };
+
+  if (k0 < k1) {
+    gload(k0);
+    lstore(0);
+    if (k0 + kKeyTile < k1) gload(k0 + kKeyTile);
+    __syncthreads();
+  }
+  int buf = 0;
+  for (int t0 = k0; t0 < k1; t0 += kKeyTile) {
+    if (t0 + kKeyTile > cut)
+      tile(t0, buf, std::true_type{});
+    else
+      tile(t0, buf, std::false_type{});
+    // The other buffer was last read in the previous tile, before the
+    // barrier that ended it: fill it with the next tile, start the loads of
+    // the one after, and publish.
+    if (t0 + kKeyTile < k1) lstore(buf ^ 1);
+    if (t0 + 2 * kKeyTile < k1) gload(t0 + 2 * kKeyTile);
+    __syncthreads();
+    buf ^= 1;
   }
 
   // This split's normalised partial rows and their lse (log2 domain).
