@@ -13,12 +13,16 @@
 // separates filling a buffer from reading it. Per tile and wave:
 //   S^T = K . Q^T        (keys x queries; lane l holds query l % 16 and keys
 //                          16 kt + 4 (l / 16) + i)
-//   online softmax per query row in the log2 domain; P is split into a bf16
-//   high part and a bf16 low part (p - hi) so the product keeps ~16 bits
-//   O^T += V^T . P^T     (dims x queries; the contraction index is ordered so
-//                          that P^T is already in the B-operand layout, and
-//                          V^T comes from the row-major V tile through the
-//                          LDS transpose read)
+//   online softmax per query row in the log2 domain; P (in [0, 1]) is
+//   rounded to fp16 (11 significant bits)
+//   O^T += V^T . P^T     (dims x queries, fp16 MFMA; the contraction index is
+//                          ordered so that P^T is already in the B-operand
+//                          layout, and V^T comes from the row-major V tile
+//                          through the LDS transpose read)
+// V tiles are converted from bf16 to fp16 on their way into LDS: every bf16
+// value of magnitude 2^-14 .. 65504 is an fp16 value (8 significant bits
+// fit in 11), so only values below 2^-14 in magnitude, whose products with
+// P in [0, 1] are below 2^-14, lose bits.
 // Masking (causal cut, end of the split) is only evaluated on the tiles that
 // reach it. A second kernel merges the splits by log-sum-exp (Alg. 2,
 // "Combine"), spread over many workgroups.
@@ -31,7 +35,9 @@ namespace resa {
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
@@ -45,16 +51,25 @@ constexpr int kMaxRectSplits = 1024;     // splits per group (bounded by the hos
 __device__ __forceinline__ f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
+__device__ __forceinline__ f32x4_t mfma16(f16x8_t a, f16x8_t b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
 
-// LDS transpose read of a 4-key x 16-dim bf16 block by each 16-lane group:
-// lane c of the group passes the address of key kbase + c / 4, dims
-// dbase + 4 (c % 4) .. + 4; lane i of the group receives dim dbase + i of
-// keys kbase .. kbase + 3.
-__device__ __forceinline__ bf16x4_t lds_read_tr(const uint16_t* p) {
+// Two bf16 (one 32-bit word) -> two fp16 (one 32-bit word).
+__device__ __forceinline__ uint32_t bf2_to_h2(uint32_t w) {
+  const f16x2_t h = {(_Float16)bf_lo(w), (_Float16)bf_hi(w)};
+  return __builtin_bit_cast(uint32_t, h);
+}
+
+// LDS transpose read of a 4-key x 16-dim block of 16-bit values by each
+// 16-lane group: lane c of the group passes the address of key
+// kbase + c / 4, dims dbase + 4 (c % 4) .. + 4; lane i of the group receives
+// dim dbase + i of keys kbase .. kbase + 3.
+__device__ __forceinline__ f16x4_t lds_read_tr(const uint16_t* p) {
   typedef __attribute__((address_space(3))) i16x4_t lds_i16x4;
   const i16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
       (lds_i16x4*)(const_cast<uint16_t*>(p)));
-  return __builtin_bit_cast(bf16x4_t, v);
+  return __builtin_bit_cast(f16x4_t, v);
 }
 
 // Writes the re-encoded rows k_f, v_f over cache rows [L - f, L).
@@ -144,7 +159,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     for (int e = 0; e < 4; ++e) {
       const int off = ((tid >> 4) + 16 * e) * kStride + part * 8;
       st16(&sK[buf][off], rk[e]);
-      st16(&sV[buf][off], rv[e]);
+      st16(&sV[buf][off], U4{bf2_to_h2(rv[e].x), bf2_to_h2(rv[e].y), bf2_to_h2(rv[e].z),
+                             bf2_to_h2(rv[e].w)});
     }
   };
 
@@ -169,7 +185,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       }
     }
 
-    bf16x8_t phi[2][2], plo[2][2];  // [qt][32-key step]
+    f16x8_t ph[2][2];  // [qt][32-key step]
 #pragma unroll
     for (int qt = 0; qt < 2; ++qt) {
       float x[16];
@@ -198,9 +214,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       for (int e = 0; e < 16; ++e) {
         const float pe = fast_exp2(fmaf(x[e], c, -mref));
         ps += pe;
-        const __bf16 hi = (__bf16)pe;
-        phi[qt][e >> 3][e & 7] = hi;
-        plo[qt][e >> 3][e & 7] = (__bf16)(pe - (float)hi);
+        ph[qt][e >> 3][e & 7] = (_Float16)pe;
       }
       l[qt] = fmaf(l[qt], alpha, ps);
       if (__any(alpha != 1.f)) {
@@ -217,14 +231,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     for (int dt = 0; dt < 8; ++dt) {
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
-        const bf16x4_t v0 = lds_read_tr(&tv[(32 * ks + tr_key) * kStride + 16 * dt + tr_dim]);
-        const bf16x4_t v1 = lds_read_tr(&tv[(32 * ks + 16 + tr_key) * kStride + 16 * dt + tr_dim]);
-        const bf16x8_t va = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+        const f16x4_t v0 = lds_read_tr(&tv[(32 * ks + tr_key) * kStride + 16 * dt + tr_dim]);
+        const f16x4_t v1 = lds_read_tr(&tv[(32 * ks + 16 + tr_key) * kStride + 16 * dt + tr_dim]);
+        const f16x8_t va = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
-          o[dt][qt] = mfma16(va, phi[qt][ks], o[dt][qt]);
-          o[dt][qt] = mfma16(va, plo[qt][ks], o[dt][qt]);
-        }
+        for (int qt = 0; qt < 2; ++qt) o[dt][qt] = mfma16(va, ph[qt][ks], o[dt][qt]);
       }
     }
   };

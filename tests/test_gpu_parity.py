@@ -352,8 +352,9 @@ def test_rectify_vs_oracle(g, f):
     torch.cuda.synchronize()
     st = O.DecodeState(O.bf16_to_f64(K), O.bf16_to_f64(V), lens, 16)
     ro, rl = st.rectify(O.bf16_to_f64(qf), O.bf16_to_f64(kf), O.bf16_to_f64(vf), f, w.sm_scale)
-    assert max_abs_err(out.cpu().numpy(), ro) <= TOL
-    assert max_abs_err(lse.cpu().numpy(), rl) <= TOL
+    eo, el = max_abs_err(out.cpu().numpy(), ro), max_abs_err(lse.cpu().numpy(), rl)
+    print(f"rectify g={g} f={f}: max |dO| {eo:.2e}, max |dlse| {el:.2e}")
+    assert eo <= TOL and el <= TOL
     gk = down(cache.k)
     for bi in range(2):
         L = lens[bi]
@@ -377,8 +378,9 @@ def test_rectify_tiny4k_full():
     torch.cuda.synchronize()
     st = O.DecodeState(O.bf16_to_f64(K), O.bf16_to_f64(V), [4096], 16)
     ro, rl = st.rectify(O.bf16_to_f64(qf), O.bf16_to_f64(kf), O.bf16_to_f64(vf), 16, w.sm_scale)
-    assert max_abs_err(out.cpu().numpy(), ro) <= TOL
-    assert max_abs_err(lse.cpu().numpy(), rl) <= TOL
+    eo, el = max_abs_err(out.cpu().numpy(), ro), max_abs_err(lse.cpu().numpy(), rl)
+    print(f"rectify tiny4k: max |dO| {eo:.2e}, max |dlse| {el:.2e}")
+    assert eo <= TOL and el <= TOL
 
 
 # ---------------------------------------------------------------- decode loop
