@@ -57,6 +57,22 @@ struct Soft {
   float m, l;
 };
 
+// The softmax reference m of a head moves only when a chunk's maximum cm
+// exceeds it by more than kRefSlack (log2 domain): weights stay <= 2^kRefSlack
+// and the accumulator rescale (returned factor != 1) is rare. The output is
+// normalised by l under the same reference, so the result does not depend on
+// where m sits.
+constexpr float kRefSlack = 8.f;
+
+__device__ __forceinline__ float move_ref(float& m, float cm) {
+  if (cm > m + kRefSlack) {
+    const float alpha = fast_exp2(m - cm);  // 0 when m was -inf
+    m = cm;
+    return alpha;
+  }
+  return 1.f;
+}
+
 // One chunk for this lane's row group (rows r + 4i of the chunk).
 //   logits: v_dot2 over the lane's 8 dims for 4 rows x GP heads, laid out so
 //           that slot s holds value n = s ^ c (n = row * GP + head), then one
@@ -97,11 +113,9 @@ __device__ __forceinline__ void consume_chunk(const Chunk& ch, int t0, int r, in
     const float x = ok ? val[0] * scale : ninf;
     float cm = fmaxf(x, dpp<kDppRor4>(x));
     cm = fmaxf(cm, dpp<kDppRor8>(cm));
-    const float mn = fmaxf(st.m, cm);
-    const float mref = mn == ninf ? 0.f : mn;
-    const float alpha = fast_exp2(st.m - mref);
+    const float alpha = move_ref(st.m, cm);
     ab_own = alpha;
-    st.m = mn;
+    const float mref = st.m == ninf ? 0.f : st.m;
     const float p = fast_exp2(x - mref);
     float ps = p + dpp<kDppRor4>(p);
     ps += dpp<kDppRor8>(ps);
@@ -121,11 +135,9 @@ __device__ __forceinline__ void consume_chunk(const Chunk& ch, int t0, int r, in
     const float x1 = ok1 ? val[16] * scale : ninf;
     float cm = fmaxf(x0, x1);
     cm = fmaxf(cm, dpp<kDppRor8>(cm));
-    const float mn = fmaxf(st.m, cm);
-    const float mref = mn == ninf ? 0.f : mn;
-    const float alpha = fast_exp2(st.m - mref);
+    const float alpha = move_ref(st.m, cm);
     ab_own = alpha;
-    st.m = mn;
+    const float mref = st.m == ninf ? 0.f : st.m;
     const float p0 = fast_exp2(x0 - mref);
     const float p1 = fast_exp2(x1 - mref);
     float ps = p0 + p1;
@@ -217,7 +229,7 @@ __device__ void merge_tail(const DecodeArgs& a, size_t grp, int S, size_t ob, fl
     const int i = tid + NT * j;
     if (i < S * G) s_lse[i] = lreg[j];
   }
-  __syncthreads();
+  lds_sync();
   float mx = ninf, wsum = 0.f;
   if (active) {
     for (int sp = 0; sp < S; ++sp) mx = fmaxf(mx, s_lse[sp * G + r]);
@@ -243,7 +255,7 @@ __device__ void merge_tail(const DecodeArgs& a, size_t grp, int S, size_t ob, fl
   }
   if constexpr (T > 1) {
     s_red[tid] = acc;
-    __syncthreads();
+    lds_sync();
     if (active && ph == 0) {
 #pragma unroll
       for (int k = 1; k < T; ++k) acc += s_red[tid + k * U];
@@ -316,7 +328,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void k_decode(DecodeArgs a) {
       const int blk = idx[cc / CPB];
       s_tok[i] = (blk < 0 || blk >= M) ? -1 : blk * BS + (cc % CPB) * kChunk;
     }
-    __syncthreads();
+    lds_sync();
     // Wave w takes chunks cb + w, cb + w + W, ... (W waves). A ring of
     // kDepth + 1 chunk buffers keeps kDepth chunks' loads in flight while one
     // is consumed; an invalid chunk reads row 0 (in bounds) and is masked out
@@ -344,7 +356,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void k_decode(DecodeArgs a) {
         }
       }
     }
-    __syncthreads();
+    lds_sync();
   }
 
   // Per-head state of this lane's row group: head h lives in lane 16 r + h.
@@ -385,7 +397,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void k_decode(DecodeArgs a) {
       }
     }
   }
-  __syncthreads();
+  lds_sync();
 
   // Merge the waves; store this split's normalised partial and its lse (log2
   // domain), or the final output directly when there is a single split.

@@ -47,6 +47,7 @@ constexpr int kKeyTile = 64;
 constexpr int kStride = kHeadDim + 8;    // bf16 per K or V row in LDS (272 B, 16-B aligned)
 constexpr int kTileElems = kKeyTile * kStride;
 constexpr int kMaxRectSplits = 1024;     // splits per group (bounded by the host)
+constexpr float kRefSlack = 8.f;         // log2-domain headroom of the softmax reference
 
 __device__ __forceinline__ f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -204,11 +205,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         }
       tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
       tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-      // Raw scores times c are log2-domain logits; c > 0 keeps the maximum.
-      const float mn = fmaxf(m[qt], tmax * c);
-      const float mref = mn == ninf ? 0.f : mn;
-      const float alpha = fast_exp2(m[qt] - mref);
-      m[qt] = mn;
+      // Raw scores times c are log2-domain logits (c > 0 keeps the maximum).
+      // The reference m moves only when the tile's maximum exceeds it by
+      // more than kRefSlack, so the accumulator rescale is rare; every
+      // weight stays <= 2^kRefSlack, well inside fp16 and fp32 range, and
+      // the normalisation by l uses the same reference.
+      const float tm = tmax * c;
+      float alpha = 1.f;
+      if (tm > m[qt] + kRefSlack) {
+        alpha = fast_exp2(m[qt] - tm);  // 0 when m was -inf
+        m[qt] = tm;
+      }
+      const float mref = m[qt] == ninf ? 0.f : m[qt];
       float ps = 0.f;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
@@ -244,7 +252,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     gload(k0);
     lstore(0);
     if (k0 + kKeyTile < k1) gload(k0 + kKeyTile);
-    __syncthreads();
+    lds_sync();
   }
   int buf = 0;
   for (int t0 = k0; t0 < k1; t0 += kKeyTile) {
@@ -257,7 +265,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     // the one after, and publish.
     if (t0 + kKeyTile < k1) lstore(buf ^ 1);
     if (t0 + 2 * kKeyTile < k1) gload(t0 + 2 * kKeyTile);
-    __syncthreads();
+    lds_sync();
     buf ^= 1;
   }
 

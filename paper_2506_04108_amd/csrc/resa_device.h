@@ -15,6 +15,17 @@ struct __attribute__((aligned(16))) U4 {
   uint32_t x, y, z, w;
 };
 
+// Workgroup barrier that orders LDS accesses only. __syncthreads() also
+// waits for every outstanding global load and store of the thread (its fence
+// covers global memory), which would drain prefetches issued before the
+// barrier; here global loads stay in flight and are waited for where their
+// data is used. Not for ordering global memory between threads.
+__device__ __forceinline__ void lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 __device__ __forceinline__ U4 ld16(const void* p) {
   return *reinterpret_cast<const U4*>(p);
 }
@@ -74,6 +85,22 @@ constexpr int kDppXor3 = 0x1B;        // quad_perm [3,2,1,0]
 constexpr int kDppRor4 = 0x124;       // rotate the row by 4 lanes
 constexpr int kDppRor8 = 0x128;       // rotate the row by 8 lanes
 constexpr int kDppBcast0 = 0x150;     // + k: every lane of the row reads lane k
+
+// Inclusive prefix sum over the 64 lanes of a wave: Hillis-Steele steps
+// within each 16-lane row (DPP row_shr 1, 2, 4, 8; lanes shifted in from
+// outside the row read 0), then every row adds the totals of the rows below
+// it, read from lanes 15, 31 and 47.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, true);
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, true);
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, true);
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, true);
+  const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)x, 15);
+  const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)x, 31);
+  const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)x, 47);
+  const int row = (threadIdx.x & 63) >> 4;
+  return x + (row >= 1 ? r0 : 0u) + (row >= 2 ? r1 : 0u) + (row >= 3 ? r2 : 0u);
+}
 
 // Transpose-reduce of 16 values across the 16 lanes of a row. Lane c enters
 // with v[s] holding the lane's partial of value n = s ^ c; it leaves with
@@ -149,7 +176,7 @@ __device__ void merge_splits(const float* po, size_t o_stride, const float* pl, 
   const int tid = threadIdx.x, nt = blockDim.x;
   const float ninf = -__builtin_inff();
   for (int i = tid; i < S * rows; i += nt) w[i] = ld_part<kCoherent>(pl + (size_t)(i / rows) * l_stride + i % rows);
-  __syncthreads();
+  lds_sync();
   for (int r = tid; r < rows; r += nt) {
     float mx = ninf;
     for (int s = 0; s < S; ++s) mx = fmaxf(mx, w[s * rows + r]);
@@ -164,7 +191,7 @@ __device__ void merge_splits(const float* po, size_t o_stride, const float* pl, 
     for (int s = 0; s < S; ++s) w[s * rows + r] *= inv;
     lse_out(r, sum > 0.f ? (mx + fast_log2(sum)) * kLn2 : ninf);
   }
-  __syncthreads();
+  lds_sync();
   const int U = rows * (kHeadDim / 4);          // float4 columns
   const int T = U >= nt ? 1 : nt / U;           // threads per column
   for (int base = 0; base < U; base += nt) {
@@ -182,11 +209,11 @@ __device__ void merge_splits(const float* po, size_t o_stride, const float* pl, 
     }
     if (T > 1) {
       red[tid] = acc;
-      __syncthreads();
+      lds_sync();
       if (active && phase == 0) {
         for (int k = 1; k < T; ++k) acc += red[tid + k * U];
       }
-      __syncthreads();
+      lds_sync();
     }
     if (active && phase == 0) *reinterpret_cast<f4_t*>(out_row(r) + 4 * c4) = acc;
   }

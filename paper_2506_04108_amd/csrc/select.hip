@@ -28,28 +28,18 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, uint32
 // thread's exclusive prefix and writes the total to *total.
 __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* lds16, uint32_t* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  uint32_t x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
+  const uint32_t x = wave_incl_scan(v);
   if (lane == 63) lds16[wave] = x;
-  __syncthreads();
+  lds_sync();
   if (wave == 0) {
-    uint32_t t = lane < 16 ? lds16[lane] : 0u;
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) {
-      const uint32_t y = __shfl_up(t, o);
-      if (lane >= o) t += y;
-    }
+    const uint32_t t = wave_incl_scan(lane < 16 ? lds16[lane] : 0u);
     if (lane < 16) lds16[16 + lane] = t;  // inclusive wave offsets
   }
-  __syncthreads();
+  lds_sync();
   const uint32_t wave_off = wave == 0 ? 0u : lds16[16 + wave - 1];
   *total = lds16[16 + 15];
   const uint32_t r = wave_off + x - v;
-  __syncthreads();  // lds16 may be reused by the next scan
+  lds_sync();  // lds16 may be reused by the next scan
   return r;
 }
 
@@ -85,12 +75,12 @@ __global__ __launch_bounds__(kTopnThreads) void k_topn(SelectArgs a) {
   uint32_t prefix = 0, pmask = 0, k = (uint32_t)n;
   for (int shift = 24; shift >= 0; shift -= 8) {
     if (tid < 256) hist[tid] = 0;
-    __syncthreads();
+    lds_sync();
     for (int m = lo; m < hi; ++m) {
       const uint32_t key = key_of(m);
       if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
     }
-    __syncthreads();
+    lds_sync();
     if (wave == 0) {
       // Lane i owns digits 255-4i .. 252-4i (descending); find the digit where
       // the count of larger-or-equal keys first reaches k.
@@ -115,12 +105,12 @@ __global__ __launch_bounds__(kTopnThreads) void k_topn(SelectArgs a) {
         cum += c[j];
       }
     }
-    __syncthreads();
+    lds_sync();
     prefix |= s_digit << shift;
     pmask |= 255u << shift;
     k = s_k;
     const uint32_t cnt = s_cnt;
-    __syncthreads();
+    lds_sync();
     if (cnt == k) break;  // the whole bucket is kept: no need to refine further
   }
 
@@ -165,11 +155,14 @@ __global__ __launch_bounds__(kTopnThreads) void k_topn(SelectArgs a) {
 
 
 // Among `nbins` counted digits (a larger digit is a larger key), finds the
-// digit holding the k-th largest key, with the 1024 threads of the group.
-// Leaves {digit, rank within the digit, count of the digit} in misc[0..2].
+// digit holding the k-th largest key, with the 1024 threads of the group:
+// thread t owns `per` consecutive digits in descending order, waves scan
+// their sums with lane shuffles, and every thread adds the totals of the
+// waves before its own (two barriers). Leaves {digit, rank within the digit,
+// count of the digit} in misc[0..2].
 __device__ void find_digit(const uint32_t* hist, int nbins, uint32_t k, uint32_t* lds32,
                            uint32_t* misc) {
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int per = nbins >= kSelThreads ? nbins / kSelThreads : 1;
   const int owners = nbins / per;
   uint32_t cnt[kBins2 / kSelThreads];
@@ -179,8 +172,11 @@ __device__ void find_digit(const uint32_t* hist, int nbins, uint32_t k, uint32_t
     cnt[j] = (tid < owners && j < per) ? hist[nbins - 1 - (tid * per + j)] : 0u;
     sum += cnt[j];
   }
-  uint32_t tot;
-  uint32_t cum = block_exclusive_scan(sum, lds32, &tot);
+  const uint32_t x = wave_incl_scan(sum);
+  if (lane == 63) lds32[wave] = x;
+  lds_sync();
+  uint32_t cum = x - sum;
+  for (int w = 0; w < wave; ++w) cum += lds32[w];
 #pragma unroll
   for (int j = 0; j < kBins2 / kSelThreads; ++j) {
     if (tid < owners && j < per && cum < k && cum + cnt[j] >= k) {
@@ -190,25 +186,28 @@ __device__ void find_digit(const uint32_t* hist, int nbins, uint32_t k, uint32_t
     }
     cum += cnt[j];
   }
-  __syncthreads();
+  lds_sync();
 }
+
+constexpr uint32_t kMaxCand = 256;  // bucket size resolved by ranking instead of a third pass
 
 // Exact top-n of one group by its last workgroup (M <= 1024 * NJ). Thread t
 // holds the keys of ids [t NJ, t NJ + NJ) in registers, so id order is
 // thread order. The key loads are issued first; while they are in flight the
 // workgroup sums the group's slots into the counts of the keys' 8 high bits.
-// While the threshold digit holds more keys than are wanted, the next 12
-// bits, then the last 12, are counted over the keys of that digit, pinning
-// the n-th largest key T. Blocks above T are kept and, of the blocks equal to
-// T, the lowest ids: one scan of the packed per-thread counts (above T in the
-// high half, equal to T in the low half) gives every thread its first output
-// position, so the ids leave in ascending order. NJ (a multiple of 4) is the
-// smallest instantiation that covers M, so the unrolled per-thread loops do
-// no more work than the group needs.
+// The threshold digit is refined by the next 12 bits counted over the keys of
+// that digit; the few keys left in the bucket of the n-th largest key are
+// then gathered and ranked among themselves (key descending, id ascending),
+// which pins the n-th largest key T and how many keys equal to T are kept
+// (the lowest ids); a bucket too large to rank is refined by the last 12
+// bits instead. Blocks above T and the kept T-equal blocks are written in
+// ascending id order: one scan of the packed per-thread counts (above T in
+// the high half, equal to T in the low half) gives every thread its first
+// output position. NJ is the smallest instantiation that covers M, so the
+// unrolled per-thread loops do no more work than the group needs.
 template <int NJ>
 __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int M, int forced_from, int W,
-                            uint32_t* s_hist, uint32_t* lds32, uint32_t* misc) {
-  static_assert(NJ % 4 == 0, "keys are loaded four at a time");
+                                            uint32_t* s_hist, uint32_t* lds32, uint32_t* misc) {
   const int tid = threadIdx.x;
   const int n = count_selected(M, a.keep_ppm, a.min_blocks, a.n_local);
   int32_t* out = a.block_idx + grp * a.n_cap;
@@ -222,10 +221,21 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
   // wholly inside the row or wholly past it (then it reads 0); ids past M
   // are never used.
   const __amdgpu_buffer_rsrc_t rs = buf_rsrc(a.scores + grp * a.score_stride, (uint32_t)((M + 3) & ~3) * 4);
-  f4_t raw[NJ / 4];
+  float raw[NJ];
+  if constexpr (NJ % 4 == 0) {
 #pragma unroll
-  for (int i = 0; i < NJ / 4; ++i)
-    raw[i] = __builtin_bit_cast(f4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (id0 + 4 * i) * 4, 0, kSc1));
+    for (int i = 0; i < NJ / 4; ++i) {
+      const f4_t v = __builtin_bit_cast(f4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (id0 + 4 * i) * 4, 0, kSc1));
+      raw[4 * i] = v.x;
+      raw[4 * i + 1] = v.y;
+      raw[4 * i + 2] = v.z;
+      raw[4 * i + 3] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < NJ; ++i)
+      raw[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (id0 + i) * 4, 0, kSc1));
+  }
 
   {
     // Sum the group's W slots: digit d gets 4 threads, each summing every 4th
@@ -234,7 +244,8 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
     const int d = tid & (kBins1 - 1), part = tid / kBins1;
     constexpr int kParts = kSelThreads / kBins1;
     if (tid < kBins1) s_hist[tid] = 0;
-    __syncthreads();
+    if (tid == 0) misc[4] = 0;  // candidate counter of the ranking step (misc[3] holds the ticket)
+    lds_sync();
     uint32_t sum = 0;
     for (int w0 = part; w0 < W; w0 += 16 * kParts) {
       uint32_t v[16];
@@ -247,17 +258,12 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
       for (int j = 0; j < 16; ++j) sum += v[j];
     }
     atomicAdd(&s_hist[d], sum);
-    __syncthreads();
+    lds_sync();
   }
 
   uint32_t key[NJ];
 #pragma unroll
-  for (int i = 0; i < NJ / 4; ++i) {
-    key[4 * i + 0] = block_key(id0 + 4 * i + 0, forced_from, raw[i].x);
-    key[4 * i + 1] = block_key(id0 + 4 * i + 1, forced_from, raw[i].y);
-    key[4 * i + 2] = block_key(id0 + 4 * i + 2, forced_from, raw[i].z);
-    key[4 * i + 3] = block_key(id0 + 4 * i + 3, forced_from, raw[i].w);
-  }
+  for (int i = 0; i < NJ; ++i) key[i] = block_key(id0 + i, forced_from, raw[i]);
   const int nv = min(max(M - id0, 0), NJ);  // this thread's valid keys: j < nv
 
   uint32_t prefix, pmask, k = (uint32_t)n;
@@ -265,18 +271,52 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
   prefix = misc[0] << 24;
   pmask = 0xFFu << 24;
   k = misc[1];
-#pragma unroll 1
-  for (int shift = 12; shift >= 0 && misc[2] != k; shift -= 12) {
+  uint32_t cnt = misc[2];
+  for (int shift = 12; shift >= 0 && cnt != k; shift -= 12) {
+    if (cnt <= kMaxCand) {
+      // Rank the bucket's keys among themselves: the one with k - 1 keys
+      // before it in (key descending, id ascending) order is the n-th.
+      uint32_t* ck = s_hist;              // candidate keys
+      uint32_t* ci = s_hist + kMaxCand;   // candidate ids
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        if (j < nv && (key[j] & pmask) == prefix) {
+          const uint32_t at = atomicAdd(&misc[4], 1u);
+          ck[at] = key[j];
+          ci[at] = (uint32_t)(id0 + j);
+        }
+      }
+      lds_sync();
+      if ((uint32_t)tid < cnt) {
+        const uint32_t kt = ck[tid], it = ci[tid];
+        uint32_t before = 0, eq_before = 0;
+        for (uint32_t j = 0; j < cnt; ++j) {
+          const uint32_t kj = ck[j], ij = ci[j];
+          before += (kj > kt) || (kj == kt && ij < it);
+          eq_before += (kj == kt && ij < it);
+        }
+        if (before == k - 1) {
+          misc[0] = kt;
+          misc[1] = eq_before + 1;  // keys equal to T that are kept
+        }
+      }
+      lds_sync();
+      prefix = misc[0];
+      pmask = 0xFFFFFFFFu;
+      k = misc[1];
+      break;
+    }
     for (int i = tid; i < kBins2; i += kSelThreads) s_hist[i] = 0;
-    __syncthreads();
+    lds_sync();
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
       if (j < nv && (key[j] & pmask) == prefix) atomicAdd(&s_hist[(key[j] >> shift) & 0xFFFu], 1u);
-    __syncthreads();
+    lds_sync();
     find_digit(s_hist, kBins2, k, lds32, misc);
     prefix |= misc[0] << shift;
     pmask |= 0xFFFu << shift;
     k = misc[1];
+    cnt = misc[2];
   }
 
   // Per-thread counts above T and equal to T (each <= NJ, totals <= M < 2^16).
@@ -329,7 +369,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
   __shared__ uint32_t s_hist[kBins2];
   __shared__ __attribute__((aligned(16))) float s_score[kMaxBlocksPerWg];
   __shared__ uint32_t s_lds32[32];
-  __shared__ uint32_t s_misc[4];
+  __shared__ uint32_t s_misc[8];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hk = blockIdx.y, bb = blockIdx.z;
@@ -344,7 +384,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
 
   if (a.fused) {
     for (int i = tid; i < kBins1; i += kSelThreads) s_hist[i] = 0;
-    __syncthreads();
+    lds_sync();
   }
   if (b0 < b1) {
     float qb[8];
@@ -412,7 +452,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
       t += kSelWaves;
     }
   }
-  __syncthreads();
+  lds_sync();
   // Coalesced write-out of this range's scores: to the workspace rows (16-byte
   // aligned, write-through at agent scope) and, if asked, to scores_out.
   const int nb = max(b1 - b0, 0);
@@ -454,6 +494,10 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
     const int per = (a.max_blocks_seq + kSelThreads - 1) / kSelThreads;
     if (per <= 4)
       hipLaunchKernelGGL(k_select<4>, grid, dim3(kSelThreads), 0, stream, a);
+    else if (per <= 5)
+      hipLaunchKernelGGL(k_select<5>, grid, dim3(kSelThreads), 0, stream, a);
+    else if (per <= 6)
+      hipLaunchKernelGGL(k_select<6>, grid, dim3(kSelThreads), 0, stream, a);
     else if (per <= 8)
       hipLaunchKernelGGL(k_select<8>, grid, dim3(kSelThreads), 0, stream, a);
     else if (per <= 12)

@@ -170,6 +170,27 @@ def test_select_exact_ties():
             assert list(gi[bi, hi, :gn[bi, hi]]) == list(ri[bi, hi])
 
 
+@pytest.mark.parametrize("M", [300, 5000, 20000])
+def test_select_exact_ties_large(M):
+    """Exact ties at several group sizes: the bucket of the n-th largest score
+    holds many equal keys, resolved by ranking when it is small and by a third
+    digit pass when it is not; the lowest ids must win either way."""
+    L = M * 16 - 7
+    w = W.TINY_4K.with_(batch=1, num_q_heads=4, num_kv_heads=1, seq_len=L, min_tokens=0,
+                        seed_tag=f"ties{M}")
+    rng = np.random.default_rng(M)
+    Kf = rng.integers(-2, 3, size=(1, 1, M * 16, 128)).astype(np.float32)
+    Vf = np.zeros((1, 1, M * 16, 128), dtype=np.float32)
+    qf = rng.integers(-1, 2, size=(1, 4, 128)).astype(np.float32)
+    K, V, q = W.f32_to_bf16_bits(Kf), W.f32_to_bf16_bits(Vf), W.f32_to_bf16_bits(qf)
+    _, gi, gn, gs, rs, ri, rn, _ = run_select(w, M * 16, [L], q, sparsity=0.93, min_blocks=0,
+                                              K=K, V=V)
+    assert O.num_blocks(L, 16) == M
+    assert np.array_equal(gs[0, 0, :M].astype(np.float64), rs[0, 0])
+    assert len(set(rs[0, 0].tolist())) < M // 4
+    assert list(gi[0, 0, :gn[0, 0]]) == list(ri[0, 0])
+
+
 @pytest.mark.parametrize("M", [4097, 8193, 12000, 16400, 20000, 28000, 32768, 32800])
 def test_select_large_groups(M):
     """Group sizes that take each per-thread key count of the fused selection
