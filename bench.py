@@ -1,8 +1,9 @@
 """Benchmark of the ReSA decode hot path on one MI355X.
 
 A step is one decode token of one attention layer for the whole batch:
-append the token's K/V (online block-summary update), select blocks (pooled
-query, Quest score, top-n) and run block-sparse flash-decoding; every f-th
+append the token's K/V (online block-summary update) and select blocks
+(pooled query, Quest score, top-n) in one launch (resa_append_select; two
+launches with --separate), then run block-sparse flash-decoding; every f-th
 step of a layer also runs the dense rectification of its last f rows. The
 default workload is the 64K batch-8 decode loop (32 query / 8 kv heads,
 head_dim 128, block 16, sparsity 0.9 with a 2048-token minimum, f = 32,
@@ -52,6 +53,8 @@ def parse():
     p.add_argument("--sparsity", type=float, default=None)
     p.add_argument("--rectify-every", type=int, default=None)
     p.add_argument("--dense", action="store_true", help="dense baseline: decode over every block")
+    p.add_argument("--separate", action="store_true",
+                   help="append and select as two launches instead of resa_append_select")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work")
     p.add_argument("--copy-probe", type=int, default=0,
@@ -168,7 +171,7 @@ def main():
     nlay = max(1, args.layers)
     total = args.warmup + args.steps
     per_layer = -(-total // nlay)
-    cap = L0 + per_layer + b
+    cap = L0 + 2 * per_layer + b  # the replay pass appends once more
     cap = -(-cap // b) * b
     stream = torch.cuda.current_stream()
     sptr = stream.cuda_stream
@@ -232,7 +235,11 @@ def main():
         ly = layers[li]
         d = C.byref(ly["desc"])
         ids, ns = (idx_all[t], nsel_all[t]) if t >= 0 else (idx, nsel)
-        if phase == "append":
+        if phase == "append_select":
+            check(lb.resa_append_select(d, ly["k"][s].data_ptr(), ly["v"][s].data_ptr(), ly["q"][s].data_ptr(),
+                                        Hq, ly["lens"].data_ptr(), Lcur, C.byref(params), ids.data_ptr(),
+                                        ns.data_ptr(), n_cap, None, ws_sel.data_ptr(), ws_sel.numel(), sptr))
+        elif phase == "append":
             check(lb.resa_append_kv(d, ly["k"][s].data_ptr(), ly["v"][s].data_ptr(),
                                     ly["lens"].data_ptr(), Lcur, sptr))
         elif phase == "select":
@@ -258,7 +265,12 @@ def main():
         ly = layers[li]
         s = ly["steps"]
         Lcur = L0 + s
-        seq = ["append", "decode"] if args.dense else ["append", "select", "decode"]
+        if args.dense:
+            seq = ["append", "decode"]
+        elif args.separate:
+            seq = ["append", "select", "decode"]
+        else:
+            seq = ["append_select", "decode"]
         if not args.dense and (s + 1) % f == 0:
             seq.append("rectify")
         if args.dense:
@@ -297,11 +309,13 @@ def main():
     # replayed back to back, bracketed by two events on the launch stream, so
     # the average is the kernel's own duration (no host launch gaps and no
     # event packets between launches). Select, decode and rectify only read
-    # the cache (rectify rewrites the rows it was given). The append kernel
-    # runs for less time than one host launch takes, so a replay would time
-    # the host; its duration is taken from a kernel trace instead.
+    # the cache (rectify rewrites the rows it was given); the fused
+    # append + select replay, last, appends the same tokens once more into the
+    # capacity kept for it. The plain append kernel (--separate, --dense) runs
+    # for less time than one host launch takes, so a replay would time the
+    # host; its duration is taken from a kernel trace instead.
     phase_us = {}
-    for ph in ("select", "decode", "rectify"):
+    for ph in ("select", "decode", "rectify", "append_select"):
         cs = [c for c in calls if c[0] == ph]
         if not cs:
             continue
@@ -310,7 +324,12 @@ def main():
         a.record(stream)
         for _, li, s, t, _ in cs:
             # The host length bound must hold for the cache as it is now.
-            launch(ph, li, s, t, L0 + layers[li]["steps"] - 1)
+            n = layers[li]["steps"]
+            if ph == "append_select":
+                launch(ph, li, s, t, L0 + n)
+                layers[li]["steps"] = n + 1
+            else:
+                launch(ph, li, s, t, L0 + n - 1)
         z.record(stream)
         torch.cuda.synchronize()
         phase_us[ph] = a.elapsed_time(z) * 1e3 / len(cs)

@@ -9,6 +9,7 @@
  *   resa_block_summarize  Eq. 3   block key summaries (element-wise min/max)
  *   resa_append_kv        Alg. 1  append one token, update its block summary
  *   resa_select_blocks    Eq. 4-5 pooled-query Quest score + dynamic top-n
+ *   resa_append_select    Alg. 1 + Eq. 4-5  append fused with the selection
  *   resa_sparse_decode    Eq. 2, Alg. 2  split flash-decoding over the
  *                                 selected blocks with log-sum-exp combine
  *   resa_dense_rectify    Sec. 2.2  rewrite the last f cache rows, dense
@@ -156,6 +157,31 @@ int resa_select_blocks(const resa_kv_cache_t* c, const void* q, int32_t num_q_he
                        const resa_select_params_t* params, int32_t* block_idx,
                        int32_t* num_sel, int32_t n_cap, float* scores_out,
                        void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Alg. 1 "update KV cache / block key cache with t", then Fig. 3 + Eq. 4 +
+ * Eq. 5, in one launch: the same results as resa_append_kv followed by
+ * resa_select_blocks with max_seq_len + 1. For every sequence b with
+ * p = seq_lens[b] < capacity: k_new[b], v_new[b] (bf16 [batch,
+ * num_kv_heads, head_dim]) are written at row p, the key is folded into
+ * block p / block_size's summary (it starts the summary when p opens the
+ * block), the blocks are scored and selected over p + 1 tokens, and
+ * seq_lens[b] becomes p + 1 once every kv head of b is done. A sequence
+ * already at capacity is left unchanged and selected over its stored length.
+ * max_seq_len is a host-side upper bound of seq_lens before the call and must
+ * be < capacity (RESA_ERR_CAPACITY otherwise). n_cap, scores_out and the
+ * workspace are sized for max_seq_len + 1 tokens
+ * (resa_select_workspace_size(batch, num_kv_heads, max_seq_len + 1,
+ * block_size)); besides the per-group tickets the workspace holds one
+ * counter per sequence, likewise zero-filled before first use and left at
+ * zero by every call.
+ */
+int resa_append_select(const resa_kv_cache_t* c, const void* k_new, const void* v_new,
+                       const void* q, int32_t num_q_heads, int32_t* seq_lens,
+                       int32_t max_seq_len, const resa_select_params_t* params,
+                       int32_t* block_idx, int32_t* num_sel, int32_t n_cap,
+                       float* scores_out, void* workspace, size_t workspace_bytes,
+                       void* stream);
 
 /* Split count resa_sparse_decode uses when num_splits = 0. */
 int32_t resa_decode_num_splits(int32_t batch, int32_t num_kv_heads, int32_t n_cap,

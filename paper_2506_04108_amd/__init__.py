@@ -23,7 +23,7 @@ import torch
 from ._lib import KVCacheDesc, ResaError, SelectParams, check, lib
 
 __all__ = ["KVCache", "Workspace", "ResaError", "num_selected", "block_summarize", "append_kv",
-           "select_blocks", "sparse_decode", "dense_rectify", "decode_num_splits", "version"]
+           "select_blocks", "append_select", "sparse_decode", "dense_rectify", "decode_num_splits", "version"]
 
 HEAD_DIM = 128
 
@@ -180,6 +180,45 @@ def select_blocks(cache: KVCache, q: torch.Tensor, seq_lens: torch.Tensor, max_s
     check(lib().resa_select_blocks(C.byref(d), q.data_ptr(), hq, seq_lens.data_ptr(), max_seq_len,
                                    C.byref(params), block_idx.data_ptr(), num_sel.data_ptr(), n_cap,
                                    _ptr(scores_out), ws_ptr, ws_bytes, _stream(stream)))
+    return block_idx, num_sel
+
+
+def append_select(cache: KVCache, k_new: torch.Tensor, v_new: torch.Tensor, q: torch.Tensor,
+                  seq_lens: torch.Tensor, max_seq_len: int, sparsity: float, min_blocks: int,
+                  n_local: int = 1, n_cap: int | None = None, block_idx: torch.Tensor | None = None,
+                  num_sel: torch.Tensor | None = None, scores_out: torch.Tensor | None = None,
+                  workspace: Workspace | None = None, stream=None):
+    """Alg. 1 append of one token per sequence fused with the Eq. 4-5
+    selection over the grown sequences (one launch); seq_lens is incremented
+    in place. ``max_seq_len`` bounds seq_lens before the call. Returns
+    ``(block_idx, num_sel)`` as :func:`select_blocks`."""
+    B, Hkv = cache.batch, cache.kv_heads
+    hq = q.shape[1]
+    shape = (B, Hkv, HEAD_DIM)
+    _need(k_new, "k_new", torch.bfloat16, shape)
+    _need(v_new, "v_new", torch.bfloat16, shape)
+    _need(q, "q", torch.bfloat16, (B, hq, HEAD_DIM))
+    _need(seq_lens, "seq_lens", torch.int32, (B,))
+    sel_len = max_seq_len + 1
+    mseq = -(-sel_len // cache.block_size)
+    if n_cap is None:
+        n_cap = max(num_selected(mseq, sparsity, min_blocks, n_local), 1)
+    if block_idx is None:
+        block_idx = torch.empty((B, Hkv, n_cap), dtype=torch.int32, device=q.device)
+    if num_sel is None:
+        num_sel = torch.empty((B, Hkv), dtype=torch.int32, device=q.device)
+    _need(block_idx, "block_idx", torch.int32, (B, Hkv, n_cap))
+    _need(num_sel, "num_sel", torch.int32, (B, Hkv))
+    if scores_out is not None:
+        _need(scores_out, "scores_out", torch.float32, (B, Hkv, mseq))
+    ws_bytes = lib().resa_select_workspace_size(B, Hkv, sel_len, cache.block_size)
+    ws = (workspace or Workspace(q.device)).get(ws_bytes)
+    params = SelectParams(float(sparsity), int(min_blocks), int(n_local))
+    d = cache.desc()
+    check(lib().resa_append_select(C.byref(d), k_new.data_ptr(), v_new.data_ptr(), q.data_ptr(), hq,
+                                   seq_lens.data_ptr(), max_seq_len, C.byref(params),
+                                   block_idx.data_ptr(), num_sel.data_ptr(), n_cap, _ptr(scores_out),
+                                   ws.data_ptr(), ws.numel(), _stream(stream)))
     return block_idx, num_sel
 
 

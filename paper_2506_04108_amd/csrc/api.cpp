@@ -99,17 +99,19 @@ int hip_fail(hipError_t e, const char* what) {
 }
 
 struct SelectLayout {
-  size_t counters, hist, scores, total;
+  size_t counters, seq_counters, hist, scores, total;
 };
 
-// Workspace of resa_select_blocks: one ticket per group (zero between calls),
-// per-workgroup key-digit counts, and the scores (rows padded to 4 floats).
+// Workspace of resa_select_blocks / resa_append_select: one ticket per group
+// and one per sequence (zero between calls), per-workgroup key-digit counts,
+// and the scores (rows padded to 4 floats).
 SelectLayout select_layout(int32_t batch, int32_t kv_heads, int32_t max_seq_len, int32_t block_size) {
   SelectLayout l;
   const size_t groups = (size_t)batch * kv_heads;
   const size_t mseq = ((size_t)max_seq_len + block_size - 1) / block_size;
   l.counters = 0;
-  l.hist = round256(groups * 4);
+  l.seq_counters = groups * 4;
+  l.hist = round256((groups + (size_t)batch) * 4);
   l.scores = l.hist + round256(groups * (size_t)resa::select_hist_words(batch, kv_heads, (int32_t)mseq) * 4);
   l.total = l.scores + groups * ((mseq + 3) & ~size_t(3)) * sizeof(float);
   return l;
@@ -205,12 +207,16 @@ size_t resa_select_workspace_size(int32_t batch, int32_t num_kv_heads, int32_t m
   return select_layout(batch, num_kv_heads, max_seq_len, block_size).total;
 }
 
-int resa_select_blocks(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
-                       const int32_t* seq_lens, int32_t max_seq_len,
-                       const resa_select_params_t* params, int32_t* block_idx, int32_t* num_sel,
-                       int32_t n_cap, float* scores_out, void* workspace, size_t workspace_bytes,
-                       void* stream) {
-  if (int e = check_cache(c)) return e;
+namespace {
+
+// Shared by resa_select_blocks and resa_append_select. `sel_len` is the host
+// bound of the lengths the selection sees (one more than the stored bound
+// when an append is fused in front).
+int select_common(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
+                  const int32_t* seq_lens, int32_t sel_len, const resa_select_params_t* params,
+                  int32_t* block_idx, int32_t* num_sel, int32_t n_cap, float* scores_out,
+                  void* workspace, size_t workspace_bytes, const void* k_new, const void* v_new,
+                  void* stream, const char* what) {
   int32_t group = 0;
   if (int e = check_heads(c, num_q_heads, &group)) return e;
   RESA_CHECK_PTR(q, 16);
@@ -224,16 +230,13 @@ int resa_select_blocks(const resa_kv_cache_t* c, const void* q, int32_t num_q_he
   if (params->min_blocks < 0 || params->n_local < 0)
     return fail(RESA_ERR_INVALID_ARG, "min_blocks (%d) and n_local (%d) must be >= 0",
                 params->min_blocks, params->n_local);
-  if (max_seq_len < 0 || max_seq_len > c->capacity)
-    return fail(RESA_ERR_INVALID_ARG, "max_seq_len %d outside [0, capacity %d]", max_seq_len,
-                c->capacity);
-  const int32_t mseq = (max_seq_len + c->block_size - 1) / c->block_size;
+  const int32_t mseq = (sel_len + c->block_size - 1) / c->block_size;
   const int32_t need = resa::count_selected(mseq, keep, params->min_blocks, params->n_local);
   if (n_cap < need)
-    return fail(RESA_ERR_CAPACITY, "n_cap %d < %d blocks selectable at max_seq_len %d", n_cap, need,
-                max_seq_len);
+    return fail(RESA_ERR_CAPACITY, "n_cap %d < %d blocks selectable at %d tokens", n_cap, need,
+                sel_len);
   if (scores_out != nullptr) RESA_CHECK_PTR(scores_out, 4);
-  const SelectLayout lay = select_layout(c->batch, c->num_kv_heads, max_seq_len, c->block_size);
+  const SelectLayout lay = select_layout(c->batch, c->num_kv_heads, sel_len, c->block_size);
   if (workspace == nullptr || workspace_bytes < lay.total)
     return fail(RESA_ERR_WORKSPACE, "select workspace needs %zu bytes, got %zu", lay.total,
                 workspace == nullptr ? (size_t)0 : workspace_bytes);
@@ -259,9 +262,46 @@ int resa_select_blocks(const resa_kv_cache_t* c, const void* q, int32_t num_q_he
   a.hist = reinterpret_cast<uint32_t*>(ws + lay.hist);
   a.blocks_per_wg = resa::select_blocks_per_wg(c->batch, c->num_kv_heads, mseq);
   a.fused = mseq <= resa::select_fused_max_blocks() ? 1 : 0;
+  a.k_new = static_cast<const uint16_t*>(k_new);
+  a.v_new = static_cast<const uint16_t*>(v_new);
+  a.lens_out = const_cast<int32_t*>(seq_lens);
+  a.seq_counters = reinterpret_cast<uint32_t*>(ws + lay.seq_counters);
   hipError_t e = resa::launch_select(a, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return hip_fail(e, "resa_select_blocks launch");
+  if (e != hipSuccess) return hip_fail(e, what);
   return ok();
+}
+
+}  // namespace
+
+int resa_select_blocks(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
+                       const int32_t* seq_lens, int32_t max_seq_len,
+                       const resa_select_params_t* params, int32_t* block_idx, int32_t* num_sel,
+                       int32_t n_cap, float* scores_out, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  if (int e = check_cache(c)) return e;
+  if (max_seq_len < 0 || max_seq_len > c->capacity)
+    return fail(RESA_ERR_INVALID_ARG, "max_seq_len %d outside [0, capacity %d]", max_seq_len,
+                c->capacity);
+  return select_common(c, q, num_q_heads, seq_lens, max_seq_len, params, block_idx, num_sel, n_cap,
+                       scores_out, workspace, workspace_bytes, nullptr, nullptr, stream,
+                       "resa_select_blocks launch");
+}
+
+int resa_append_select(const resa_kv_cache_t* c, const void* k_new, const void* v_new,
+                       const void* q, int32_t num_q_heads, int32_t* seq_lens, int32_t max_seq_len,
+                       const resa_select_params_t* params, int32_t* block_idx, int32_t* num_sel,
+                       int32_t n_cap, float* scores_out, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  if (int e = check_cache(c)) return e;
+  RESA_CHECK_PTR(k_new, 16);
+  RESA_CHECK_PTR(v_new, 16);
+  if (max_seq_len < 0) return fail(RESA_ERR_INVALID_ARG, "max_seq_len %d < 0", max_seq_len);
+  if (max_seq_len >= c->capacity)
+    return fail(RESA_ERR_CAPACITY, "cache full: max_seq_len %d, capacity %d", max_seq_len,
+                c->capacity);
+  return select_common(c, q, num_q_heads, seq_lens, max_seq_len + 1, params, block_idx, num_sel,
+                       n_cap, scores_out, workspace, workspace_bytes, k_new, v_new, stream,
+                       "resa_append_select launch");
 }
 
 int32_t resa_decode_num_splits(int32_t batch, int32_t num_kv_heads, int32_t n_cap,

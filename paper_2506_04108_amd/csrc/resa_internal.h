@@ -47,6 +47,11 @@ struct SelectArgs {
   uint32_t* counters;          // [B, Hkv], zero between calls
   int32_t blocks_per_wg;
   int32_t fused;               // top-n in the scoring kernel's last workgroup
+  // Append fused in front of the selection (null k_new: plain selection).
+  const uint16_t* k_new;       // [B, Hkv, D] key of the new token
+  const uint16_t* v_new;       // [B, Hkv, D] value of the new token
+  int32_t* lens_out;           // seq_lens, written once every group of the sequence is done
+  uint32_t* seq_counters;      // [B], zero between calls
 };
 
 struct DecodeArgs {

@@ -24,6 +24,30 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, uint32
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, kBufWord3);
 }
 
+// Length of sequence bb seen by the selection. With an append fused in
+// front (k_new set), the new token goes to row `pos` = the stored length and
+// the selection sees one more token; a full cache is left as it is.
+struct SeqLen {
+  int L, pos;  // pos = row of the appended token, -1 without one
+};
+
+__device__ __forceinline__ SeqLen seq_len_of(const SelectArgs& a, int bb) {
+  const int L0 = a.seq_lens[bb];
+  if (a.k_new != nullptr && L0 >= 0 && L0 < a.c.capacity) return {L0 + 1, L0};
+  return {L0, -1};
+}
+
+// Each group takes a ticket on its sequence's counter once every workgroup
+// of the group has read the old length (after the group's last ticket); the
+// group holding the last ticket (t) stores the new length, which therefore
+// no workgroup of this launch can see, and returns the counter to zero.
+__device__ __forceinline__ void finish_append(const SelectArgs& a, int bb, int L, uint32_t t) {
+  if (t == (uint32_t)a.c.kv_heads - 1) {
+    a.lens_out[bb] = L;
+    __hip_atomic_store(a.seq_counters + bb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
 // Exclusive prefix sum over the 1024 threads of the workgroup; returns the
 // thread's exclusive prefix and writes the total to *total.
 __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* lds16, uint32_t* total) {
@@ -47,14 +71,13 @@ __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* lds16, uint32_t* 
 // preserving 32-bit keys finds the n-th largest key T; every block with a
 // larger key is kept, and of the blocks equal to T the lowest ids are kept.
 // The kept ids are then written in ascending order.
-__global__ __launch_bounds__(kTopnThreads) void k_topn(SelectArgs a) {
+__device__ void topn_group(const SelectArgs& a, int L) {
   __shared__ uint32_t hist[256];
   __shared__ uint32_t scan_lds[32];
   __shared__ uint32_t s_digit, s_k, s_cnt;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hk = blockIdx.x, bb = blockIdx.y;
   const int bs = a.c.block_size;
-  const int L = a.seq_lens[bb];
   const int M = max(0, min(min((L + bs - 1) / bs, a.max_blocks_seq), a.c.max_blocks));
   const int n = count_selected(M, a.keep_ppm, a.min_blocks, a.n_local);
   const size_t grp = (size_t)bb * a.c.kv_heads + hk;
@@ -151,6 +174,14 @@ __global__ __launch_bounds__(kTopnThreads) void k_topn(SelectArgs a) {
     }
   }
   for (int i = n + tid; i < a.n_cap; i += kTopnThreads) out[i] = -1;
+}
+
+__global__ __launch_bounds__(kTopnThreads) void k_topn(SelectArgs a) {
+  const SeqLen sl = seq_len_of(a, blockIdx.y);
+  topn_group(a, sl.L);
+  if (a.k_new != nullptr && threadIdx.x == 0)
+    finish_append(a, blockIdx.y, sl.L,
+                  __hip_atomic_fetch_add(a.seq_counters + blockIdx.y, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
 }
 
 
@@ -374,13 +405,26 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hk = blockIdx.y, bb = blockIdx.z;
   const size_t grp = (size_t)bb * a.c.kv_heads + hk;
-  const int L = a.seq_lens[bb];
+  const SeqLen sl = seq_len_of(a, bb);
+  const int L = sl.L;
   // Lengths beyond max_seq_len are clamped so every access stays in bounds.
   const int M = max(0, min(min((L + a.c.block_size - 1) / a.c.block_size, a.max_blocks_seq), a.c.max_blocks));
   const int forced_from = M - a.n_local;
   const int b0 = blockIdx.x * a.blocks_per_wg;
   const int b1 = min(b0 + a.blocks_per_wg, M);
   const int r = lane >> 4, c = lane & 15, col = c * 8;
+
+  // Fused append (Alg. 1): the first workgroup of the group writes the new
+  // K and V rows; the workgroup owning block pos / b folds the new key into
+  // that block's summary (or starts it) before scoring it, and stores it.
+  const int m_new = sl.pos >= 0 ? sl.pos / a.c.block_size : -1;
+  const bool opening = sl.pos >= 0 && sl.pos % a.c.block_size == 0;
+  U4 knew = U4{0, 0, 0, 0}, vnew = U4{0, 0, 0, 0};
+  const bool row_writer = sl.pos >= 0 && blockIdx.x == 0 && tid < 32;
+  if (sl.pos >= 0) {
+    knew = ld16(a.k_new + grp * kHeadDim + col);
+    if (row_writer && tid >= 16) vnew = ld16(a.v_new + grp * kHeadDim + col);
+  }
 
   if (a.fused) {
     for (int i = tid; i < kBins1; i += kSelThreads) s_hist[i] = 0;
@@ -426,6 +470,13 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
+        const int mu = b0 + 16 * t + 4 * u + r;
+        if (mu == m_new && mu < b1) {
+          lo4[u] = opening ? knew : u4_min(lo4[u], knew);
+          hi4[u] = opening ? knew : u4_max(hi4[u], knew);
+          st16(const_cast<uint16_t*>(kmin) + (size_t)mu * kHeadDim, lo4[u]);
+          st16(const_cast<uint16_t*>(kmax) + (size_t)mu * kHeadDim, hi4[u]);
+        }
         const uint32_t wl[4] = {lo4[u].x, lo4[u].y, lo4[u].z, lo4[u].w};
         const uint32_t wh[4] = {hi4[u].x, hi4[u].y, hi4[u].z, hi4[u].w};
         float s = 0.f;
@@ -453,6 +504,15 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
     }
   }
   lds_sync();
+  if (row_writer) {
+    // The new K and V rows (stored after the scoring, so the loads above have
+    // long arrived).
+    const size_t row = (grp * a.c.capacity + sl.pos) * kHeadDim + col;
+    if (tid < 16)
+      st16(const_cast<uint16_t*>(a.c.k) + row, knew);
+    else
+      st16(const_cast<uint16_t*>(a.c.v) + row, vnew);
+  }
   // Coalesced write-out of this range's scores: to the workspace rows (16-byte
   // aligned, write-through at agent scope) and, if asked, to scores_out.
   const int nb = max(b1 - b0, 0);
@@ -480,8 +540,17 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
   __syncthreads();
   if (s_misc[3] != gridDim.x - 1) return;
   const int W = gridDim.x;
+  // Every workgroup of this group has read the old length (all took their
+  // tickets), so the sequence's counter is bumped now; its result is only
+  // looked at after the selection, so the round trip overlaps the tail.
+  uint32_t seq_ticket = 0;
+  if (a.k_new != nullptr && tid == 0)
+    seq_ticket = __hip_atomic_fetch_add(a.seq_counters + bb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   select_tail<NJ>(a, grp, M, forced_from, W, s_hist, s_lds32, s_misc);
-  if (tid == 0) __hip_atomic_store(a.counters + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (tid == 0) {
+    __hip_atomic_store(a.counters + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (a.k_new != nullptr) finish_append(a, bb, L, seq_ticket);
+  }
 }
 
 }  // namespace

@@ -110,6 +110,31 @@ def test_select_validation():
     expect(select(wsb=100), 3, "workspace")
 
 
+def append_select(**kw):
+    a = dict(c=C.byref(cache()), k=FAKE, v=FAKE, q=FAKE, hq=8, seq=FAKE, mx=1000,
+             p=C.byref(L.SelectParams(0.9, 4, 1)), idx=FAKE, ns=FAKE, n_cap=64, sc=None,
+             ws=FAKE, wsb=1 << 20, st=None)
+    a.update(kw)
+    return L.lib().resa_append_select(*a.values())
+
+
+def test_append_select_validation():
+    expect(append_select(k=None), 1, "k_new")
+    expect(append_select(v=FAKE + 2), 1, "v_new")
+    expect(append_select(mx=1024), 4, "cache full")
+    expect(append_select(mx=-1), 1, "max_seq_len")
+    expect(append_select(hq=7), 1, "num_q_heads")
+    expect(append_select(n_cap=3), 4, "n_cap")
+    expect(append_select(wsb=100), 3, "workspace")
+    # n_cap and the workspace are sized for one token more than max_seq_len.
+    lib = L.lib()
+    n = lib.resa_num_selected(64, 0.9, 4, 1)
+    expect(append_select(mx=1008, n_cap=lib.resa_num_selected(63, 0.9, 4, 1) - 1), 4, "n_cap")
+    assert n >= 4
+    need = lib.resa_select_workspace_size(2, 2, 1009, 16)
+    expect(append_select(mx=1008, wsb=need - 1), 3, "workspace")
+
+
 def decode(**kw):
     a = dict(c=C.byref(cache()), q=FAKE, hq=8, seq=FAKE, idx=FAKE, ns=FAKE, n_cap=16, S=0,
              sc=0.088, out=FAKE, lse=None, ws=FAKE, wsb=16, st=None)

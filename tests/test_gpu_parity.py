@@ -355,6 +355,53 @@ def test_decode_deterministic():
     assert torch.equal(idx, idx2) and torch.equal(a, b) and torch.equal(la, lb)
 
 
+@pytest.mark.parametrize("b,n_local,M", [(16, 1, 40), (16, 0, 40), (32, 1, 40), (64, 0, 40),
+                                         (16, 1, 33000)])
+def test_append_select_matches_separate(b, n_local, M):
+    """resa_append_select == resa_append_kv then resa_select_blocks, bit for
+    bit: ids, counts, scores, cache rows, summaries and lengths, over three
+    steps with appends that open a block and appends inside one (M = 33000
+    takes the standalone top-n kernel)."""
+    B = 3 if M < 1000 else 1
+    H, g = 2, 4
+    cap = M * b
+    rng = np.random.default_rng(b * 100 + n_local + M)
+    lens0 = [cap - 3 * b, cap // 2 - 1, cap // 3 + 5][:B]
+    Kf = rng.standard_normal((B, H, cap, 128)).astype(np.float32)
+    Vf = rng.standard_normal((B, H, cap, 128)).astype(np.float32)
+    K, V = W.f32_to_bf16_bits(Kf), W.f32_to_bf16_bits(Vf)
+    del Kf, Vf
+    c1 = make_cache(K, V, b, sentinel=False)
+    c2 = make_cache(K, V, b, sentinel=False)
+    l1, l2 = i32(lens0), i32(lens0)
+    R.block_summarize(c1, l1)
+    R.block_summarize(c2, l2)
+    ws1, ws2 = R.Workspace(dev()), R.Workspace(dev())
+    bound = max(lens0)
+    for step in range(3):
+        kn = W.f32_to_bf16_bits(rng.standard_normal((B, H, 128)).astype(np.float32))
+        vn = W.f32_to_bf16_bits(rng.standard_normal((B, H, 128)).astype(np.float32))
+        q = W.f32_to_bf16_bits(rng.standard_normal((B, H * g, 128)).astype(np.float32))
+        mseq = -(-(bound + 1) // b)
+        n_cap = R.num_selected(mseq, 0.9, 2, n_local)
+        s1 = torch.full((B, H, mseq), float("nan"), device=dev())
+        s2 = torch.full((B, H, mseq), float("nan"), device=dev())
+        R.append_kv(c1, up(kn), up(vn), l1, bound)
+        i1, n1 = R.select_blocks(c1, up(q), l1, bound + 1, 0.9, 2, n_local, n_cap=n_cap,
+                                 scores_out=s1, workspace=ws1)
+        i2, n2 = R.append_select(c2, up(kn), up(vn), up(q), l2, bound, 0.9, 2, n_local,
+                                 n_cap=n_cap, scores_out=s2, workspace=ws2)
+        torch.cuda.synchronize()
+        assert torch.equal(l1, l2)
+        assert torch.equal(n1, n2) and torch.equal(i1, i2)
+        assert torch.equal(s1.isnan(), s2.isnan())
+        assert torch.equal(torch.nan_to_num(s1), torch.nan_to_num(s2))
+        bound += 1
+    assert l2.cpu().tolist() == [x + 3 for x in lens0]
+    for name in ("k", "v", "kmin", "kmax"):
+        assert torch.equal(getattr(c1, name), getattr(c2, name)), name
+
+
 # -------------------------------------------------------------------- rectify
 
 @pytest.mark.parametrize("g,f", [(4, 16), (4, 1), (7, 32), (8, 32), (2, 64)])
@@ -406,9 +453,11 @@ def test_rectify_tiny4k_full():
 
 # ---------------------------------------------------------------- decode loop
 
-def test_decode_loop_small():
+@pytest.mark.parametrize("fused", [False, True])
+def test_decode_loop_small(fused):
     """Kernel-level Alg. 1 loop (append, select, decode; rectify every f steps)
-    on a reduced copy of the 64K batch-8 workload (outlier key channels)."""
+    on a reduced copy of the 64K batch-8 workload (outlier key channels);
+    `fused` runs the append and the selection as one resa_append_select."""
     w = W.LONG_64K.with_(batch=2, num_q_heads=8, num_kv_heads=2, seq_len=600, min_tokens=64,
                          seed_tag="loop")
     f, steps, cap = 16, 40, 704
@@ -422,9 +471,14 @@ def test_decode_loop_small():
     for step in range(steps):
         kn, vn = W.decode_kv(w, step)
         q = W.decode_query(w, step)
-        R.append_kv(cache, up(kn), up(vn), lt, max(st.L))
-        st.append(O.bf16_to_f64(kn), O.bf16_to_f64(vn))
-        idx, ns = R.select_blocks(cache, up(q), lt, max(st.L), w.sparsity, w.min_blocks, 1)
+        if fused:
+            idx, ns = R.append_select(cache, up(kn), up(vn), up(q), lt, max(st.L), w.sparsity,
+                                      w.min_blocks, 1)
+            st.append(O.bf16_to_f64(kn), O.bf16_to_f64(vn))
+        else:
+            R.append_kv(cache, up(kn), up(vn), lt, max(st.L))
+            st.append(O.bf16_to_f64(kn), O.bf16_to_f64(vn))
+            idx, ns = R.select_blocks(cache, up(q), lt, max(st.L), w.sparsity, w.min_blocks, 1)
         out, _ = R.sparse_decode(cache, up(q), lt, idx, ns)
         rs, ri, rn = st.select(O.bf16_to_f64(q), w.sparsity, w.min_blocks, 1)
         ro, _ = st.attend(O.bf16_to_f64(q), ri, w.sm_scale)
