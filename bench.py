@@ -202,8 +202,10 @@ def main():
     out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
     lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
     splits = R.decode_num_splits(B, H, n_cap, b)
-    ws_sel = torch.zeros(max(lb.resa_select_workspace_size(B, H, cap, b), 256), dtype=torch.uint8,
-                         device=dev)
+    # One selection workspace per layer: besides scratch it carries the
+    # digit-window hint of the layer's previous call.
+    ws_sels = [torch.zeros(max(lb.resa_select_workspace_size(B, H, cap, b), 256), dtype=torch.uint8,
+                           device=dev) for _ in range(nlay)]
     ws_dec = torch.zeros(lb.resa_decode_workspace_size(B, H, Hq, n_cap, b, splits), dtype=torch.uint8,
                          device=dev)
     ws_rec = torch.zeros(lb.resa_rectify_workspace_size(B, H, Hq, f, cap), dtype=torch.uint8, device=dev)
@@ -238,14 +240,14 @@ def main():
         if phase == "append_select":
             check(lb.resa_append_select(d, ly["k"][s].data_ptr(), ly["v"][s].data_ptr(), ly["q"][s].data_ptr(),
                                         Hq, ly["lens"].data_ptr(), Lcur, C.byref(params), ids.data_ptr(),
-                                        ns.data_ptr(), n_cap, None, ws_sel.data_ptr(), ws_sel.numel(), sptr))
+                                        ns.data_ptr(), n_cap, None, ws_sels[li].data_ptr(), ws_sels[li].numel(), sptr))
         elif phase == "append":
             check(lb.resa_append_kv(d, ly["k"][s].data_ptr(), ly["v"][s].data_ptr(),
                                     ly["lens"].data_ptr(), Lcur, sptr))
         elif phase == "select":
             check(lb.resa_select_blocks(d, ly["q"][s].data_ptr(), Hq, ly["lens"].data_ptr(), Lcur + 1,
                                         C.byref(params), ids.data_ptr(), ns.data_ptr(), n_cap, None,
-                                        ws_sel.data_ptr(), ws_sel.numel(), sptr))
+                                        ws_sels[li].data_ptr(), ws_sels[li].numel(), sptr))
         elif phase == "decode":
             if args.dense:
                 ids = all_idx

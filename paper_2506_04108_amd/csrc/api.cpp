@@ -99,19 +99,21 @@ int hip_fail(hipError_t e, const char* what) {
 }
 
 struct SelectLayout {
-  size_t counters, seq_counters, hist, scores, total;
+  size_t counters, seq_counters, window, hist, scores, total;
 };
 
 // Workspace of resa_select_blocks / resa_append_select: one ticket per group
-// and one per sequence (zero between calls), per-workgroup key-digit counts,
-// and the scores (rows padded to 4 floats).
+// and one per sequence (zero between calls), one digit-window hint per group
+// (kept from call to call; any value is valid), per-workgroup key-digit
+// counts, and the scores (rows padded to 4 floats).
 SelectLayout select_layout(int32_t batch, int32_t kv_heads, int32_t max_seq_len, int32_t block_size) {
   SelectLayout l;
   const size_t groups = (size_t)batch * kv_heads;
   const size_t mseq = ((size_t)max_seq_len + block_size - 1) / block_size;
   l.counters = 0;
   l.seq_counters = groups * 4;
-  l.hist = round256((groups + (size_t)batch) * 4);
+  l.window = (groups + (size_t)batch) * 4;
+  l.hist = round256((2 * groups + (size_t)batch) * 4);
   l.scores = l.hist + round256(groups * (size_t)resa::select_hist_words(batch, kv_heads, (int32_t)mseq) * 4);
   l.total = l.scores + groups * ((mseq + 3) & ~size_t(3)) * sizeof(float);
   return l;
@@ -266,6 +268,7 @@ int select_common(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
   a.v_new = static_cast<const uint16_t*>(v_new);
   a.lens_out = const_cast<int32_t*>(seq_lens);
   a.seq_counters = reinterpret_cast<uint32_t*>(ws + lay.seq_counters);
+  a.window = reinterpret_cast<uint32_t*>(ws + lay.window);
   hipError_t e = resa::launch_select(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, what);
   return ok();

@@ -224,6 +224,10 @@ __device__ void merge_tail(const DecodeArgs& a, size_t grp, int S, size_t ob, fl
     }
   };
   issue(0);
+  // Every split has taken its ticket: reset the counter for the next call.
+  // The store goes out after the loads (a wave's memory counter drains in
+  // issue order), so it does not delay their use.
+  if (tid == 0) __hip_atomic_store(a.counters + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll
   for (int j = 0; j < kLse; ++j) {
     const int i = tid + NT * j;
@@ -446,7 +450,6 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void k_decode(DecodeArgs a) {
   __syncthreads();
   if (s_ticket != (uint32_t)(S - 1)) return;
   merge_tail<G>(a, grp, S, ob, s_w, s_red);
-  if (threadIdx.x == 0) __hip_atomic_store(a.counters + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <int G>

@@ -52,6 +52,7 @@ struct SelectArgs {
   const uint16_t* v_new;       // [B, Hkv, D] value of the new token
   int32_t* lens_out;           // seq_lens, written once every group of the sequence is done
   uint32_t* seq_counters;      // [B], zero between calls
+  uint32_t* window;            // [B, Hkv] digit-window hint kept across calls (any value is valid)
 };
 
 struct DecodeArgs {

@@ -10,6 +10,7 @@ constexpr int kSelThreads = 1024;                 // 16 waves
 constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kTopnThreads = 1024;
 constexpr int kBins1 = 256;                       // first digit: key bits 31..24
+constexpr int kSlotWords = 256;                   // per-workgroup slot: two 256-bin 16-bit histograms
 constexpr int kBins2 = 4096;                      // next digits: bits 23..12, then 11..0
 constexpr int kKeysPerLane = 32;                  // fused top-n: M <= 1024 threads x 32
 constexpr int kMaxBlocksPerWg = 4096;             // scores staged in LDS per workgroup
@@ -49,22 +50,24 @@ __device__ __forceinline__ void finish_append(const SelectArgs& a, int bb, int L
 }
 
 // Exclusive prefix sum over the 1024 threads of the workgroup; returns the
-// thread's exclusive prefix and writes the total to *total.
+// thread's exclusive prefix and writes the total to *total. Waves scan with
+// DPP, publish their totals, and every thread adds the totals of the waves
+// before its own.
 __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* lds16, uint32_t* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint32_t x = wave_incl_scan(v);
   if (lane == 63) lds16[wave] = x;
   lds_sync();
-  if (wave == 0) {
-    const uint32_t t = wave_incl_scan(lane < 16 ? lds16[lane] : 0u);
-    if (lane < 16) lds16[16 + lane] = t;  // inclusive wave offsets
+  uint32_t off = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kSelWaves; ++w) {
+    const uint32_t t = lds16[w];
+    off += w < wave ? t : 0u;
+    tot += t;
   }
-  lds_sync();
-  const uint32_t wave_off = wave == 0 ? 0u : lds16[16 + wave - 1];
-  *total = lds16[16 + 15];
-  const uint32_t r = wave_off + x - v;
+  *total = tot;
   lds_sync();  // lds16 may be reused by the next scan
-  return r;
+  return off + x - v;
 }
 
 // Exact top-n per (sequence, kv head): an MSD radix select over order-
@@ -220,7 +223,7 @@ __device__ void find_digit(const uint32_t* hist, int nbins, uint32_t k, uint32_t
   lds_sync();
 }
 
-constexpr uint32_t kMaxCand = 256;  // bucket size resolved by ranking instead of a third pass
+constexpr uint32_t kMaxCand = 256;  // bucket size resolved by ranking (4 threads per candidate)
 
 // Exact top-n of one group by its last workgroup (M <= 1024 * NJ). Thread t
 // holds the keys of ids [t NJ, t NJ + NJ) in registers, so id order is
@@ -238,12 +241,17 @@ constexpr uint32_t kMaxCand = 256;  // bucket size resolved by ranking instead o
 // unrolled per-thread loops do no more work than the group needs.
 template <int NJ>
 __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int M, int forced_from, int W,
-                                            uint32_t* s_hist, uint32_t* lds32, uint32_t* misc) {
+                                            uint32_t win, uint32_t* s_hist, uint32_t* lds32, uint32_t* misc,
+                                            int32_t* s_out, int bb, int L, uint32_t seq_ticket) {
   const int tid = threadIdx.x;
   const int n = count_selected(M, a.keep_ppm, a.min_blocks, a.n_local);
   int32_t* out = a.block_idx + grp * a.n_cap;
-  if (tid == 0) a.num_sel[grp] = n;
   if (n == 0 || n >= M) {
+    if (tid == 0) {
+      a.num_sel[grp] = n;
+      __hip_atomic_store(a.counters + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (a.k_new != nullptr) finish_append(a, bb, L, seq_ticket);
+    }
     for (int i = tid; i < a.n_cap; i += kSelThreads) out[i] = i < n ? i : -1;
     return;
   }
@@ -252,6 +260,19 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
   // wholly inside the row or wholly past it (then it reads 0); ids past M
   // are never used.
   const __amdgpu_buffer_rsrc_t rs = buf_rsrc(a.scores + grp * a.score_stride, (uint32_t)((M + 3) & ~3) * 4);
+  // The digit search needs only the group's W slots (word d holds two 16-bit
+  // counts): word d gets 4 threads, each summing every 4th slot. The first
+  // round of slot loads is issued before the key loads, so the slot sums can
+  // be used while the keys are still arriving.
+  const uint32_t* slots = a.hist + grp * W * kSlotWords;
+  const int sd = tid & (kSlotWords - 1), spart = tid / kSlotWords;
+  constexpr int kParts = kSelThreads / kSlotWords;
+  uint32_t sv[16];
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const int w = spart + j * kParts;
+    sv[j] = w < W ? __hip_atomic_load(slots + w * kSlotWords + sd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+  }
   float raw[NJ];
   if constexpr (NJ % 4 == 0) {
 #pragma unroll
@@ -268,86 +289,187 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
       raw[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (id0 + i) * 4, 0, kSc1));
   }
 
+  // Stores go out after the loads: a wave's memory counter drains in issue
+  // order, so a store issued before a load would make the load's consumer
+  // wait for the store's acknowledgement too. Every workgroup of the group
+  // has taken its ticket, so the counter can be reset for the next call.
+  if (tid == 0) {
+    a.num_sel[grp] = n;
+    __hip_atomic_store(a.counters + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
   {
-    // Sum the group's W slots: digit d gets 4 threads, each summing every 4th
-    // slot with independent loads (16 per round).
-    const uint32_t* slots = a.hist + grp * W * kBins1;
-    const int d = tid & (kBins1 - 1), part = tid / kBins1;
-    constexpr int kParts = kSelThreads / kBins1;
-    if (tid < kBins1) s_hist[tid] = 0;
+    // Bins 0..255 of s_hist get the top-byte counts, 256..511 the window
+    // counts.
+    if (tid < 2 * kSlotWords) s_hist[tid] = 0;
     if (tid == 0) misc[4] = 0;  // candidate counter of the ranking step (misc[3] holds the ticket)
     lds_sync();
-    uint32_t sum = 0;
-    for (int w0 = part; w0 < W; w0 += 16 * kParts) {
+    uint32_t lo = 0, hi = 0;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      lo += sv[j] & 0xFFFFu;
+      hi += sv[j] >> 16;
+    }
+    for (int w0 = spart + 16 * kParts; w0 < W; w0 += 16 * kParts) {
       uint32_t v[16];
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         const int w = w0 + j * kParts;
-        v[j] = w < W ? __hip_atomic_load(slots + w * kBins1 + d, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+        v[j] = w < W ? __hip_atomic_load(slots + w * kSlotWords + sd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
       }
 #pragma unroll
-      for (int j = 0; j < 16; ++j) sum += v[j];
+      for (int j = 0; j < 16; ++j) {
+        lo += v[j] & 0xFFFFu;
+        hi += v[j] >> 16;
+      }
     }
-    atomicAdd(&s_hist[d], sum);
+    atomicAdd(&s_hist[2 * sd], lo);
+    atomicAdd(&s_hist[2 * sd + 1], hi);
     lds_sync();
   }
 
+
+  // Window hint: keys whose top 9 bits equal W9 were also counted by bits
+  // 22..15. When the n-th largest key falls inside that window, those counts
+  // pin 17 bits at once; otherwise the top-byte counts give 8.
+  uint32_t prefix, pmask, k = (uint32_t)n;
+  int known;
+  bool in_win = false;
+  if (win >> 31) {
+    const uint32_t w9 = win & 0x1FFu, w8 = w9 >> 1;
+    // Keys in the window, and keys above it.
+    uint32_t inw = 0, above = 0;
+    if (tid < 64) {
+      uint32_t x = 0, y = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        x += s_hist[256 + 4 * tid + j];
+        const uint32_t t8 = 4 * tid + j;
+        y += t8 > w8 ? s_hist[t8] : 0u;
+      }
+      x = wave_incl_scan(x);
+      y = wave_incl_scan(y);
+      inw = (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+      above = (uint32_t)__builtin_amdgcn_readlane((int)y, 63);
+      // The other half of the window's top byte lies above it when W9 is even.
+      if ((w9 & 1u) == 0) above += s_hist[w8] - inw;
+      if (tid == 0) {
+        misc[5] = inw;
+        misc[6] = above;
+      }
+    }
+    lds_sync();
+    inw = misc[5];
+    above = misc[6];
+    in_win = above < k && k <= above + inw;
+    if (in_win) {
+      find_digit(s_hist + 256, 256, k - above, lds32, misc);
+      prefix = (w9 << 23) | (misc[0] << 15);
+      pmask = 0xFFFF8000u;
+      known = 17;
+    }
+  }
+  if (!in_win) {
+    find_digit(s_hist, kBins1, k, lds32, misc);
+    prefix = misc[0] << 24;
+    pmask = 0xFFu << 24;
+    known = 8;
+  }
+  k = misc[1];
+  uint32_t cnt = misc[2];
+  // Keys are first needed here; their loads overlapped the digit search.
   uint32_t key[NJ];
 #pragma unroll
   for (int i = 0; i < NJ; ++i) key[i] = block_key(id0 + i, forced_from, raw[i]);
   const int nv = min(max(M - id0, 0), NJ);  // this thread's valid keys: j < nv
-
-  uint32_t prefix, pmask, k = (uint32_t)n;
-  find_digit(s_hist, kBins1, k, lds32, misc);
-  prefix = misc[0] << 24;
-  pmask = 0xFFu << 24;
-  k = misc[1];
-  uint32_t cnt = misc[2];
-  for (int shift = 12; shift >= 0 && cnt != k; shift -= 12) {
+  while (known < 32 && cnt != k) {
     if (cnt <= kMaxCand) {
       // Rank the bucket's keys among themselves: the one with k - 1 keys
-      // before it in (key descending, id ascending) order is the n-th.
-      uint32_t* ck = s_hist;              // candidate keys
-      uint32_t* ci = s_hist + kMaxCand;   // candidate ids
+      // before it in (key descending, id ascending) order is the n-th. A
+      // candidate is stored as (key << 32 | ~id), so that order is plain
+      // 64-bit descending order. Each wave reserves room for its candidates
+      // with one LDS atomic.
+      uint64_t* cv = reinterpret_cast<uint64_t*>(s_hist);
+      uint32_t mine = 0;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) mine += (j < nv && (key[j] & pmask) == prefix);
+      const uint32_t incl = wave_incl_scan(mine);
+      const uint32_t wave_tot = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+      uint32_t base = 0;
+      if ((tid & 63) == 63 && wave_tot != 0) base = atomicAdd(&misc[4], wave_tot);
+      uint32_t at = (uint32_t)__builtin_amdgcn_readlane((int)base, 63) + incl - mine;
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
         if (j < nv && (key[j] & pmask) == prefix) {
-          const uint32_t at = atomicAdd(&misc[4], 1u);
-          ck[at] = key[j];
-          ci[at] = (uint32_t)(id0 + j);
+          cv[at] = ((uint64_t)key[j] << 32) | (uint32_t)~(uint32_t)(id0 + j);
+          ++at;
         }
       }
       lds_sync();
-      if ((uint32_t)tid < cnt) {
-        const uint32_t kt = ck[tid], it = ci[tid];
-        uint32_t before = 0, eq_before = 0;
-        for (uint32_t j = 0; j < cnt; ++j) {
-          const uint32_t kj = ck[j], ij = ci[j];
-          before += (kj > kt) || (kj == kt && ij < it);
-          eq_before += (kj == kt && ij < it);
+      {
+        // Four threads per candidate (lanes 4c .. 4c + 3 of one wave), each
+        // counting over a quarter of the bucket; the quarters are added with
+        // DPP quad swaps.
+        const uint32_t cand = (uint32_t)tid >> 2, part = (uint32_t)tid & 3u;
+        uint32_t before = 0, gtk = 0, kt = 0;
+        if (cand < cnt) {
+          const uint64_t vt = cv[cand];
+          kt = (uint32_t)(vt >> 32);
+          const uint32_t qlen = (cnt + 3) >> 2;
+          const uint32_t j1 = min((part + 1) * qlen, cnt);
+          uint32_t j = part * qlen;
+          for (; j + 8 <= j1; j += 8) {
+            uint64_t v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = cv[j + u];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              before += v[u] > vt;
+              gtk += (uint32_t)(v[u] >> 32) > kt;
+            }
+          }
+          for (; j < j1; ++j) {
+            const uint64_t vj = cv[j];
+            before += vj > vt;
+            gtk += (uint32_t)(vj >> 32) > kt;
+          }
         }
-        if (before == k - 1) {
+        before += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)before, kDppXor1, 0xf, 0xf, true);
+        before += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)before, kDppXor2, 0xf, 0xf, true);
+        gtk += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)gtk, kDppXor1, 0xf, 0xf, true);
+        gtk += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)gtk, kDppXor2, 0xf, 0xf, true);
+        if (cand < cnt && part == 0 && before == k - 1) {
           misc[0] = kt;
-          misc[1] = eq_before + 1;  // keys equal to T that are kept
+          misc[1] = before - gtk + 1;  // keys equal to T that are kept (lowest ids)
         }
       }
       lds_sync();
       prefix = misc[0];
       pmask = 0xFFFFFFFFu;
       k = misc[1];
+      known = 32;
       break;
     }
-    for (int i = tid; i < kBins2; i += kSelThreads) s_hist[i] = 0;
+    // Next digit: up to 12 bits below the known prefix.
+    const int width = min(12, 32 - known), shift = 32 - known - width;
+    const uint32_t dmask = (1u << width) - 1u;
+    for (int i = tid; i < (1 << width); i += kSelThreads) s_hist[i] = 0;
     lds_sync();
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
-      if (j < nv && (key[j] & pmask) == prefix) atomicAdd(&s_hist[(key[j] >> shift) & 0xFFFu], 1u);
+      if (j < nv && (key[j] & pmask) == prefix) atomicAdd(&s_hist[(key[j] >> shift) & dmask], 1u);
     lds_sync();
-    find_digit(s_hist, kBins2, k, lds32, misc);
+    find_digit(s_hist, 1 << width, k, lds32, misc);
     prefix |= misc[0] << shift;
-    pmask |= 0xFFFu << shift;
+    pmask |= dmask << shift;
+    known += width;
     k = misc[1];
     cnt = misc[2];
+  }
+  // The next call's window: the top 9 bits of this threshold. The stores
+  // here go out before the compaction so their latency overlaps it.
+  if (tid == 0) {
+    if (a.k_new != nullptr) finish_append(a, bb, L, seq_ticket);
+    a.window[grp] = 0x80000000u | (prefix >> 23);
   }
 
   // Per-thread counts above T and equal to T (each <= NJ, totals <= M < 2^16).
@@ -362,6 +484,24 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
   const uint32_t before = block_exclusive_scan((gt << 16) | eq, lds32, &tot);
   uint32_t e = before & 0xFFFFu;
   uint32_t pos = (before >> 16) + min(e, k);
+  if (a.n_cap < kMaxBlocksPerWg) {
+    // Rows shorter than the workgroup's score staging area (free by now) are
+    // assembled there and written out coalesced. The loop is branch-free:
+    // ids not kept are written to the spare last slot.
+    constexpr uint32_t kSpare = kMaxBlocksPerWg - 1;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const uint32_t km = key[j] & pmask;
+      const bool q = j < nv && km == prefix;
+      const bool take = (j < nv && km > prefix) || (q && e < k);
+      e += q ? 1u : 0u;
+      s_out[(take && pos < (uint32_t)a.n_cap) ? pos : kSpare] = id0 + j;
+      pos += take ? 1u : 0u;
+    }
+    lds_sync();
+    for (int i = tid; i < a.n_cap; i += kSelThreads) out[i] = i < n ? s_out[i] : -1;
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
     const uint32_t km = key[j] & pmask;
@@ -397,7 +537,7 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
 // between workgroups.
 template <int NJ>
 __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
-  __shared__ uint32_t s_hist[kBins2];
+  __shared__ __attribute__((aligned(16))) uint32_t s_hist[kBins2];
   __shared__ __attribute__((aligned(16))) float s_score[kMaxBlocksPerWg];
   __shared__ uint32_t s_lds32[32];
   __shared__ uint32_t s_misc[8];
@@ -426,10 +566,20 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
     if (row_writer && tid >= 16) vnew = ld16(a.v_new + grp * kHeadDim + col);
   }
 
+  // Window hint left by the previous call on this workspace (any value is
+  // valid: it only chooses which key bits get a second histogram).
+  const uint32_t win = a.fused ? a.window[grp] : 0u;
+  const bool win_on = (win >> 31) != 0;
+  const uint32_t w9 = win & 0x1FFu;
   if (a.fused) {
-    for (int i = tid; i < kBins1; i += kSelThreads) s_hist[i] = 0;
+    for (int i = tid; i < 2 * kSlotWords; i += kSelThreads) s_hist[i] = 0;
     lds_sync();
   }
+  // The appended block's updated summary row, held by the lanes that score
+  // it and stored after the loop (a store inside it would hold up that
+  // wave's next tile: the memory counter drains in issue order).
+  U4 new_lo = U4{0, 0, 0, 0}, new_hi = U4{0, 0, 0, 0};
+  bool owns_row = false;
   if (b0 < b1) {
     float qb[8];
 #pragma unroll
@@ -474,8 +624,9 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
         if (mu == m_new && mu < b1) {
           lo4[u] = opening ? knew : u4_min(lo4[u], knew);
           hi4[u] = opening ? knew : u4_max(hi4[u], knew);
-          st16(const_cast<uint16_t*>(kmin) + (size_t)mu * kHeadDim, lo4[u]);
-          st16(const_cast<uint16_t*>(kmax) + (size_t)mu * kHeadDim, hi4[u]);
+          new_lo = lo4[u];
+          new_hi = hi4[u];
+          owns_row = true;
         }
         const uint32_t wl[4] = {lo4[u].x, lo4[u].y, lo4[u].z, lo4[u].w};
         const uint32_t wh[4] = {hi4[u].x, hi4[u].y, hi4[u].z, hi4[u].w};
@@ -491,7 +642,11 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
         const int m = b0 + 16 * t + 4 * u + r;
         if (c == 0 && m < b1) {
           s_score[m - b0] = s;
-          if (a.fused) atomicAdd(&s_hist[block_key(m, forced_from, s) >> 24], 1u);
+          if (a.fused) {
+            const uint32_t key = block_key(m, forced_from, s);
+            atomicAdd(&s_hist[key >> 24], 1u);
+            if (win_on && (key >> 23) == w9) atomicAdd(&s_hist[256 + ((key >> 15) & 0xFFu)], 1u);
+          }
         }
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -504,6 +659,11 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
     }
   }
   lds_sync();
+  if (owns_row) {
+    const size_t so = (grp * a.c.max_blocks + m_new) * kHeadDim + col;
+    st16(a.c.kmin + so, new_lo);
+    st16(a.c.kmax + so, new_hi);
+  }
   if (row_writer) {
     // The new K and V rows (stored after the scoring, so the loads above have
     // long arrived).
@@ -530,9 +690,11 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
   }
   if (!a.fused) return;
   // This workgroup's digit counts go to its own slot: no shared counters.
-  uint32_t* slot = a.hist + (grp * gridDim.x + blockIdx.x) * kBins1;
-  for (int i = tid; i < kBins1; i += kSelThreads)
-    __hip_atomic_store(slot + i, s_hist[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  // Counts fit in 16 bits (at most kMaxBlocksPerWg per workgroup): two per word.
+  uint32_t* slot = a.hist + (grp * gridDim.x + blockIdx.x) * kSlotWords;
+  for (int i = tid; i < kSlotWords; i += kSelThreads)
+    __hip_atomic_store(slot + i, s_hist[2 * i] | (s_hist[2 * i + 1] << 16), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
   __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (tid == 0)
@@ -546,11 +708,8 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
   uint32_t seq_ticket = 0;
   if (a.k_new != nullptr && tid == 0)
     seq_ticket = __hip_atomic_fetch_add(a.seq_counters + bb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  select_tail<NJ>(a, grp, M, forced_from, W, s_hist, s_lds32, s_misc);
-  if (tid == 0) {
-    __hip_atomic_store(a.counters + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (a.k_new != nullptr) finish_append(a, bb, L, seq_ticket);
-  }
+  select_tail<NJ>(a, grp, M, forced_from, W, win, s_hist, s_lds32, s_misc,
+                  reinterpret_cast<int32_t*>(s_score), bb, L, seq_ticket);
 }
 
 }  // namespace
@@ -602,7 +761,7 @@ int32_t select_blocks_per_wg(int32_t batch, int32_t kv_heads, int32_t max_blocks
 int32_t select_hist_words(int32_t batch, int32_t kv_heads, int32_t max_blocks_seq) {
   const int32_t bpw = select_blocks_per_wg(batch, kv_heads, max_blocks_seq);
   const int32_t wgs = (max_blocks_seq + bpw - 1) / bpw;
-  return wgs * kBins1;
+  return wgs * kSlotWords;
 }
 
 }  // namespace resa

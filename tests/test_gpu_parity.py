@@ -231,6 +231,33 @@ def test_select_reused_workspace():
     assert np.all(tickets == 0)
 
 
+@pytest.mark.parametrize("L", [4800, 80000])
+def test_select_window_hint(L):
+    """The digit-window hint a call leaves in the workspace must never change
+    the result: queries scaled by powers of two (and negated) move the score
+    distribution so the hint hits, misses above and misses below; every call
+    must equal a call on a fresh workspace and the oracle."""
+    w, cap = small(g=4, L=L, cap=L + 64, B=1, H=2, tag=f"win{L}")
+    K, V = W.kv_cache(w, capacity=cap)
+    cache = make_cache(K, V, 16)
+    lt = i32([L])
+    R.block_summarize(cache, lt)
+    ws = R.Workspace(dev())
+    st = O.DecodeState(O.bf16_to_f64(K), O.bf16_to_f64(V), [L], 16)
+    q0 = W.bf16_bits_to_f32(W.decode_query(w, 0))
+    for scale in [1.0, 1.0, 4.0, 0.25, -1.0, 1.0, 64.0]:
+        q = W.f32_to_bf16_bits(q0 * scale)
+        idx, ns = R.select_blocks(cache, up(q), lt, L, 0.9, 4, 1, workspace=ws)
+        idx2, ns2 = R.select_blocks(cache, up(q), lt, L, 0.9, 4, 1)
+        torch.cuda.synchronize()
+        assert torch.equal(idx, idx2) and torch.equal(ns, ns2)
+        rs, ri, rn = st.select(O.bf16_to_f64(q), 0.9, 4, 1)
+        gi, gn = idx.cpu().numpy(), ns.cpu().numpy()
+        for hi in range(2):
+            assert gn[0, hi] == rn[0, hi]
+            check_selection(gi[0, hi, :gn[0, hi]], ri[0, hi], rs[0, hi], rn[0, hi], 1)
+
+
 def test_select_planted_blocks_win():
     w = W.TINY_4K.with_(plant_norm=math.sqrt(128), seed_tag="strong")
     q = W.decode_query(w)
