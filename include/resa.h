@@ -150,7 +150,11 @@ size_t resa_select_workspace_size(int32_t batch, int32_t num_kv_heads,
  * finish, selects them (groups of more than 32768 blocks use a second
  * kernel). The workspace starts with one ticket per group: zero-fill it
  * before its first use (resa_workspace_clear); every call leaves the tickets
- * at zero again. Calls sharing a workspace must be ordered on one stream.
+ * at zero again. It also keeps, per group, a hint from the previous call
+ * (which bits of the scores to count twice); the hint never changes the
+ * result, only how fast the threshold is found, so reusing one workspace per
+ * attention layer keeps it matched to that layer's scores. Calls sharing a
+ * workspace must be ordered on one stream.
  */
 int resa_select_blocks(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
                        const int32_t* seq_lens, int32_t max_seq_len,
