@@ -53,6 +53,8 @@ def parse():
     p.add_argument("--sparsity", type=float, default=None)
     p.add_argument("--rectify-every", type=int, default=None)
     p.add_argument("--dense", action="store_true", help="dense baseline: decode over every block")
+    p.add_argument("--breakdown", action="store_true",
+                   help="latency breakdown at 16K/64K/256K (batch 8) against dense decoding")
     p.add_argument("--separate", action="store_true",
                    help="append and select as two launches instead of resa_append_select")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -149,21 +151,14 @@ def cpu_baseline(w, budget_s):
                        f"{f} rows amortised over {f} steps, scaled to all {groups} groups")}
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no "
-              "multi-GPU path.", file=sys.stderr)
-        sys.exit(2)
-
-    import numpy as np
+def measure(args, w, dense: bool) -> dict:
+    """Runs the decode loop of workload `w` and returns the result fields."""
     import torch
 
     import paper_2506_04108_amd as R
-    from paper_2506_04108_amd._lib import KVCacheDesc, SelectParams, check, lib
+    from paper_2506_04108_amd._lib import SelectParams, check, lib
     import workloads.device as WD
 
-    w = workload_of(args)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     L0, B, H, Hq, D, b = w.seq_len, w.batch, w.num_kv_heads, w.num_q_heads, w.head_dim, w.block_size
@@ -177,7 +172,7 @@ def main():
     sptr = stream.cuda_stream
     lb = lib()
 
-    log(f"[bench] {describe(w, nlay, args.dense)}; capacity {cap}")
+    log(f"[bench] {describe(w, nlay, dense)}; capacity {cap}")
     t_gen = time.perf_counter()
     layers = []
     for li in range(nlay):
@@ -193,7 +188,7 @@ def main():
     log(f"[bench] inputs ready in {time.perf_counter() - t_gen:.1f}s")
 
     mcap = cap // b
-    if args.dense:
+    if dense:
         n_cap = mcap
     else:
         n_cap = R.num_selected(mcap, w.sparsity, w.min_blocks, w.n_local)
@@ -214,7 +209,7 @@ def main():
     sm = 1.0 / math.sqrt(D)
 
     # Dense baseline: every block id in order, count = M (decode only).
-    if args.dense:
+    if dense:
         all_idx = torch.arange(n_cap, dtype=torch.int32, device=dev).repeat(B, H, 1).contiguous()
 
     # Rectification rows are prepared ahead (inputs, not timed work).
@@ -249,7 +244,7 @@ def main():
                                         C.byref(params), ids.data_ptr(), ns.data_ptr(), n_cap, None,
                                         ws_sels[li].data_ptr(), ws_sels[li].numel(), sptr))
         elif phase == "decode":
-            if args.dense:
+            if dense:
                 ids = all_idx
             check(lb.resa_sparse_decode(d, ly["q"][s].data_ptr(), Hq, ly["lens"].data_ptr(),
                                         ids.data_ptr(), ns.data_ptr(), n_cap, splits, sm, out.data_ptr(),
@@ -267,15 +262,15 @@ def main():
         ly = layers[li]
         s = ly["steps"]
         Lcur = L0 + s
-        if args.dense:
+        if dense:
             seq = ["append", "decode"]
         elif args.separate:
             seq = ["append", "select", "decode"]
         else:
             seq = ["append_select", "decode"]
-        if not args.dense and (s + 1) % f == 0:
+        if not dense and (s + 1) % f == 0:
             seq.append("rectify")
-        if args.dense:
+        if dense:
             (nsel_all[t] if t >= 0 else nsel).fill_(-(-(Lcur + 1) // b))
         for ph in seq:
             launch(ph, li, s, t, Lcur)
@@ -340,7 +335,7 @@ def main():
     bytes_dec = []
     for L in lens_seen:
         M = -(-L // b)
-        n = M if args.dense else R.num_selected(M, w.sparsity, w.min_blocks, w.n_local)
+        n = M if dense else R.num_selected(M, w.sparsity, w.min_blocks, w.n_local)
         bytes_dec.append(B * H * n * b * D * 2 * 2)
     avg_dec_us = phase_us["decode"]
     avg_bytes = sum(bytes_dec) / len(bytes_dec)
@@ -362,9 +357,9 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": describe(w, nlay, args.dense), "batch": B, "q_heads": Hq, "kv_heads": H,
+        "config": {"workload": describe(w, nlay, dense), "batch": B, "q_heads": Hq, "kv_heads": H,
                    "head_dim": D, "context_start": L0, "block_size": b,
-                   "sparsity": None if args.dense else w.sparsity, "min_tokens": w.min_tokens,
+                   "sparsity": None if dense else w.sparsity, "min_tokens": w.min_tokens,
                    "rectify_every": f, "decode_splits": splits, "layers_rotated": nlay},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
@@ -374,6 +369,47 @@ def main():
         "kernel_us_per_step": {k: round(v * n_calls[k] / args.steps, 2) for k, v in phase_us.items()},
         "wall_us_per_step": round(wall * 1e6 / args.steps, 2),
     }
+    return res
+
+
+def breakdown(args) -> dict:
+    """Per-kernel latency of one decode step at 16K, 64K and 256K context
+    (batch 8, the 64K workload's recipe), against a dense decode over every
+    block: sparse estimation (append + select), attention (decode) and
+    rectification (one call amortised over f steps)."""
+    import workloads as W
+    rows = []
+    for L in (16384, 65536, 262144):
+        w = W.LONG_64K.with_(seq_len=L)
+        sp = measure(args, w, False)
+        dn = measure(args, w, True)
+        k = sp["kernel_us_per_launch"]
+        f = w.rectify_every
+        est, att, rect = k["append_select"], k["decode"], k["rectify"] / f
+        tot = est + att + rect
+        rows.append({"context": L, "estimation_us": round(est, 2), "attention_us": round(att, 2),
+                     "rectification_us": round(rect, 2),
+                     "rectification_share": round(rect / tot, 4),
+                     "resa_kernel_us": round(tot, 2), "dense_decode_us": dn["kernel_us_per_launch"]["decode"],
+                     "speedup_vs_dense": round(dn["kernel_us_per_launch"]["decode"] / tot, 3),
+                     "decode_hbm_frac": sp["roofline"]["frac"],
+                     "dense_hbm_frac": dn["roofline"]["frac"]})
+    return {"breakdown": rows, "workload": describe(W.LONG_64K, args.layers, False)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no "
+              "multi-GPU path.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    torch.cuda.set_device(0)
+    if args.breakdown:
+        print(json.dumps(breakdown(args)), flush=True)
+        return
+    w = workload_of(args)
+    res = measure(args, w, args.dense)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)

@@ -13,7 +13,7 @@ constexpr int kBins1 = 256;                       // first digit: key bits 31..2
 constexpr int kSlotWords = 256;                   // per-workgroup slot: two 256-bin 16-bit histograms
 constexpr int kBins2 = 4096;                      // next digits: bits 23..12, then 11..0
 constexpr int kKeysPerLane = 32;                  // fused top-n: M <= 1024 threads x 32
-constexpr int kMaxBlocksPerWg = 4096;             // scores staged in LDS per workgroup
+constexpr int kMaxBlocksPerWg = 8192;             // scores staged in LDS per workgroup (32 KiB)
 constexpr int kBufWord3 = 0x00020000;             // raw buffer resource, 32-bit data format
 constexpr int kSc1 = 16;                          // cache policy: agent-scope coherent
 
