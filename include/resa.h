@@ -54,6 +54,7 @@ extern "C" {
 
 #define RESA_HEAD_DIM 128
 #define RESA_MAX_GROUP 8
+#define RESA_MAX_RECTIFY_ROWS 8192  /* largest f of resa_dense_rectify */
 
 typedef enum resa_status {
   RESA_OK = 0,
@@ -236,10 +237,15 @@ size_t resa_rectify_workspace_size(int32_t batch, int32_t num_kv_heads,
  *        lse[b, h, r]    = log sum_t exp(...)            (optional, may be NULL)
  *   3. if refresh_summaries, blocks floor((L - f) / b) .. M_b - 1 are
  *      re-summarised (Eq. 3).
- * 1 <= f <= 128 and f <= max_seq_len <= capacity. max_seq_len bounds every
- * seq_lens[b] (host side, for launch sizing). A sequence with
- * seq_lens[b] < f is left untouched and its out rows are 0 (lse -inf). The
- * workspace holds split partials and needs no initialisation.
+ * 1 <= f <= RESA_MAX_RECTIFY_ROWS and f <= max_seq_len <= capacity.
+ * max_seq_len bounds every seq_lens[b] (host side, for launch sizing). A
+ * sequence with seq_lens[b] < f is left untouched and its out rows are 0 (lse
+ * -inf). The workspace holds split partials and needs no initialisation.
+ * The same call serves (chunked) prefill (Alg. 1, prefill step): with
+ * seq_lens[b] already counting a prompt chunk of f tokens, the chunk's keys
+ * and values are written, its queries attend causally to the cache before
+ * it and to themselves, and its blocks are summarised; with f = L the whole
+ * prompt is prefilled and every block summary built.
  */
 int resa_dense_rectify(const resa_kv_cache_t* c, const void* q_f, const void* k_f,
                        const void* v_f, int32_t num_q_heads, int32_t f,

@@ -389,7 +389,8 @@ int resa_dense_rectify(const resa_kv_cache_t* c, const void* q_f, const void* k_
   RESA_CHECK_PTR(seq_lens, 4);
   RESA_CHECK_PTR(out, 16);
   if (lse != nullptr && !aligned(lse, 4)) return fail(RESA_ERR_INVALID_ARG, "lse is not 4-byte aligned");
-  if (f < 1 || f > 128) return fail(RESA_ERR_INVALID_ARG, "f %d outside [1, 128]", f);
+  if (f < 1 || f > RESA_MAX_RECTIFY_ROWS)
+    return fail(RESA_ERR_INVALID_ARG, "f %d outside [1, %d]", f, RESA_MAX_RECTIFY_ROWS);
   if (max_seq_len < f || max_seq_len > c->capacity)
     return fail(RESA_ERR_INVALID_ARG, "max_seq_len %d outside [f = %d, capacity %d]", max_seq_len,
                 f, c->capacity);

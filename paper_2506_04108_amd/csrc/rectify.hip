@@ -74,14 +74,16 @@ __device__ __forceinline__ f16x4_t lds_read_tr(const uint16_t* p) {
 }
 
 // Writes the re-encoded rows k_f, v_f over cache rows [L - f, L).
+// Grid (ceil(f / 16), batch * kv_heads): each workgroup copies 16 rows.
 __global__ __launch_bounds__(256) void k_rectify_rows(RectifyArgs a) {
-  const int grp = blockIdx.x;
+  const int grp = blockIdx.y;
   const int bb = grp / a.c.kv_heads;
   const int L = a.seq_lens[bb];
   if (L < a.f || L > a.c.capacity) return;
   uint16_t* k = const_cast<uint16_t*>(a.c.k);
   uint16_t* v = const_cast<uint16_t*>(a.c.v);
-  for (int s = threadIdx.x; s < a.f * 16; s += 256) {
+  const int s = blockIdx.x * 256 + threadIdx.x;
+  if (s < a.f * 16) {
     const int row = s >> 4, part = s & 15;
     const size_t src = ((size_t)grp * a.f + row) * kHeadDim + part * 8;
     const size_t dst = ((size_t)grp * a.c.capacity + (L - a.f + row)) * kHeadDim + part * 8;
@@ -101,7 +103,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int L = a.seq_lens[bb];
   const bool seq_ok = L >= f && L <= a.c.capacity;
   const int k0 = split * a.chunk;
-  const int k1 = seq_ok ? min(k0 + a.chunk, L) : k0;
+  // Keys past the last causal limit of this workgroup's rows are never
+  // needed (row rho sits at L - f + rho / G): long windows (chunked prefill)
+  // skip them instead of masking them.
+  const int last_row = min(R - 1, (qblk + 1) * kRowsPerWg - 1);
+  const int k1 = seq_ok ? min(min(k0 + a.chunk, L), L - f + last_row / G + 1) : k0;
   const int j = lane >> 4, lq = lane & 15;
   const int row_base = qblk * kRowsPerWg + wave * kRowsPerWave;
   const float ninf = -__builtin_inff();
@@ -333,7 +339,8 @@ int32_t rectify_chunk(int32_t batch, int32_t kv_heads, int32_t nqblk, int32_t ma
 }
 
 hipError_t launch_rectify(const RectifyArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL(k_rectify_rows, dim3(a.c.batch * a.c.kv_heads), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(k_rectify_rows, dim3((a.f + 15) / 16, a.c.batch * a.c.kv_heads), dim3(256), 0,
+                     stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (a.refresh) {

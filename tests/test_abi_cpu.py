@@ -162,7 +162,7 @@ def rectify(**kw):
 
 def test_rectify_validation():
     expect(rectify(f=0), 1, "f 0")
-    expect(rectify(f=129), 1, "f 129")
+    expect(rectify(f=8193), 1, "f 8193")
     expect(rectify(mx=8), 1, "max_seq_len")
     expect(rectify(mx=4096), 1, "max_seq_len")
     expect(rectify(k=None), 1, "k_f")

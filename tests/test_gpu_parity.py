@@ -478,6 +478,62 @@ def test_rectify_tiny4k_full():
     assert eo <= TOL and el <= TOL
 
 
+@pytest.mark.parametrize("g,f,lens,cap", [
+    (4, 300, [1000, 777], 1024),     # a prompt chunk after a cached prefix
+    (4, 512, [512, 512], 512),       # whole-prompt prefill, f = L
+    (8, 640, [640, 400], 704),       # prefill; the short sequence is left as it is
+    (2, 2080, [2100, 2080], 2112),   # long chunk: many query blocks, causal key clamp
+])
+def test_rectify_prefill(g, f, lens, cap):
+    """Chunked and whole-prompt prefill through the rectification call: the
+    chunk's rows are written, its queries attend causally over the cache and
+    themselves, and every touched block summary is rebuilt. Sequences shorter
+    than f are untouched (zero rows, lse -inf)."""
+    w, cap = small(g=g, L=max(lens), cap=cap, tag=f"prefill{f}")
+    K, V = W.kv_cache(w, capacity=cap)
+    K0 = K.copy()
+    cache = make_cache(K, V, 16, sentinel=False)
+    lt = i32(lens)
+    if f < min(lens):
+        R.block_summarize(cache, lt)
+    kmin0, kmax0 = down(cache.kmin), down(cache.kmax)
+    base_k = np.stack([np.stack([K[bi, hi, max(lens[bi] - f, 0):max(lens[bi] - f, 0) + f]
+                                 for hi in range(2)]) for bi in range(2)])
+    base_v = np.stack([np.stack([V[bi, hi, max(lens[bi] - f, 0):max(lens[bi] - f, 0) + f]
+                                 for hi in range(2)]) for bi in range(2)])
+    qf, kf, vf = W.rectify_inputs(w, 5, base_k, base_v, f)
+    out, lse = R.dense_rectify(cache, up(qf), up(kf), up(vf), lt, max(lens))
+    torch.cuda.synchronize()
+    go, gl = out.cpu().numpy(), lse.cpu().numpy()
+    gk = down(cache.k)
+    qg = O.split_heads(O.bf16_to_f64(qf), 2)
+    Kd, Vd = O.bf16_to_f64(K), O.bf16_to_f64(V)
+    for bi in range(2):
+        L = lens[bi]
+        if L < f:
+            assert np.all(go[bi] == 0) and np.all(np.isneginf(gl[bi]))
+            assert np.array_equal(gk[bi], K0[bi])
+            assert np.array_equal(down(cache.kmin)[bi], kmin0[bi])
+            continue
+        for hi in range(2):
+            M = O.num_blocks(L, 16)
+            kmin, kmax = O.block_summaries(Kd[bi, hi], L, 16)
+            ro, rl = O.rectify_group(qg[bi, hi], Kd[bi, hi].copy(), Vd[bi, hi].copy(), kmin, kmax,
+                                     L, f, 16, w.sm_scale, O.bf16_to_f64(kf[bi, hi]),
+                                     O.bf16_to_f64(vf[bi, hi]))
+            eo = max_abs_err(go[bi, hi * g:(hi + 1) * g], ro)
+            el = max_abs_err(gl[bi, hi * g:(hi + 1) * g], rl)
+            print(f"prefill g={g} f={f} seq {bi} head {hi}: |dO| {eo:.2e} |dlse| {el:.2e}",
+                  flush=True)
+            assert eo <= TOL and el <= TOL
+            assert np.array_equal(gk[bi, hi, L - f:L], kf[bi, hi])
+            assert np.array_equal(gk[bi, hi, :L - f], K0[bi, hi, :L - f])
+            assert np.array_equal(gk[bi, hi, L:], K0[bi, hi, L:])
+            lo = (L - f) // 16
+            assert np.array_equal(O.bf16_to_f64(down(cache.kmin)[bi, hi, lo:M]), kmin[lo:M])
+            assert np.array_equal(O.bf16_to_f64(down(cache.kmax)[bi, hi, lo:M]), kmax[lo:M])
+
+
 # ---------------------------------------------------------------- decode loop
 
 @pytest.mark.parametrize("fused", [False, True])
