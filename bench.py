@@ -55,6 +55,8 @@ def parse():
     p.add_argument("--dense", action="store_true", help="dense baseline: decode over every block")
     p.add_argument("--breakdown", action="store_true",
                    help="latency breakdown at 16K/64K/256K (batch 8) against dense decoding")
+    p.add_argument("--prefill", action="store_true",
+                   help="time prefill (chunked and whole-prompt) through the rectification call")
     p.add_argument("--separate", action="store_true",
                    help="append and select as two launches instead of resa_append_select")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -397,6 +399,65 @@ def breakdown(args) -> dict:
     return {"breakdown": rows, "workload": describe(W.LONG_64K, args.layers, False)}
 
 
+MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 / fp16 matrix-core peak
+
+
+def prefill(args) -> dict:
+    """Prefill through the rectification call (Alg. 1, prefill step): a prompt
+    chunk of f rows is written into the cache, its queries attend causally to
+    the cache before it and to themselves, and its block summaries are built.
+    Cases: the last 4096-token chunk of a 64K prompt at batch 8, and whole
+    8K and 32K prompts (f = L). The rate counts the matrix work of causal
+    attention, 4 * 128 flops per (query head, row, visible key)."""
+    import torch
+
+    import paper_2506_04108_amd as R
+    import workloads as W
+    import workloads.device as WD
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    rows = []
+    for name, B, L, f in (("chunk4096_ctx65536_batch8", 8, 65536, 4096),
+                          ("prompt8192_batch8", 8, 8192, 8192),
+                          ("prompt32768_batch1", 1, 32768, 32768)):
+        w = W.LONG_64K.with_(batch=B, seq_len=L)
+        H, Hq, D, b = w.num_kv_heads, w.num_q_heads, w.head_dim, w.block_size
+        K, V, scale, plant = WD.caches(w, L, 0, dev)
+        mb = L // b
+        cache = R.KVCache(K, V, torch.empty((B, H, mb, D), dtype=torch.bfloat16, device=dev),
+                          torch.empty((B, H, mb, D), dtype=torch.bfloat16, device=dev), b)
+        lens = torch.full((B,), L, dtype=torch.int32, device=dev)
+        if f < L:
+            R.block_summarize(cache, lens)
+        qf, kf, vf = WD.rectify_rows(w, K[:, :, L - f:], V[:, :, L - f:], f, 7, dev)
+        out = torch.empty((B, Hq, f, D), dtype=torch.float32, device=dev)
+        lse = torch.empty((B, Hq, f), dtype=torch.float32, device=dev)
+        ws = R.Workspace(dev)
+        call = lambda: R.dense_rectify(cache, qf, kf, vf, lens, L, out=out, lse=lse, workspace=ws)
+        for _ in range(3):
+            call()
+        torch.cuda.synchronize()
+        reps = 10 if f * L * B < 2 ** 31 else 4
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        visible = f * (L - f) + f * (f + 1) // 2
+        flops = 4.0 * D * Hq * B * visible
+        tf = flops / (us * 1e-6) / 1e12
+        log(f"[bench] prefill {name}: {us:.1f} us, {tf:.1f} TFLOP/s")
+        rows.append({"case": name, "batch": B, "context": L, "f": f, "us_per_call": round(us, 2),
+                     "tflops": round(tf, 1), "peak": MFMA_PEAK_TFLOPS,
+                     "frac": round(tf / MFMA_PEAK_TFLOPS, 4)})
+        del K, V, cache, qf, kf, vf, out, lse, ws
+        torch.cuda.empty_cache()
+    return {"prefill": rows, "unit": "TFLOP/s", "bound": "mfma", "dtype": "bf16/f16 in, f32 acc"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -407,6 +468,9 @@ def main():
     torch.cuda.set_device(0)
     if args.breakdown:
         print(json.dumps(breakdown(args)), flush=True)
+        return
+    if args.prefill:
+        print(json.dumps(prefill(args)), flush=True)
         return
     w = workload_of(args)
     res = measure(args, w, args.dense)

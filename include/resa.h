@@ -54,7 +54,7 @@ extern "C" {
 
 #define RESA_HEAD_DIM 128
 #define RESA_MAX_GROUP 8
-#define RESA_MAX_RECTIFY_ROWS 8192  /* largest f of resa_dense_rectify */
+#define RESA_MAX_RECTIFY_ROWS 65536 /* largest f of resa_dense_rectify */
 
 typedef enum resa_status {
   RESA_OK = 0,
@@ -222,7 +222,8 @@ int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_he
                        float sm_scale, float* out, float* lse, void* workspace,
                        size_t workspace_bytes, void* stream);
 
-/* Workspace bytes resa_dense_rectify needs. */
+/* Workspace bytes resa_dense_rectify needs: 0 when one key split covers
+ * the window (long windows such as prefill), and then workspace may be NULL. */
 size_t resa_rectify_workspace_size(int32_t batch, int32_t num_kv_heads,
                                    int32_t num_q_heads, int32_t f, int32_t max_seq_len);
 
@@ -241,6 +242,8 @@ size_t resa_rectify_workspace_size(int32_t batch, int32_t num_kv_heads,
  * max_seq_len bounds every seq_lens[b] (host side, for launch sizing). A
  * sequence with seq_lens[b] < f is left untouched and its out rows are 0 (lse
  * -inf). The workspace holds split partials and needs no initialisation.
+ * Errors: RESA_ERR_INVALID_ARG for the ranges above or misaligned pointers,
+ * RESA_ERR_WORKSPACE when a needed workspace is missing or too small.
  * The same call serves (chunked) prefill (Alg. 1, prefill step): with
  * seq_lens[b] already counting a prompt chunk of f tokens, the chunk's keys
  * and values are written, its queries attend causally to the cache before

@@ -150,6 +150,7 @@ RectifyLayout rectify_layout(int32_t batch, int32_t kv_heads, int32_t group, int
   r.lse = 0;
   r.o = round256(groups * r.splits * rows * 4);
   r.total = r.o + groups * r.splits * rows * RESA_HEAD_DIM * 4;
+  if (r.splits == 1) r.total = 0;  // one split writes out / lse itself
   return r;
 }
 
@@ -396,10 +397,11 @@ int resa_dense_rectify(const resa_kv_cache_t* c, const void* q_f, const void* k_
                 f, c->capacity);
   if (!std::isfinite(sm_scale)) return fail(RESA_ERR_INVALID_ARG, "sm_scale is not finite");
   const RectifyLayout lay = rectify_layout(c->batch, c->num_kv_heads, group, f, max_seq_len);
-  if (workspace == nullptr || workspace_bytes < lay.total)
+  if (lay.total > 0 && (workspace == nullptr || workspace_bytes < lay.total))
     return fail(RESA_ERR_WORKSPACE, "rectify workspace needs %zu bytes, got %zu", lay.total,
                 workspace == nullptr ? (size_t)0 : workspace_bytes);
-  if (!aligned(workspace, 16)) return fail(RESA_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
+  if (workspace != nullptr && !aligned(workspace, 16))
+    return fail(RESA_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
   char* ws = static_cast<char*>(workspace);
   resa::RectifyArgs a;
   a.c = cache_args(c);

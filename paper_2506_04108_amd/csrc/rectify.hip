@@ -284,13 +284,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const int rho = row_base + 16 * qt + lq;
     if (rho < R) {
       const float inv = lt > 0.f ? 1.f / lt : 0.f;
-      float* po = a.part_o + (((size_t)grp * S + split) * R + rho) * kHeadDim;
+      const float l2 = lt > 0.f ? m[qt] + fast_log2(lt) : ninf;
+      // With a single split (long windows, e.g. prefill) this is the final
+      // row: it goes straight to out / lse and the combine is skipped.
+      const size_t oi = ((size_t)bb * a.q_heads + (size_t)hk * G + rho % G) * f + rho / G;
+      float* po = S == 1 ? a.out + oi * kHeadDim
+                         : a.part_o + (((size_t)grp * S + split) * R + rho) * kHeadDim;
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) {
         const f32x4_t y = o[dt][qt] * inv;
         *reinterpret_cast<f32x4_t*>(po + 16 * dt + 4 * j) = y;
       }
-      if (j == 0) a.part_lse[((size_t)grp * S + split) * R + rho] = lt > 0.f ? m[qt] + fast_log2(lt) : ninf;
+      if (j == 0) {
+        if (S > 1)
+          a.part_lse[((size_t)grp * S + split) * R + rho] = l2;
+        else if (a.lse)
+          a.lse[oi] = lt > 0.f ? l2 * kLn2 : ninf;
+      }
     }
   }
 
@@ -352,6 +362,7 @@ hipError_t launch_rectify(const RectifyArgs& a, hipStream_t stream) {
                      stream, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (a.num_splits == 1) return hipSuccess;  // the attention kernel wrote out / lse
   const int32_t rows = a.group * a.f;
   hipLaunchKernelGGL(k_rectify_combine, dim3((rows + kCombineRows - 1) / kCombineRows,
                      a.c.batch * a.c.kv_heads), dim3(256), 0, stream, a);

@@ -162,7 +162,7 @@ def rectify(**kw):
 
 def test_rectify_validation():
     expect(rectify(f=0), 1, "f 0")
-    expect(rectify(f=8193), 1, "f 8193")
+    expect(rectify(f=65537), 1, "f 65537")
     expect(rectify(mx=8), 1, "max_seq_len")
     expect(rectify(mx=4096), 1, "max_seq_len")
     expect(rectify(k=None), 1, "k_f")
@@ -177,6 +177,9 @@ def test_workspace_sizes():
     assert 1 <= s <= 256
     assert lib.resa_decode_workspace_size(8, 8, 32, 410, 16, s) >= 64 * s * 4 * 128 * 4
     assert lib.resa_rectify_workspace_size(8, 8, 32, 32, 65664) >= 64 * 128 * 128 * 4
+    # A whole-prompt window fills the chip with query blocks alone: one key split,
+    # written straight to the output, no workspace.
+    assert lib.resa_rectify_workspace_size(1, 8, 32, 32768, 32768) == 0
 
 
 def test_product_never_imports_oracle():

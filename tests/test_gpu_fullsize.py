@@ -145,3 +145,44 @@ def test_fullsize_extreme_256k():
     """1 x 32/8 heads, 256K context, sparsity 0.95 with a 4096-token minimum."""
     w = W.EXTREME_256K
     _full_size_step(w, [(0, 1), (0, 6)], [(0, 6)])
+
+
+def test_fullsize_prefill_32k():
+    """Whole-prompt prefill of a 32K prompt (1 x 32/8 heads, f = L = 32768)
+    through the rectification call, in the launch shape bench.py's prefill
+    case times (one key split, output written directly): sampled rows of two
+    groups against the oracle, the written rows and every block summary."""
+    w = W.LONG_64K.with_(batch=1, seq_len=32768, seed_tag="prefill32k")
+    L = f = w.seq_len
+    H, g, b, sm = w.num_kv_heads, w.group_size, w.block_size, w.sm_scale
+    assert R.lib().resa_rectify_workspace_size(1, H, w.num_q_heads, f, L) == 0
+    K, V = W.kv_cache(w)
+    qf, kf, vf = W.rectify_inputs(w, 0, K, V, f)
+    del K, V
+    mb = L // b
+    cache = R.KVCache(torch.zeros((1, H, L, 128), dtype=torch.bfloat16, device=dev()),
+                      torch.zeros((1, H, L, 128), dtype=torch.bfloat16, device=dev()),
+                      torch.zeros((1, H, mb, 128), dtype=torch.bfloat16, device=dev()),
+                      torch.zeros((1, H, mb, 128), dtype=torch.bfloat16, device=dev()), b)
+    lens = i32([L])
+    print(f"[fullsize] prefill 32K: B=1 Hq={w.num_q_heads} Hkv={H} f=L={L}", flush=True)
+    out, lse = R.dense_rectify(cache, up(qf), up(kf), up(vf), lens, L)
+    torch.cuda.synchronize()
+    rows = [0, 1, 63, 64, 127, 128, 4095, 16383, 20000, 32767]
+    for hi in (0, 5):
+        k64, v64 = O.bf16_to_f64(kf[0, hi]), O.bf16_to_f64(vf[0, hi])
+        qg = O.bf16_to_f64(qf[0, hi * g:(hi + 1) * g])
+        go = out[0, hi * g:(hi + 1) * g].cpu().numpy()
+        gl = lse[0, hi * g:(hi + 1) * g].cpu().numpy()
+        worst = 0.0
+        for r in rows:
+            ro, rl = O.attend(qg[:, r], k64, v64, range(r + 1), sm)
+            eo, el = max_abs_err(go[:, r], ro), max_abs_err(gl[:, r], rl)
+            worst = max(worst, eo, el)
+            assert eo <= TOL and el <= TOL, (hi, r, eo, el)
+        print(f"[fullsize] prefill 32K head {hi}: worst sampled error {worst:.2e}", flush=True)
+        assert np.array_equal(down(cache.k[0, hi]), kf[0, hi])
+        assert np.array_equal(down(cache.v[0, hi]), vf[0, hi])
+        mn, mx = O.block_summaries(k64, L, b)
+        assert np.array_equal(O.bf16_to_f64(down(cache.kmin[0, hi])), mn)
+        assert np.array_equal(O.bf16_to_f64(down(cache.kmax[0, hi])), mx)
