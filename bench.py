@@ -12,7 +12,10 @@ layer caches, as a model's layers do, so data reused from one step to the
 next cannot be served by the 256 MB last-level cache.
 
 Prints one JSON line. `value` is the GPU time of the timed steps (HIP events
-on the launch stream around the whole loop, host launches included). The
+on the launch stream around the whole loop). By default the timed steps are
+recorded once into a HIP graph and replayed, as a serving loop would run
+them; `--eager` launches every step from the host instead (the gaps between
+host launches then count too). The
 per-kernel figures come from a second pass that replays every launch of one
 kernel from the timed loop back to back between two events; the sparse-decode
 roofline divides the bytes of the selected K/V blocks per launch by that
@@ -55,6 +58,9 @@ def parse():
     p.add_argument("--dense", action="store_true", help="dense baseline: decode over every block")
     p.add_argument("--breakdown", action="store_true",
                    help="latency breakdown at 16K/64K/256K (batch 8) against dense decoding")
+    p.add_argument("--eager", dest="graph", action="store_false",
+                   help="launch every timed step from the host instead of replaying them "
+                        "from one HIP graph")
     p.add_argument("--prefill", action="store_true",
                    help="time prefill (chunked and whole-prompt) through the rectification call")
     p.add_argument("--separate", action="store_true",
@@ -172,6 +178,7 @@ def measure(args, w, dense: bool) -> dict:
     cap = -(-cap // b) * b
     stream = torch.cuda.current_stream()
     sptr = stream.cuda_stream
+    launch_stream = [sptr]  # the capture stream while a graph is recorded
     lb = lib()
 
     log(f"[bench] {describe(w, nlay, dense)}; capacity {cap}")
@@ -237,25 +244,25 @@ def measure(args, w, dense: bool) -> dict:
         if phase == "append_select":
             check(lb.resa_append_select(d, ly["k"][s].data_ptr(), ly["v"][s].data_ptr(), ly["q"][s].data_ptr(),
                                         Hq, ly["lens"].data_ptr(), Lcur, C.byref(params), ids.data_ptr(),
-                                        ns.data_ptr(), n_cap, None, ws_sels[li].data_ptr(), ws_sels[li].numel(), sptr))
+                                        ns.data_ptr(), n_cap, None, ws_sels[li].data_ptr(), ws_sels[li].numel(), launch_stream[0]))
         elif phase == "append":
             check(lb.resa_append_kv(d, ly["k"][s].data_ptr(), ly["v"][s].data_ptr(),
-                                    ly["lens"].data_ptr(), Lcur, sptr))
+                                    ly["lens"].data_ptr(), Lcur, launch_stream[0]))
         elif phase == "select":
             check(lb.resa_select_blocks(d, ly["q"][s].data_ptr(), Hq, ly["lens"].data_ptr(), Lcur + 1,
                                         C.byref(params), ids.data_ptr(), ns.data_ptr(), n_cap, None,
-                                        ws_sels[li].data_ptr(), ws_sels[li].numel(), sptr))
+                                        ws_sels[li].data_ptr(), ws_sels[li].numel(), launch_stream[0]))
         elif phase == "decode":
             if dense:
                 ids = all_idx
             check(lb.resa_sparse_decode(d, ly["q"][s].data_ptr(), Hq, ly["lens"].data_ptr(),
                                         ids.data_ptr(), ns.data_ptr(), n_cap, splits, sm, out.data_ptr(),
-                                        lse.data_ptr(), ws_dec.data_ptr(), ws_dec.numel(), sptr))
+                                        lse.data_ptr(), ws_dec.data_ptr(), ws_dec.numel(), launch_stream[0]))
         else:
             qf, kf, vf = rect_inputs[li, s + 1]
             check(lb.resa_dense_rectify(d, qf.data_ptr(), kf.data_ptr(), vf.data_ptr(), Hq, f,
                                         ly["lens"].data_ptr(), Lcur + 1, sm, rout.data_ptr(), None, 1,
-                                        ws_rec.data_ptr(), ws_rec.numel(), sptr))
+                                        ws_rec.data_ptr(), ws_rec.numel(), launch_stream[0]))
 
     def step(t):
         """One decode step (t >= 0: timed step t, its selection kept)."""
@@ -295,11 +302,39 @@ def measure(args, w, dense: bool) -> dict:
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     lens_seen = []
-    t0 = time.perf_counter()
-    e0.record(stream)
-    for t in range(args.steps):
-        lens_seen.append(step(t))
-    e1.record(stream)
+    if args.graph:
+        # The timed steps are recorded once into a HIP graph (recording runs
+        # nothing), replayed once to warm up, and after the lengths are put
+        # back, replayed again under the events: the same launches with the
+        # same host bounds, without per-launch host work. The second replay
+        # rewrites the same rows; summaries already hold them, so the
+        # selections can differ slightly from an eager run, not the amount
+        # of work.
+        lens0 = [ly["lens"].clone() for ly in layers]
+        graph = torch.cuda.CUDAGraph()
+        cap_stream = torch.cuda.Stream()
+        cap_stream.wait_stream(stream)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=cap_stream):
+            launch_stream[0] = cap_stream.cuda_stream
+            for t in range(args.steps):
+                lens_seen.append(step(t))
+        launch_stream[0] = sptr
+        graph.replay()
+        torch.cuda.synchronize()
+        for ly, l0 in zip(layers, lens0):
+            ly["lens"].copy_(l0)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        e0.record(stream)
+        graph.replay()
+        e1.record(stream)
+    else:
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for t in range(args.steps):
+            lens_seen.append(step(t))
+        e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     gpu_ms = e0.elapsed_time(e1)
@@ -362,7 +397,8 @@ def measure(args, w, dense: bool) -> dict:
         "config": {"workload": describe(w, nlay, dense), "batch": B, "q_heads": Hq, "kv_heads": H,
                    "head_dim": D, "context_start": L0, "block_size": b,
                    "sparsity": None if dense else w.sparsity, "min_tokens": w.min_tokens,
-                   "rectify_every": f, "decode_splits": splits, "layers_rotated": nlay},
+                   "rectify_every": f, "decode_splits": splits, "layers_rotated": nlay,
+                   "hip_graph": bool(args.graph)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "kernel": "k_decode",

@@ -584,3 +584,71 @@ def test_decode_loop_small(fused):
     torch.cuda.synchronize()
     assert lt.cpu().tolist() == st.L
     assert swaps <= 4
+
+
+# ------------------------------------------------------------------ HIP graph
+
+def test_graph_replay_matches_eager():
+    """One decode step (fused append + selection, then sparse decode) recorded
+    once in a HIP graph and replayed for several steps, with eager work and
+    synchronisations between the replays, gives bit-identical selections,
+    outputs, lengths and caches to the same calls made eagerly."""
+    w = W.LONG_64K.with_(batch=2, num_q_heads=8, num_kv_heads=2, seq_len=600, min_tokens=64,
+                         seed_tag="graph")
+    b, cap, steps = 16, 704, 4
+    B, H, Hq = 2, 2, 8
+    K, V = W.kv_cache(w, capacity=cap)
+    c1 = make_cache(K, V, b, sentinel=False)
+    c2 = make_cache(K, V, b, sentinel=False)
+    lens0 = [600, 555]
+    l1, l2 = i32(lens0), i32(lens0)
+    R.block_summarize(c1, l1)
+    R.block_summarize(c2, l2)
+    bound = max(lens0) + steps  # one host bound that holds for every step
+    mseq = -(-(bound + 1) // b)
+    n_cap = R.num_selected(mseq, w.sparsity, w.min_blocks, w.n_local)
+    splits = R.decode_num_splits(B, H, n_cap, b)
+    d = dev()
+    bf = torch.bfloat16
+    kn_s = torch.zeros((B, H, 128), dtype=bf, device=d)
+    vn_s = torch.zeros((B, H, 128), dtype=bf, device=d)
+    q_s = torch.zeros((B, Hq, 128), dtype=bf, device=d)
+    idx2 = torch.empty((B, H, n_cap), dtype=torch.int32, device=d)
+    ns2 = torch.empty((B, H), dtype=torch.int32, device=d)
+    out2 = torch.empty((B, Hq, 128), dtype=torch.float32, device=d)
+    lse2 = torch.empty((B, Hq), dtype=torch.float32, device=d)
+    wss = [R.Workspace(d) for _ in range(4)]
+    lib = R.lib()
+    for ws_sel, ws_dec in (wss[:2], wss[2:]):
+        ws_sel.get(lib.resa_select_workspace_size(B, H, bound + 1, b))
+        ws_dec.get(lib.resa_decode_workspace_size(B, H, Hq, n_cap, b, splits))
+    torch.cuda.synchronize()
+
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.graph(graph, stream=side):
+        R.append_select(c2, kn_s, vn_s, q_s, l2, bound, w.sparsity, w.min_blocks, w.n_local,
+                        n_cap=n_cap, block_idx=idx2, num_sel=ns2, workspace=wss[0])
+        R.sparse_decode(c2, q_s, l2, idx2, ns2, num_splits=splits, out=out2, lse=lse2,
+                        workspace=wss[1])
+    torch.cuda.synchronize()
+    for step in range(steps):
+        kn, vn = W.decode_kv(w, step)
+        q = W.decode_query(w, step)
+        kn_s.copy_(up(kn))
+        vn_s.copy_(up(vn))
+        q_s.copy_(up(q))
+        graph.replay()
+        torch.cuda.synchronize()
+        i1, n1 = R.append_select(c1, up(kn), up(vn), up(q), l1, bound, w.sparsity, w.min_blocks,
+                                 w.n_local, n_cap=n_cap, workspace=wss[2])
+        o1, s1 = R.sparse_decode(c1, up(q), l1, i1, n1, num_splits=splits, workspace=wss[3])
+        torch.cuda.synchronize()
+        print(f"graph replay {step}: n_sel {ns2.cpu().tolist()}", flush=True)
+        assert torch.equal(l1, l2)
+        assert torch.equal(n1, ns2) and torch.equal(i1, idx2)
+        assert torch.equal(o1, out2) and torch.equal(s1, lse2)
+    assert l2.cpu().tolist() == [x + steps for x in lens0]
+    for name in ("k", "v", "kmin", "kmax"):
+        assert torch.equal(getattr(c1, name), getattr(c2, name)), name
