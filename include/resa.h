@@ -67,15 +67,30 @@ typedef enum resa_status {
 
 /* The KV cache of one attention layer and its block-key cache. */
 typedef struct resa_kv_cache {
-  void* k;              /* bf16 [batch, num_kv_heads, capacity, head_dim] */
+  void* k;              /* bf16 [batch, num_kv_heads, capacity, head_dim], or a page
+                           pool (see block_table) */
   void* v;              /* bf16, same layout as k */
   void* kmin;           /* bf16 [batch, num_kv_heads, capacity / block_size, head_dim] */
   void* kmax;           /* bf16, same layout as kmin */
   int32_t batch;
   int32_t num_kv_heads;
   int32_t head_dim;     /* 128 */
-  int32_t capacity;     /* rows per (batch, kv head); multiple of block_size */
+  int32_t capacity;     /* tokens per sequence; multiple of block_size */
   int32_t block_size;   /* b: 16, 32 or 64 */
+  /* Paged layout (serving; optional). NULL: k and v are contiguous per
+   * sequence as above. Otherwise k and v are page pools, bf16
+   * [num_pages, num_kv_heads, block_size, head_dim]: one page holds one
+   * selection block (b tokens) of every kv head, and block_table (device
+   * int32 [batch, capacity / block_size]) names the page of logical block m
+   * of sequence s at block_table[s * (capacity / block_size) + m]. Block ids
+   * (selection output, Eq. 5) stay logical; the kernels translate them.
+   * Summaries stay per sequence (kmin / kmax layout above). Entries of the
+   * blocks a call touches must lie in [0, num_pages); an entry outside it is
+   * never dereferenced (its rows read as absent or zero and writes to them
+   * are dropped), and that sequence's results are then unspecified.
+   * num_pages * num_kv_heads * block_size must stay below 2^31. */
+  const int32_t* block_table;
+  int32_t num_pages;    /* pages in each pool (ignored when block_table is NULL) */
 } resa_kv_cache_t;
 
 /* Block-selection parameters (Sec. 2.1, Eq. 5). */

@@ -58,13 +58,20 @@ def version() -> str:
 
 @dataclasses.dataclass
 class KVCache:
-    """A layer's KV cache and block-key cache (caller-owned device tensors)."""
+    """A layer's KV cache and block-key cache (caller-owned device tensors).
 
-    k: torch.Tensor      # bf16 [B, Hkv, capacity, 128]
+    Contiguous layout: k, v are ``[B, Hkv, capacity, 128]``. Paged layout
+    (``block_table`` given): k, v are page pools ``[num_pages, Hkv,
+    block_size, 128]`` and ``block_table`` (int32 ``[B, capacity /
+    block_size]``) names the page of each logical block of each sequence.
+    Summaries are per sequence in both layouts."""
+
+    k: torch.Tensor      # bf16 [B, Hkv, capacity, 128] or [num_pages, Hkv, b, 128]
     v: torch.Tensor
     kmin: torch.Tensor   # bf16 [B, Hkv, capacity / block_size, 128]
     kmax: torch.Tensor
     block_size: int
+    block_table: torch.Tensor | None = None  # int32 [B, capacity / block_size]
 
     @classmethod
     def empty(cls, batch, kv_heads, capacity, block_size, device="cuda"):
@@ -75,9 +82,25 @@ class KVCache:
                    torch.zeros((batch, kv_heads, mb, HEAD_DIM), **mk),
                    torch.zeros((batch, kv_heads, mb, HEAD_DIM), **mk), block_size)
 
+    @classmethod
+    def empty_paged(cls, batch, kv_heads, capacity, block_size, num_pages, device="cuda"):
+        """Zeroed page pools of ``num_pages`` pages and an identity-free table
+        (all entries -1: the caller assigns pages)."""
+        mk = dict(dtype=torch.bfloat16, device=device)
+        pool = (num_pages, kv_heads, block_size, HEAD_DIM)
+        mb = capacity // block_size
+        return cls(torch.zeros(pool, **mk), torch.zeros(pool, **mk),
+                   torch.zeros((batch, kv_heads, mb, HEAD_DIM), **mk),
+                   torch.zeros((batch, kv_heads, mb, HEAD_DIM), **mk), block_size,
+                   torch.full((batch, mb), -1, dtype=torch.int32, device=device))
+
+    @property
+    def paged(self) -> bool:
+        return self.block_table is not None
+
     @property
     def batch(self):
-        return self.k.shape[0]
+        return self.kmin.shape[0]
 
     @property
     def kv_heads(self):
@@ -85,14 +108,25 @@ class KVCache:
 
     @property
     def capacity(self):
-        return self.k.shape[2]
+        return self.kmin.shape[2] * self.block_size
 
     def desc(self) -> KVCacheDesc:
         for name in ("k", "v", "kmin", "kmax"):
             _need(getattr(self, name), name, torch.bfloat16)
+        B, H, mb = self.kmin.shape[0], self.kmin.shape[1], self.kmin.shape[2]
+        if self.block_table is None:
+            _need(self.k, "k", torch.bfloat16, (B, H, mb * self.block_size, HEAD_DIM))
+            _need(self.v, "v", torch.bfloat16, (B, H, mb * self.block_size, HEAD_DIM))
+            return KVCacheDesc(self.k.data_ptr(), self.v.data_ptr(), self.kmin.data_ptr(),
+                               self.kmax.data_ptr(), B, H, HEAD_DIM, mb * self.block_size,
+                               self.block_size, None, 0)
+        P = self.k.shape[0]
+        _need(self.k, "k", torch.bfloat16, (P, H, self.block_size, HEAD_DIM))
+        _need(self.v, "v", torch.bfloat16, (P, H, self.block_size, HEAD_DIM))
+        _need(self.block_table, "block_table", torch.int32, (B, mb))
         return KVCacheDesc(self.k.data_ptr(), self.v.data_ptr(), self.kmin.data_ptr(),
-                           self.kmax.data_ptr(), self.k.shape[0], self.k.shape[1],
-                           self.k.shape[3], self.k.shape[2], self.block_size)
+                           self.kmax.data_ptr(), B, H, HEAD_DIM, mb * self.block_size,
+                           self.block_size, self.block_table.data_ptr(), P)
 
 
 class Workspace:

@@ -25,7 +25,8 @@ class ResaError(RuntimeError):
 class KVCacheDesc(C.Structure):
     _fields_ = [("k", C.c_void_p), ("v", C.c_void_p), ("kmin", C.c_void_p), ("kmax", C.c_void_p),
                 ("batch", C.c_int32), ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32),
-                ("capacity", C.c_int32), ("block_size", C.c_int32)]
+                ("capacity", C.c_int32), ("block_size", C.c_int32),
+                ("block_table", C.c_void_p), ("num_pages", C.c_int32)]
 
 
 class SelectParams(C.Structure):

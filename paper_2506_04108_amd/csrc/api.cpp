@@ -59,6 +59,16 @@ int check_cache(const resa_kv_cache_t* c) {
   if (c->capacity < c->block_size || c->capacity % c->block_size != 0)
     return fail(RESA_ERR_INVALID_ARG, "capacity %d must be a positive multiple of block_size %d",
                 c->capacity, c->block_size);
+  if (c->block_table != nullptr) {
+    if (!aligned(c->block_table, 4))
+      return fail(RESA_ERR_INVALID_ARG, "block_table is not 4-byte aligned");
+    if (c->num_pages < 1)
+      return fail(RESA_ERR_INVALID_ARG, "num_pages %d must be >= 1 with a block table",
+                  c->num_pages);
+    if ((int64_t)c->num_pages * c->num_kv_heads * c->block_size >= ((int64_t)1 << 31))
+      return fail(RESA_ERR_UNSUPPORTED, "page pool of %d pages x %d heads x %d rows exceeds 2^31 rows",
+                  c->num_pages, c->num_kv_heads, c->block_size);
+  }
   return RESA_OK;
 }
 
@@ -73,6 +83,9 @@ resa::CacheArgs cache_args(const resa_kv_cache_t* c) {
   a.capacity = c->capacity;
   a.block_size = c->block_size;
   a.max_blocks = c->capacity / c->block_size;
+  a.log2_block = c->block_size == 16 ? 4 : c->block_size == 32 ? 5 : 6;
+  a.table = c->block_table;
+  a.num_pages = c->block_table != nullptr ? c->num_pages : 0;
   return a;
 }
 

@@ -36,11 +36,11 @@ struct Chunk {
 };
 
 __device__ __forceinline__ void load_chunk(Chunk& ch, const uint16_t* kp, const uint16_t* vp,
-                                           const int (&krow)[4], int t0) {
+                                           const int (&krow)[4], int row0) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    ch.k[i] = ld16_stream(kp + (size_t)(t0 + krow[i]) * kHeadDim);
-    ch.v[i] = ld16_stream(vp + (size_t)(t0 + 4 * i) * kHeadDim);
+    ch.k[i] = ld16_stream(kp + (size_t)(row0 + krow[i]) * kHeadDim);
+    ch.v[i] = ld16_stream(vp + (size_t)(row0 + 4 * i) * kHeadDim);
   }
 }
 
@@ -276,6 +276,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void k_decode(DecodeArgs a) {
   __shared__ float sm_acc[kDecodeWaves][G][kHeadDim];
   __shared__ float sm_m[kDecodeWaves][G], sm_l[kDecodeWaves][G];
   __shared__ int s_tok[kIdxBatch];
+  __shared__ int s_row[kIdxBatch];
 
   constexpr int GP = Pad<G>::GP;
   constexpr int CPB = BS / kChunk;  // chunks per block
@@ -311,7 +312,10 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void k_decode(DecodeArgs a) {
     q[h][2] = t.z;
     q[h][3] = t.w;
   }
-  const size_t gbase = grp * (size_t)a.c.capacity * kHeadDim + (size_t)r * kHeadDim + col;
+  // Contiguous layout: chunk rows are counted from the group's first row;
+  // paged layout: from the start of the pool (the page's row is staged).
+  const bool paged = a.c.table != nullptr;
+  const size_t gbase = (paged ? 0 : grp * (size_t)a.c.capacity * kHeadDim) + (size_t)r * kHeadDim + col;
   const uint16_t* kp = a.c.k + gbase;
   const uint16_t* vp = a.c.v + gbase;
   const float scale = a.scale_log2;
@@ -326,11 +330,22 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void k_decode(DecodeArgs a) {
 
   for (int cb = c0; cb < c1; cb += kIdxBatch) {
     const int ce = min(c1, cb + kIdxBatch);
-    // First token of each chunk of this pass; -1 for ids outside [0, M).
+    // First token of each chunk of this pass (-1 for ids outside [0, M)) and
+    // the row holding it (0 for an invalid chunk: in bounds, masked out).
     for (int i = threadIdx.x; i < ce - cb; i += 64 * kDecodeWaves) {
       const int cc = cb + i;
       const int blk = idx[cc / CPB];
-      s_tok[i] = (blk < 0 || blk >= M) ? -1 : blk * BS + (cc % CPB) * kChunk;
+      int t = (blk < 0 || blk >= M) ? -1 : blk * BS + (cc % CPB) * kChunk;
+      int row = t;
+      if (paged && t >= 0) {
+        const int page = a.c.table[(size_t)bb * a.c.max_blocks + blk];
+        if ((unsigned)page < (unsigned)a.c.num_pages)
+          row = (page * a.c.kv_heads + hk) * BS + (cc % CPB) * kChunk;
+        else
+          t = -1;
+      }
+      s_tok[i] = t;
+      s_row[i] = t < 0 ? 0 : row;
     }
     lds_sync();
     // Wave w takes chunks cb + w, cb + w + W, ... (W waves). A ring of
@@ -338,13 +353,14 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void k_decode(DecodeArgs a) {
     // is consumed; an invalid chunk reads row 0 (in bounds) and is masked out
     // entirely. The scheduling barriers keep the refills ahead of the compute.
     auto tok = [&](int cc) -> int { return cc < ce ? __builtin_amdgcn_readfirstlane(s_tok[cc - cb]) : -1; };
+    auto row_of = [&](int cc) -> int { return cc < ce ? __builtin_amdgcn_readfirstlane(s_row[cc - cb]) : 0; };
     Chunk ring[kDepth + 1];
     int tring[kDepth + 1];
     int cc = cb + wave;
 #pragma unroll
     for (int k = 0; k <= kDepth; ++k) {
       tring[k] = tok(cc + k * kDecodeWaves);
-      load_chunk(ring[k], kp, vp, krow, max(tring[k], 0));
+      load_chunk(ring[k], kp, vp, krow, row_of(cc + k * kDecodeWaves));
     }
     __builtin_amdgcn_sched_barrier(0);
     while (cc < ce) {
@@ -354,7 +370,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void k_decode(DecodeArgs a) {
           consume_chunk<G>(ring[k], tring[k], r, c, L, scale, q, st, acc);
           __builtin_amdgcn_sched_barrier(0);
           tring[k] = tok(cc + (kDepth + 1) * kDecodeWaves);
-          load_chunk(ring[k], kp, vp, krow, max(tring[k], 0));
+          load_chunk(ring[k], kp, vp, krow, row_of(cc + (kDepth + 1) * kDecodeWaves));
           __builtin_amdgcn_sched_barrier(0);
           cc += kDecodeWaves;
         }

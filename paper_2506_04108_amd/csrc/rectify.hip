@@ -86,9 +86,12 @@ __global__ __launch_bounds__(256) void k_rectify_rows(RectifyArgs a) {
   if (s < a.f * 16) {
     const int row = s >> 4, part = s & 15;
     const size_t src = ((size_t)grp * a.f + row) * kHeadDim + part * 8;
-    const size_t dst = ((size_t)grp * a.c.capacity + (L - a.f + row)) * kHeadDim + part * 8;
-    st16(k + dst, ld16(a.k_f + src));
-    st16(v + dst, ld16(a.v_f + src));
+    const int64_t kr = kv_row(a.c, bb, grp % a.c.kv_heads, L - a.f + row);
+    if (kr >= 0) {
+      const size_t dst = (size_t)kr * kHeadDim + part * 8;
+      st16(k + dst, ld16(a.k_f + src));
+      st16(v + dst, ld16(a.v_f + src));
+    }
   }
 }
 
@@ -145,16 +148,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 
   // Thread tid moves 16-byte pieces tid + 256 e (e < 4) of a tile's K and V:
   // key (tid + 256 e) / 16, dims 8 (tid % 16) .. + 8.
-  const size_t gbase = (size_t)grp * a.c.capacity * kHeadDim;
   const int part = tid & 15;
   U4 rk[4], rv[4];
   auto gload = [&](int t0) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int kk = t0 + (tid >> 4) + 16 * e;
-      if (kk < k1) {
-        rk[e] = ld16_stream(a.c.k + gbase + (size_t)kk * kHeadDim + part * 8);
-        rv[e] = ld16_stream(a.c.v + gbase + (size_t)kk * kHeadDim + part * 8);
+      const int64_t kr = kk < k1 ? kv_row(a.c, bb, hk, kk) : -1;
+      if (kr >= 0) {
+        rk[e] = ld16_stream(a.c.k + (size_t)kr * kHeadDim + part * 8);
+        rv[e] = ld16_stream(a.c.v + (size_t)kr * kHeadDim + part * 8);
       } else {
         rk[e] = U4{0, 0, 0, 0};
         rv[e] = U4{0, 0, 0, 0};

@@ -28,7 +28,20 @@ struct CacheArgs {
   uint16_t* kmin;
   uint16_t* kmax;
   int32_t batch, kv_heads, capacity, block_size, max_blocks;  // max_blocks = capacity / b
+  int32_t log2_block;        // log2(block_size)
+  const int32_t* table;      // paged layout: block table [batch, max_blocks], else nullptr
+  int32_t num_pages;
 };
+
+// Row (of head_dim elements) of k / v that holds token t of group (bb, hk),
+// or -1 when the block table sends its block outside the page pool.
+__device__ __forceinline__ int64_t kv_row(const CacheArgs& c, int bb, int hk, int t) {
+  if (c.table == nullptr) return ((int64_t)bb * c.kv_heads + hk) * c.capacity + t;
+  const int m = t >> c.log2_block;
+  const int page = c.table[(size_t)bb * c.max_blocks + m];
+  if ((unsigned)page >= (unsigned)c.num_pages) return -1;
+  return ((int64_t)page * c.kv_heads + hk) * c.block_size + (t - (m << c.log2_block));
+}
 
 struct SelectArgs {
   CacheArgs c;

@@ -561,6 +561,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
   const bool opening = sl.pos >= 0 && sl.pos % a.c.block_size == 0;
   U4 knew = U4{0, 0, 0, 0}, vnew = U4{0, 0, 0, 0};
   const bool row_writer = sl.pos >= 0 && blockIdx.x == 0 && tid < 32;
+  const int64_t new_row = row_writer ? kv_row(a.c, bb, hk, sl.pos) : -1;
   if (sl.pos >= 0) {
     knew = ld16(a.k_new + grp * kHeadDim + col);
     if (row_writer && tid >= 16) vnew = ld16(a.v_new + grp * kHeadDim + col);
@@ -664,10 +665,10 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
     st16(a.c.kmin + so, new_lo);
     st16(a.c.kmax + so, new_hi);
   }
-  if (row_writer) {
+  if (new_row >= 0) {
     // The new K and V rows (stored after the scoring, so the loads above have
     // long arrived).
-    const size_t row = (grp * a.c.capacity + sl.pos) * kHeadDim + col;
+    const size_t row = (size_t)new_row * kHeadDim + col;
     if (tid < 16)
       st16(const_cast<uint16_t*>(a.c.k) + row, knew);
     else

@@ -31,7 +31,9 @@ __global__ __launch_bounds__(256) void k_summarize(CacheArgs c, const int32_t* _
 
   const int r = lane >> 4, col = (lane & 15) * 8;
   const size_t grp = (size_t)bb * c.kv_heads + hk;
-  const uint16_t* kb = c.k + (grp * c.capacity + (size_t)m * BS) * kHeadDim + col;
+  const int64_t row0 = kv_row(c, bb, hk, m * BS);  // a block never straddles pages
+  if (row0 < 0) return;
+  const uint16_t* kb = c.k + (size_t)row0 * kHeadDim + col;
   float mn[8], mx[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
@@ -86,7 +88,9 @@ __global__ __launch_bounds__(256) void k_append(CacheArgs c, const uint16_t* __r
   const int col = (lane & 15) * 8;
   for (int hk = wave; hk < c.kv_heads; hk += 4) {
     const size_t grp = (size_t)bb * c.kv_heads + hk;
-    const size_t row = (grp * c.capacity + pos) * kHeadDim + col;
+    const int64_t kr = kv_row(c, bb, hk, pos);
+    if (kr < 0) continue;  // page outside the pool: nothing is written
+    const size_t row = (size_t)kr * kHeadDim + col;
     const size_t src = grp * kHeadDim + col;
     if (lane < 16) {
       const U4 kv = ld16(k_new + src);

@@ -52,3 +52,50 @@ def padded_idx(idx_lists, B, H, n_cap):
         a[bi, hi, :len(ids)] = ids
         n[bi, hi] = len(ids)
     return a, n
+
+
+def make_paged_cache(K: np.ndarray, V: np.ndarray, block_size: int, lens_final, seed=0,
+                     spare=5, sentinel=True) -> R.KVCache:
+    """The same contents as make_cache in the paged layout: every logical
+    block that holds a token of sequence b (up to lens_final[b]) gets its own
+    page of a shuffled pool with `spare` extra pages; the other table entries
+    stay -1 (unassigned), so a kernel that touched them would be caught."""
+    B, H, cap, D = K.shape
+    mb = cap // block_size
+    used = [min(-(-int(L) // block_size), mb) for L in lens_final]
+    P = sum(used) + spare
+    rng = np.random.default_rng(seed)
+    perm = rng.permutation(P).astype(np.int32)
+    table = np.full((B, mb), -1, dtype=np.int32)
+    Kp = rng.integers(0, 2 ** 16, size=(P, H, block_size, D), dtype=np.uint16) & 0xBFFF  # finite junk
+    Vp = rng.integers(0, 2 ** 16, size=(P, H, block_size, D), dtype=np.uint16) & 0xBFFF
+    i = 0
+    for bi in range(B):
+        for m in range(used[bi]):
+            p = perm[i]
+            i += 1
+            table[bi, m] = p
+            Kp[p] = K[bi, :, m * block_size:(m + 1) * block_size]
+            Vp[p] = V[bi, :, m * block_size:(m + 1) * block_size]
+    fill = np.full((B, H, mb, D), SENTINEL if sentinel else 0, dtype=np.uint16)
+    return R.KVCache(up(Kp), up(Vp), up(fill), up(fill.copy()), block_size,
+                     torch.from_numpy(table).to(dev()))
+
+
+def unpage(cache: R.KVCache, lens):
+    """Rows [0, L_b) of a paged cache, gathered back to ``[B, Hkv, cap, D]``
+    uint16 (rows past L_b are zero)."""
+    table = cache.block_table.cpu().numpy()
+    Kp, Vp = down(cache.k), down(cache.v)
+    B, mb = table.shape
+    b = cache.block_size
+    H = Kp.shape[1]
+    K = np.zeros((B, H, mb * b, Kp.shape[3]), dtype=np.uint16)
+    V = np.zeros_like(K)
+    for bi in range(B):
+        for m in range(-(-int(lens[bi]) // b)):
+            K[bi, :, m * b:(m + 1) * b] = Kp[table[bi, m]]
+            V[bi, :, m * b:(m + 1) * b] = Vp[table[bi, m]]
+        K[bi, :, lens[bi]:] = 0
+        V[bi, :, lens[bi]:] = 0
+    return K, V

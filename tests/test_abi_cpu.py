@@ -67,6 +67,16 @@ def expect(rc, code, text):
     assert text in L.lib().resa_last_error().decode()
 
 
+def test_paged_cache_validation():
+    """Paged layout: the block table must be 4-byte aligned, the pool must
+    hold at least one page, and its rows must stay below 2^31."""
+    lib = L.lib()
+    run = lambda **kw: lib.resa_block_summarize(C.byref(cache(**kw)), FAKE, 0, -1, None)
+    expect(run(block_table=FAKE + 2, num_pages=8), 1, "block_table")
+    expect(run(block_table=FAKE, num_pages=0), 1, "num_pages")
+    expect(run(block_table=FAKE, num_pages=1 << 26, num_kv_heads=2), 2, "2^31")
+
+
 def test_summarize_validation():
     lib = L.lib()
     expect(lib.resa_block_summarize(None, FAKE, 0, -1, None), 1, "cache descriptor")

@@ -1,0 +1,111 @@
+"""Paged (block-table) caches: every entry point on a shuffled page pool gives
+bit-identical results to the same call on the contiguous layout (whose
+parity with the oracle the other GPU tests establish), and touches no page
+outside the sequences' own blocks (unassigned table entries are -1; spare
+pages hold junk that must never surface)."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2506_04108_amd as R
+import workloads as W
+from gpu_util import down, i32, make_cache, make_paged_cache, unpage, up
+
+pytestmark = pytest.mark.gpu
+
+
+def _pair(w, cap, lens, final, b, seed):
+    K, V = W.kv_cache(w, capacity=cap)
+    c1 = make_cache(K, V, b)
+    c2 = make_paged_cache(K, V, b, final, seed=seed)
+    return K, V, c1, c2
+
+
+def _same_cache(c1, c2, lens):
+    k1, v1 = down(c1.k), down(c1.v)
+    k2, v2 = unpage(c2, lens)
+    for bi, L in enumerate(lens):
+        assert np.array_equal(k1[bi, :, :L], k2[bi, :, :L])
+        assert np.array_equal(v1[bi, :, :L], v2[bi, :, :L])
+    assert torch.equal(c1.kmin, c2.kmin) and torch.equal(c1.kmax, c2.kmax)
+
+
+@pytest.mark.parametrize("b,g", [(16, 4), (32, 7), (64, 8)])
+def test_paged_matches_contiguous(b, g):
+    """Summaries, fused append + selection, separate append and selection,
+    sparse decode and rectification, step by step on both layouts."""
+    w = W.LONG_64K.with_(batch=3, num_q_heads=2 * g, num_kv_heads=2, seq_len=900, min_tokens=4 * b,
+                         block_size=b, seed_tag=f"paged{b}")
+    cap = -(-1100 // b) * b
+    lens = [900, 517, 64]
+    steps, f = 12, 8
+    final = [x + steps for x in lens]
+    _, _, c1, c2 = _pair(w, cap, lens, final, b, seed=b)
+    l1, l2 = i32(lens), i32(lens)
+    R.block_summarize(c1, l1)
+    R.block_summarize(c2, l2)
+    torch.cuda.synchronize()
+    _same_cache(c1, c2, lens)
+    ws = [R.Workspace() for _ in range(6)]
+    bound = max(lens)
+    for step in range(steps):
+        kn, vn = W.decode_kv(w, step)
+        q = W.decode_query(w, step)
+        if step % 3 == 2:   # the unfused path now and then
+            R.append_kv(c1, up(kn), up(vn), l1, bound)
+            R.append_kv(c2, up(kn), up(vn), l2, bound)
+            i1, n1 = R.select_blocks(c1, up(q), l1, bound + 1, w.sparsity, w.min_blocks, 1, workspace=ws[0])
+            i2, n2 = R.select_blocks(c2, up(q), l2, bound + 1, w.sparsity, w.min_blocks, 1, workspace=ws[1])
+        else:
+            i1, n1 = R.append_select(c1, up(kn), up(vn), up(q), l1, bound, w.sparsity, w.min_blocks, 1,
+                                     workspace=ws[0])
+            i2, n2 = R.append_select(c2, up(kn), up(vn), up(q), l2, bound, w.sparsity, w.min_blocks, 1,
+                                     workspace=ws[1])
+        bound += 1
+        o1, s1 = R.sparse_decode(c1, up(q), l1, i1, n1, workspace=ws[2])
+        o2, s2 = R.sparse_decode(c2, up(q), l2, i2, n2, workspace=ws[3])
+        torch.cuda.synchronize()
+        assert torch.equal(l1, l2) and torch.equal(n1, n2) and torch.equal(i1, i2), step
+        assert torch.equal(o1, o2) and torch.equal(s1, s2), step
+        if (step + 1) % f == 0:
+            cur = l1.cpu().tolist()
+            last_k = np.stack([np.stack([down(c1.k)[bi, hi, cur[bi] - f:cur[bi]] for hi in range(2)])
+                               for bi in range(3)])
+            last_v = np.stack([np.stack([down(c1.v)[bi, hi, cur[bi] - f:cur[bi]] for hi in range(2)])
+                               for bi in range(3)])
+            qf, kf, vf = W.rectify_inputs(w, step, last_k, last_v, f)
+            r1, t1 = R.dense_rectify(c1, up(qf), up(kf), up(vf), l1, bound, workspace=ws[4])
+            r2, t2 = R.dense_rectify(c2, up(qf), up(kf), up(vf), l2, bound, workspace=ws[5])
+            torch.cuda.synchronize()
+            assert torch.equal(r1, r2) and torch.equal(t1, t2), step
+    cur = l1.cpu().tolist()
+    assert cur == final
+    _same_cache(c1, c2, cur)
+
+
+def test_paged_prefill():
+    """Whole-prompt prefill (f = L) into a paged cache through the
+    rectification call, then one decode step: identical to the contiguous
+    layout, rows and summaries included."""
+    w = W.LONG_64K.with_(batch=2, num_q_heads=8, num_kv_heads=2, seq_len=700, min_tokens=64,
+                         seed_tag="pagedprefill")
+    b, cap = 16, 768
+    lens = [700, 700]
+    _, _, c1, c2 = _pair(w, cap, lens, [701, 701], b, seed=3)
+    base_k = np.zeros((2, 2, 700, 128), dtype=np.uint16)
+    qf, kf, vf = W.rectify_inputs(w, 0, base_k, base_k.copy(), 700)
+    l1, l2 = i32(lens), i32(lens)
+    r1, t1 = R.dense_rectify(c1, up(qf), up(kf), up(vf), l1, 700)
+    r2, t2 = R.dense_rectify(c2, up(qf), up(kf), up(vf), l2, 700)
+    torch.cuda.synchronize()
+    assert torch.equal(r1, r2) and torch.equal(t1, t2)
+    _same_cache(c1, c2, lens)
+    kn, vn = W.decode_kv(w, 0)
+    q = W.decode_query(w, 0)
+    i1, n1 = R.append_select(c1, up(kn), up(vn), up(q), l1, 700, w.sparsity, w.min_blocks, 1)
+    i2, n2 = R.append_select(c2, up(kn), up(vn), up(q), l2, 700, w.sparsity, w.min_blocks, 1)
+    o1, _ = R.sparse_decode(c1, up(q), l1, i1, n1)
+    o2, _ = R.sparse_decode(c2, up(q), l2, i2, n2)
+    torch.cuda.synchronize()
+    assert torch.equal(i1, i2) and torch.equal(o1, o2)
+    _same_cache(c1, c2, [701, 701])

@@ -14,7 +14,8 @@ import torch
 import oracle as O
 import paper_2506_04108_amd as R
 import workloads as W
-from gpu_util import SENTINEL, dev, down, i32, make_cache, oracle_summaries, padded_idx, up
+from gpu_util import (SENTINEL, dev, down, i32, make_cache, make_paged_cache, oracle_summaries,
+                      padded_idx, unpage, up)
 from oracle.compare import check_selection, max_abs_err
 
 pytestmark = pytest.mark.gpu
@@ -536,17 +537,21 @@ def test_rectify_prefill(g, f, lens, cap):
 
 # ---------------------------------------------------------------- decode loop
 
-@pytest.mark.parametrize("fused", [False, True])
-def test_decode_loop_small(fused):
+@pytest.mark.parametrize("fused,paged", [(False, False), (True, False), (True, True)])
+def test_decode_loop_small(fused, paged):
     """Kernel-level Alg. 1 loop (append, select, decode; rectify every f steps)
     on a reduced copy of the 64K batch-8 workload (outlier key channels);
-    `fused` runs the append and the selection as one resa_append_select."""
+    `fused` runs the append and the selection as one resa_append_select;
+    `paged` keeps K and V in a shuffled page pool behind a block table."""
     w = W.LONG_64K.with_(batch=2, num_q_heads=8, num_kv_heads=2, seq_len=600, min_tokens=64,
                          seed_tag="loop")
     f, steps, cap = 16, 40, 704
     K, V = W.kv_cache(w, capacity=cap)
-    cache = make_cache(K, V, 16, sentinel=False)
     lens = [600, 555]
+    if paged:
+        cache = make_paged_cache(K, V, 16, [x + steps for x in lens], seed=11, sentinel=False)
+    else:
+        cache = make_cache(K, V, 16, sentinel=False)
     lt = i32(lens)
     R.block_summarize(cache, lt)
     st = O.DecodeState(O.bf16_to_f64(K), O.bf16_to_f64(V), lens, 16)
@@ -584,6 +589,12 @@ def test_decode_loop_small(fused):
     torch.cuda.synchronize()
     assert lt.cpu().tolist() == st.L
     assert swaps <= 4
+    if paged:
+        gk, gv = unpage(cache, st.L)
+        for bi in range(2):
+            L = st.L[bi]
+            assert np.array_equal(O.bf16_to_f64(gk[bi, :, :L]), st.K[bi, :, :L])
+            assert np.array_equal(O.bf16_to_f64(gv[bi, :, :L]), st.V[bi, :, :L])
 
 
 # ------------------------------------------------------------------ HIP graph
