@@ -58,6 +58,8 @@ def parse():
     p.add_argument("--dense", action="store_true", help="dense baseline: decode over every block")
     p.add_argument("--breakdown", action="store_true",
                    help="latency breakdown at 16K/64K/256K (batch 8) against dense decoding")
+    p.add_argument("--paged", action="store_true",
+                   help="keep K and V in a shuffled page pool behind a block table")
     p.add_argument("--eager", dest="graph", action="store_false",
                    help="launch every timed step from the host instead of replaying them "
                         "from one HIP graph")
@@ -187,8 +189,15 @@ def measure(args, w, dense: bool) -> dict:
     for li in range(nlay):
         K, V, scale, plant = WD.caches(w, cap, li, dev)
         mb = cap // b
+        table = None
+        if args.paged:
+            # Serving layout: the layer's blocks scattered over a shuffled page pool.
+            g = torch.Generator(device=dev)
+            g.manual_seed(4108 + li)
+            table = torch.randperm(B * mb, generator=g, device=dev).to(torch.int32).view(B, mb)
+            K, V = (WD.to_pages(X, table, b) for X in (K, V))
         cache = R.KVCache(K, V, torch.empty((B, H, mb, D), dtype=torch.bfloat16, device=dev),
-                          torch.empty((B, H, mb, D), dtype=torch.bfloat16, device=dev), b)
+                          torch.empty((B, H, mb, D), dtype=torch.bfloat16, device=dev), b, table)
         lens = torch.full((B,), L0, dtype=torch.int32, device=dev)
         R.block_summarize(cache, lens)
         q, k, v = WD.step_inputs(w, per_layer, li, scale, plant, dev)
@@ -398,7 +407,7 @@ def measure(args, w, dense: bool) -> dict:
                    "head_dim": D, "context_start": L0, "block_size": b,
                    "sparsity": None if dense else w.sparsity, "min_tokens": w.min_tokens,
                    "rectify_every": f, "decode_splits": splits, "layers_rotated": nlay,
-                   "hip_graph": bool(args.graph)},
+                   "hip_graph": bool(args.graph), "paged": bool(args.paged)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "kernel": "k_decode",

@@ -150,19 +150,29 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   // key (tid + 256 e) / 16, dims 8 (tid % 16) .. + 8.
   const int part = tid & 15;
   U4 rk[4], rv[4];
-  auto gload = [&](int t0) {
+  // Cache rows of the next tile to load. With a block table they are looked
+  // up one load ahead (gload(t0) loads tile t0 and looks up tile t0 + 64, the
+  // next one loaded), so the table read is not on the path of the data loads.
+  int64_t nrow[4];
+  auto lookup = [&](int t0) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int kk = t0 + (tid >> 4) + 16 * e;
-      const int64_t kr = kk < k1 ? kv_row(a.c, bb, hk, kk) : -1;
-      if (kr >= 0) {
-        rk[e] = ld16_stream(a.c.k + (size_t)kr * kHeadDim + part * 8);
-        rv[e] = ld16_stream(a.c.v + (size_t)kr * kHeadDim + part * 8);
+      nrow[e] = kk < k1 ? kv_row(a.c, bb, hk, kk) : -1;
+    }
+  };
+  auto gload = [&](int t0) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (nrow[e] >= 0) {
+        rk[e] = ld16_stream(a.c.k + (size_t)nrow[e] * kHeadDim + part * 8);
+        rv[e] = ld16_stream(a.c.v + (size_t)nrow[e] * kHeadDim + part * 8);
       } else {
         rk[e] = U4{0, 0, 0, 0};
         rv[e] = U4{0, 0, 0, 0};
       }
     }
+    lookup(t0 + kKeyTile);
   };
   auto lstore = [&](int buf) {
 #pragma unroll
@@ -258,6 +268,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   };
 
   if (k0 < k1) {
+    lookup(k0);
     gload(k0);
     lstore(0);
     if (k0 + kKeyTile < k1) gload(k0 + kKeyTile);

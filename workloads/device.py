@@ -74,3 +74,14 @@ def rectify_rows(w: Workload, k_last: torch.Tensor, v_last: torch.Tensor, f: int
     k = (k_last.float() + 0.05 * torch.randn(k_last.shape, generator=g, device=device)).to(torch.bfloat16)
     v = (v_last.float() + 0.05 * torch.randn(v_last.shape, generator=g, device=device)).to(torch.bfloat16)
     return q.contiguous(), k.contiguous(), v.contiguous()
+
+
+def to_pages(X: torch.Tensor, table: torch.Tensor, block_size: int) -> torch.Tensor:
+    """Contiguous ``[B, Hkv, cap, 128]`` -> page pool ``[B * cap / b, Hkv, b, 128]``
+    with logical block m of sequence s on page ``table[s, m]``."""
+    B, H, cap, D = X.shape
+    mb = cap // block_size
+    pool = torch.empty((B * mb, H, block_size, D), dtype=X.dtype, device=X.device)
+    pool[table.reshape(-1).long()] = X.view(B, H, mb, block_size, D).permute(0, 2, 1, 3, 4).reshape(
+        B * mb, H, block_size, D)
+    return pool
