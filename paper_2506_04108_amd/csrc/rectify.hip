@@ -222,18 +222,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
           x[4 * kt + i] = y;
           tmax = fmaxf(tmax, y);
         }
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
       // Raw scores times c are log2-domain logits (c > 0 keeps the maximum).
       // The reference m moves only when the tile's maximum exceeds it by
       // more than kRefSlack, so the accumulator rescale is rare; every
       // weight stays <= 2^kRefSlack, well inside fp16 and fp32 range, and
-      // the normalisation by l uses the same reference.
-      const float tm = tmax * c;
+      // the normalisation by l uses the same reference. A query's 64 keys
+      // sit in four lanes (lq + 16 j): the row maximum across them is only
+      // needed when one of them exceeds the reference, so the cross-lane
+      // reduction runs on those (rare) tiles only.
       float alpha = 1.f;
-      if (tm > m[qt] + kRefSlack) {
-        alpha = fast_exp2(m[qt] - tm);  // 0 when m was -inf
-        m[qt] = tm;
+      if (__any(tmax * c > m[qt] + kRefSlack)) {
+        tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
+        tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+        const float tm = tmax * c;
+        if (tm > m[qt] + kRefSlack) {
+          alpha = fast_exp2(m[qt] - tm);  // 0 when m was -inf
+          m[qt] = tm;
+        }
       }
       const float mref = m[qt] == ninf ? 0.f : m[qt];
       float ps = 0.f;
