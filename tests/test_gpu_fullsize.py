@@ -64,10 +64,16 @@ def _full_size_step(w, select_groups, rectify_groups):
     kn, vn = W.decode_kv(w, 0)
     q = W.decode_query(w, 0)
     R.append_kv(cache, up(kn), up(vn), lens, L)
+    ws_sel = R.Workspace(d)
     idx, ns = R.select_blocks(cache, up(q), lens, L + 1, w.sparsity, w.min_blocks, w.n_local,
-                              n_cap=n_cap)
+                              n_cap=n_cap, workspace=ws_sel)
+    # A second call on the same workspace starts from the digit window the
+    # first call left behind: the same selection.
+    idx_h, ns_h = R.select_blocks(cache, up(q), lens, L + 1, w.sparsity, w.min_blocks, w.n_local,
+                                  n_cap=n_cap, workspace=ws_sel)
     out, lse = R.sparse_decode(cache, up(q), lens, idx, ns, num_splits=splits)
     torch.cuda.synchronize()
+    assert torch.equal(idx, idx_h) and torch.equal(ns, ns_h)
     gi, gn = idx.cpu().numpy(), ns.cpu().numpy()
     go, gl = out.cpu().numpy(), lse.cpu().numpy()
     sm = w.sm_scale

@@ -259,6 +259,35 @@ def test_select_window_hint(L):
             check_selection(gi[0, hi, :gn[0, hi]], ri[0, hi], rs[0, hi], rn[0, hi], 1)
 
 
+@pytest.mark.parametrize("b", [16, 64])
+def test_select_window_hint_ragged(b):
+    """Repeated calls on one workspace use the digit window the previous
+    call left behind: every call must equal a call on a fresh workspace and
+    the oracle, over ragged lengths, several workgroups per group, the forced
+    local block and a moving score distribution."""
+    w, cap = small(g=4, b=b, L=20000, cap=20480, B=3, H=2, tag=f"wl{b}")
+    lens = [20000, 13001, 700]
+    K, V = W.kv_cache(w, capacity=cap)
+    cache = make_cache(K, V, b)
+    lt = i32(lens)
+    R.block_summarize(cache, lt)
+    ws = R.Workspace(dev())
+    st = O.DecodeState(O.bf16_to_f64(K), O.bf16_to_f64(V), lens, b)
+    q0 = W.bf16_bits_to_f32(W.decode_query(w, 1))
+    for scale in [1.0, 1.0, 1.0, 1.25, 1.25, 0.8, 1.0]:
+        q = W.f32_to_bf16_bits(q0 * scale)
+        idx, ns = R.select_blocks(cache, up(q), lt, max(lens), 0.9, 4, 1, workspace=ws)
+        idx2, ns2 = R.select_blocks(cache, up(q), lt, max(lens), 0.9, 4, 1)
+        torch.cuda.synchronize()
+        assert torch.equal(idx, idx2) and torch.equal(ns, ns2), scale
+        rs, ri, rn = st.select(O.bf16_to_f64(q), 0.9, 4, 1)
+        gi, gn = idx.cpu().numpy(), ns.cpu().numpy()
+        for bi in range(3):
+            for hi in range(2):
+                assert gn[bi, hi] == rn[bi, hi]
+                check_selection(gi[bi, hi, :gn[bi, hi]], ri[bi, hi], rs[bi, hi], rn[bi, hi], 1)
+
+
 def test_select_planted_blocks_win():
     w = W.TINY_4K.with_(plant_norm=math.sqrt(128), seed_tag="strong")
     q = W.decode_query(w)
