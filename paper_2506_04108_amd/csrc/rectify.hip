@@ -6,8 +6,10 @@
 // Against the whole cache they form a dense contraction, so this is the one
 // place the library uses MFMA (v_mfma_f32_16x16x32_bf16).
 //
-// Grid (num_splits, ceil(R / 128), batch * kv_heads); 4 waves per workgroup,
-// each owning 32 query rows (two 16-row tiles). A workgroup walks its key
+// Grid (num_splits, ceil(R / rows), batch * kv_heads) with 4 waves (rows =
+// 128, windows of up to 128 rows) or 8 waves (rows = 256, longer windows
+// such as prefill) per workgroup, each wave owning 32 query rows (two
+// 16-row tiles). A workgroup walks its key
 // range in tiles of 64 keys: K and V rows go from registers (loaded one tile
 // ahead) into one of two LDS buffers, row-major, so one barrier per tile
 // separates filling a buffer from reading it. Per tile and wave:
@@ -42,7 +44,12 @@ typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kRowsPerWave = 32;
-constexpr int kRowsPerWg = 128;
+// Workgroups of 4 waves (128 rows) for short windows; long windows (prefill)
+// use 8 waves (256 rows), so each K / V tile brought into LDS serves twice
+// the rows.
+template <int kWaves>
+constexpr int rows_per_wg() { return kWaves * kRowsPerWave; }
+__host__ __device__ constexpr int waves_for_rows(int rows) { return rows > 128 ? 8 : 4; }
 constexpr int kKeyTile = 64;
 constexpr int kStride = kHeadDim + 8;    // bf16 per K or V row in LDS (272 B, 16-B aligned)
 constexpr int kTileElems = kKeyTile * kStride;
@@ -95,7 +102,12 @@ __global__ __launch_bounds__(256) void k_rectify_rows(RectifyArgs a) {
   }
 }
 
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_rectify_attn(RectifyArgs a) {
+template <int kWaves>
+__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_rectify_attn(RectifyArgs a) {
+  constexpr int kRowsPerWg = rows_per_wg<kWaves>();
+  constexpr int kThreads = 64 * kWaves;
+  constexpr int kPieces = kKeyTile * 16 / kThreads;  // 16-byte pieces of K (and of V) per thread per tile
+  constexpr int kRowStep = kThreads / 16;           // tile rows covered by one pass of the threads
   __shared__ __attribute__((aligned(16))) uint16_t sK[2][kTileElems];
   __shared__ __attribute__((aligned(16))) uint16_t sV[2][kTileElems];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -146,24 +158,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     for (int qt = 0; qt < 2; ++qt) o[dt][qt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m[2] = {ninf, ninf}, l[2] = {0.f, 0.f};
 
-  // Thread tid moves 16-byte pieces tid + 256 e (e < 4) of a tile's K and V:
-  // key (tid + 256 e) / 16, dims 8 (tid % 16) .. + 8.
+  // Thread tid moves 16-byte pieces tid + kThreads e (e < kPieces) of a
+  // tile's K and V: key (tid + kThreads e) / 16, dims 8 (tid % 16) .. + 8.
   const int part = tid & 15;
-  U4 rk[4], rv[4];
+  U4 rk[kPieces], rv[kPieces];
   // Cache rows of the next tile to load. With a block table they are looked
   // up one load ahead (gload(t0) loads tile t0 and looks up tile t0 + 64, the
   // next one loaded), so the table read is not on the path of the data loads.
-  int64_t nrow[4];
+  int64_t nrow[kPieces];
   auto lookup = [&](int t0) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int kk = t0 + (tid >> 4) + 16 * e;
+    for (int e = 0; e < kPieces; ++e) {
+      const int kk = t0 + (tid >> 4) + kRowStep * e;
       nrow[e] = kk < k1 ? kv_row(a.c, bb, hk, kk) : -1;
     }
   };
   auto gload = [&](int t0) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
+    for (int e = 0; e < kPieces; ++e) {
       if (nrow[e] >= 0) {
         rk[e] = ld16_stream(a.c.k + (size_t)nrow[e] * kHeadDim + part * 8);
         rv[e] = ld16_stream(a.c.v + (size_t)nrow[e] * kHeadDim + part * 8);
@@ -176,8 +188,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   };
   auto lstore = [&](int buf) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int off = ((tid >> 4) + 16 * e) * kStride + part * 8;
+    for (int e = 0; e < kPieces; ++e) {
+      const int off = ((tid >> 4) + kRowStep * e) * kStride + part * 8;
       st16(&sK[buf][off], rk[e]);
       st16(&sV[buf][off], U4{bf2_to_h2(rv[e].x), bf2_to_h2(rv[e].y), bf2_to_h2(rv[e].z),
                              bf2_to_h2(rv[e].w)});
@@ -351,7 +363,9 @@ __global__ __launch_bounds__(256) void k_rectify_combine(RectifyArgs a) {
 }  // namespace
 
 int32_t rectify_num_qblocks(int32_t group, int32_t f) {
-  return (group * f + kRowsPerWg - 1) / kRowsPerWg;
+  const int rows = group * f;
+  const int per = waves_for_rows(rows) * kRowsPerWave;
+  return (rows + per - 1) / per;
 }
 
 int32_t rectify_chunk(int32_t batch, int32_t kv_heads, int32_t nqblk, int32_t max_seq_len) {
@@ -377,8 +391,11 @@ hipError_t launch_rectify(const RectifyArgs& a, hipStream_t stream) {
     if (e != hipSuccess) return e;
   }
   const int32_t nq = rectify_num_qblocks(a.group, a.f);
-  hipLaunchKernelGGL(k_rectify_attn, dim3(a.num_splits, nq, a.c.batch * a.c.kv_heads), dim3(256), 0,
-                     stream, a);
+  const dim3 grid(a.num_splits, nq, a.c.batch * a.c.kv_heads);
+  if (waves_for_rows(a.group * a.f) == 8)
+    hipLaunchKernelGGL(k_rectify_attn<8>, grid, dim3(512), 0, stream, a);
+  else
+    hipLaunchKernelGGL(k_rectify_attn<4>, grid, dim3(256), 0, stream, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (a.num_splits == 1) return hipSuccess;  // the attention kernel wrote out / lse
