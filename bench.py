@@ -95,10 +95,13 @@ def describe(w, layers, dense):
             + f"rectify every {w.rectify_every} steps, {layers} layer caches in rotation")
 
 
-def traffic_from_profile(kernel_src: str):
-    """HBM bytes per decode launch measured by rocprofv3 PMC counters, if the
-    committed profile was taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", "sparse_decode_long64k_pmc.md")
+def traffic_from_profile(kernel_src: str, workload: str | None):
+    """HBM bytes per decode launch measured by rocprofv3 PMC counters for this
+    workload, if a committed profile of it was taken on the current kernel
+    source; else None (also for variants: dense, paged, overridden sizes)."""
+    if workload is None:
+        return None
+    path = os.path.join(ROOT, "profiles", f"sparse_decode_{workload.replace('_', '')}_pmc.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -387,7 +390,9 @@ def measure(args, w, dense: bool) -> dict:
     avg_bytes = sum(bytes_dec) / len(bytes_dec)
     achieved = avg_bytes / (avg_dec_us * 1e-6) / 1e9
     kernel_src = os.path.join(ROOT, "paper_2506_04108_amd", "csrc", "decode.hip")
-    traffic = traffic_from_profile(kernel_src)
+    import workloads as W
+    plain = w == W.WORKLOADS.get(w.name) and not (dense or args.paged or args.separate)
+    traffic = traffic_from_profile(kernel_src, w.name if plain else None)
     ms_per_step = gpu_ms / args.steps
     n_calls = {ph: sum(1 for c in calls if c[0] == ph) for ph in phase_us}
     res = {

@@ -228,21 +228,22 @@ constexpr uint32_t kMaxCand = 256;  // bucket size resolved by ranking (4 thread
 // Exact top-n of one group by its last workgroup (M <= 1024 * NJ). Thread t
 // holds the keys of ids [t NJ, t NJ + NJ) in registers, so id order is
 // thread order. The key loads are issued first; while they are in flight the
-// workgroup sums the group's slots into the counts of the keys' 8 high bits.
-// The threshold digit is refined by the next 12 bits counted over the keys of
-// that digit; the few keys left in the bucket of the n-th largest key are
-// then gathered and ranked among themselves (key descending, id ascending),
-// which pins the n-th largest key T and how many keys equal to T are kept
-// (the lowest ids); a bucket too large to rank is refined by the last 12
-// bits instead. Blocks above T and the kept T-equal blocks are written in
-// ascending id order: one scan of the packed per-thread counts (above T in
-// the high half, equal to T in the low half) gives every thread its first
-// output position. NJ is the smallest instantiation that covers M, so the
-// unrolled per-thread loops do no more work than the group needs.
+// workgroup sums the group's slots into the counts of the keys' 8 high bits
+// (or of 8 more bits inside the window hint). A bucket too large to rank is
+// narrowed by 12 more bits. Then one pass over the keys marks, per thread,
+// the keys above the bucket of the n-th largest key and the keys inside it
+// (bit masks); the few keys in the bucket are gathered and ranked among
+// themselves (key descending, id ascending), and those ranked before the
+// remaining count are kept: every key above the n-th largest key T and the
+// lowest ids among the keys equal to T. One scan of the per-thread kept
+// counts gives every thread its first output position, and the kept ids are
+// written in ascending order by walking the set bits. NJ is the smallest
+// instantiation that covers M, so the unrolled per-thread loops do no more
+// work than the group needs.
 template <int NJ>
 __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int M, int forced_from, int W,
                                             uint32_t win, uint32_t* s_hist, uint32_t* lds32, uint32_t* misc,
-                                            int32_t* s_out, int bb, int L, uint32_t seq_ticket) {
+                                            int32_t* s_out, int bb, int L) {
   const int tid = threadIdx.x;
   const int n = count_selected(M, a.keep_ppm, a.min_blocks, a.n_local);
   int32_t* out = a.block_idx + grp * a.n_cap;
@@ -250,7 +251,9 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
     if (tid == 0) {
       a.num_sel[grp] = n;
       __hip_atomic_store(a.counters + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (a.k_new != nullptr) finish_append(a, bb, L, seq_ticket);
+      if (a.k_new != nullptr)
+        finish_append(a, bb, L, __hip_atomic_fetch_add(a.seq_counters + bb, 1u, __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT));
     }
     for (int i = tid; i < a.n_cap; i += kSelThreads) out[i] = i < n ? i : -1;
     return;
@@ -293,7 +296,13 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
   // order, so a store issued before a load would make the load's consumer
   // wait for the store's acknowledgement too. Every workgroup of the group
   // has taken its ticket, so the counter can be reset for the next call.
+  // Every workgroup of the group has read the old length (all took their
+  // tickets), so the sequence's counter is bumped now; its result is only
+  // looked at after the selection, so the round trip overlaps the tail.
+  uint32_t seq_ticket = 0;
   if (tid == 0) {
+    if (a.k_new != nullptr)
+      seq_ticket = __hip_atomic_fetch_add(a.seq_counters + bb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     a.num_sel[grp] = n;
     __hip_atomic_store(a.counters + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
@@ -381,75 +390,10 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
 #pragma unroll
   for (int i = 0; i < NJ; ++i) key[i] = block_key(id0 + i, forced_from, raw[i]);
   const int nv = min(max(M - id0, 0), NJ);  // this thread's valid keys: j < nv
-  while (known < 32 && cnt != k) {
-    if (cnt <= kMaxCand) {
-      // Rank the bucket's keys among themselves: the one with k - 1 keys
-      // before it in (key descending, id ascending) order is the n-th. A
-      // candidate is stored as (key << 32 | ~id), so that order is plain
-      // 64-bit descending order. Each wave reserves room for its candidates
-      // with one LDS atomic.
-      uint64_t* cv = reinterpret_cast<uint64_t*>(s_hist);
-      uint32_t mine = 0;
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) mine += (j < nv && (key[j] & pmask) == prefix);
-      const uint32_t incl = wave_incl_scan(mine);
-      const uint32_t wave_tot = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
-      uint32_t base = 0;
-      if ((tid & 63) == 63 && wave_tot != 0) base = atomicAdd(&misc[4], wave_tot);
-      uint32_t at = (uint32_t)__builtin_amdgcn_readlane((int)base, 63) + incl - mine;
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) {
-        if (j < nv && (key[j] & pmask) == prefix) {
-          cv[at] = ((uint64_t)key[j] << 32) | (uint32_t)~(uint32_t)(id0 + j);
-          ++at;
-        }
-      }
-      lds_sync();
-      {
-        // Four threads per candidate (lanes 4c .. 4c + 3 of one wave), each
-        // counting over a quarter of the bucket; the quarters are added with
-        // DPP quad swaps.
-        const uint32_t cand = (uint32_t)tid >> 2, part = (uint32_t)tid & 3u;
-        uint32_t before = 0, gtk = 0, kt = 0;
-        if (cand < cnt) {
-          const uint64_t vt = cv[cand];
-          kt = (uint32_t)(vt >> 32);
-          const uint32_t qlen = (cnt + 3) >> 2;
-          const uint32_t j1 = min((part + 1) * qlen, cnt);
-          uint32_t j = part * qlen;
-          for (; j + 8 <= j1; j += 8) {
-            uint64_t v[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = cv[j + u];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-              before += v[u] > vt;
-              gtk += (uint32_t)(v[u] >> 32) > kt;
-            }
-          }
-          for (; j < j1; ++j) {
-            const uint64_t vj = cv[j];
-            before += vj > vt;
-            gtk += (uint32_t)(vj >> 32) > kt;
-          }
-        }
-        before += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)before, kDppXor1, 0xf, 0xf, true);
-        before += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)before, kDppXor2, 0xf, 0xf, true);
-        gtk += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)gtk, kDppXor1, 0xf, 0xf, true);
-        gtk += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)gtk, kDppXor2, 0xf, 0xf, true);
-        if (cand < cnt && part == 0 && before == k - 1) {
-          misc[0] = kt;
-          misc[1] = before - gtk + 1;  // keys equal to T that are kept (lowest ids)
-        }
-      }
-      lds_sync();
-      prefix = misc[0];
-      pmask = 0xFFFFFFFFu;
-      k = misc[1];
-      known = 32;
-      break;
-    }
-    // Next digit: up to 12 bits below the known prefix.
+  const uint32_t valid = nv >= 32 ? 0xFFFFFFFFu : (1u << nv) - 1u;
+  // A bucket too large to rank is narrowed by the next 12 bits (rare once
+  // the window hint follows the threshold).
+  while (known < 32 && cnt != k && cnt > kMaxCand) {
     const int width = min(12, 32 - known), shift = 32 - known - width;
     const uint32_t dmask = (1u << width) - 1u;
     for (int i = tid; i < (1 << width); i += kSelThreads) s_hist[i] = 0;
@@ -465,57 +409,129 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
     k = misc[1];
     cnt = misc[2];
   }
+
+  // One pass over the keys: bit j of `take` marks key j above the bucket of
+  // the n-th largest key, bit j of `inb` key j inside it.
+  uint32_t take = 0, inb = 0;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const uint32_t km = key[j] & pmask;
+    take |= km > prefix ? 1u << j : 0u;
+    inb |= km == prefix ? 1u << j : 0u;
+  }
+  take &= valid;
+  inb &= valid;
+  uint32_t thr = prefix;  // the threshold key (its known bits), for the next call's window
+  // 0: the whole bucket is kept; 1: its candidates were ranked; 2: every key
+  // of the bucket equals the threshold and the k lowest ids are kept.
+  const int mode = cnt == k ? 0 : (cnt <= kMaxCand ? 1 : 2);
+  if (mode == 0) {
+    take |= inb;
+  } else if (mode == 1) {
+    // Rank the bucket's keys among themselves in (key descending, id
+    // ascending) order: a candidate is kept iff fewer than k candidates come
+    // before it, which keeps every key above the threshold T and the lowest
+    // ids among the keys equal to T. A candidate is stored as
+    // (key << 32 | ~id), so that order is plain 64-bit descending order; the
+    // kept ones set their id's bit in an LDS bitmap (ids < 32768: 1024 words).
+    uint64_t* cv = reinterpret_cast<uint64_t*>(s_hist);   // words [0, 2 kMaxCand)
+    uint32_t* bits = s_hist + 2048;                       // words [2048, 3072)
+    bits[tid] = 0;
+    const uint32_t mine = __builtin_popcount(inb);
+    const uint32_t incl = wave_incl_scan(mine);
+    const uint32_t wave_tot = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+    uint32_t base = 0;
+    if ((tid & 63) == 63 && wave_tot != 0) base = atomicAdd(&misc[4], wave_tot);
+    uint32_t at = (uint32_t)__builtin_amdgcn_readlane((int)base, 63) + incl - mine;
+    if (inb != 0) {
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        if ((inb >> j) & 1u) {
+          cv[at] = ((uint64_t)key[j] << 32) | (uint32_t)~(uint32_t)(id0 + j);
+          ++at;
+        }
+      }
+    }
+    lds_sync();
+    {
+      // Four threads per candidate (lanes 4c .. 4c + 3 of one wave), each
+      // counting over a quarter of the bucket; the quarters are added with
+      // DPP quad swaps.
+      const uint32_t cand = (uint32_t)tid >> 2, part = (uint32_t)tid & 3u;
+      uint32_t before = 0;
+      uint64_t vt = 0;
+      if (cand < cnt) {
+        vt = cv[cand];
+        const uint32_t qlen = (cnt + 3) >> 2;
+        const uint32_t j1 = min((part + 1) * qlen, cnt);
+        uint32_t j = part * qlen;
+        for (; j + 8 <= j1; j += 8) {
+          uint64_t v[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) v[u] = cv[j + u];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) before += v[u] > vt;
+        }
+        for (; j < j1; ++j) before += cv[j] > vt;
+      }
+      before += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)before, kDppXor1, 0xf, 0xf, true);
+      before += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)before, kDppXor2, 0xf, 0xf, true);
+      if (cand < cnt && part == 0 && before < k) {
+        const uint32_t id = ~(uint32_t)vt;
+        atomicOr(&bits[id >> 5], 1u << (id & 31u));
+        if (before == k - 1) misc[0] = (uint32_t)(vt >> 32);  // T
+      }
+    }
+    lds_sync();
+    thr = misc[0];
+    // This thread's ids [id0, id0 + NJ) span at most two bitmap words.
+    const uint32_t w0 = (uint32_t)id0 >> 5, sh = (uint32_t)id0 & 31u;
+    uint64_t pair = bits[w0];
+    if (sh + NJ > 32) pair |= (uint64_t)bits[w0 + 1] << 32;
+    take |= (uint32_t)(pair >> sh) & valid;
+  }
   // The next call's window: the top 9 bits of this threshold. The stores
   // here go out before the compaction so their latency overlaps it.
   if (tid == 0) {
     if (a.k_new != nullptr) finish_append(a, bb, L, seq_ticket);
-    a.window[grp] = 0x80000000u | (prefix >> 23);
+    a.window[grp] = 0x80000000u | (thr >> 23);
   }
 
-  // Per-thread counts above T and equal to T (each <= NJ, totals <= M < 2^16).
-  uint32_t gt = 0, eq = 0;
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    const uint32_t km = key[j] & pmask;
-    gt += (j < nv && km > prefix);
-    eq += (j < nv && km == prefix);
-  }
+  // Output positions: one scan of the packed per-thread counts (kept keys in
+  // the high half; in mode 2 also the bucket keys, which are kept in id
+  // order up to k, in the low half; totals <= M < 2^16).
+  const uint32_t nb = mode == 2 ? (uint32_t)__builtin_popcount(inb) : 0u;
   uint32_t tot;
-  const uint32_t before = block_exclusive_scan((gt << 16) | eq, lds32, &tot);
-  uint32_t e = before & 0xFFFFu;
-  uint32_t pos = (before >> 16) + min(e, k);
-  if (a.n_cap < kMaxBlocksPerWg) {
-    // Rows shorter than the workgroup's score staging area (free by now) are
-    // assembled there and written out coalesced. The loop is branch-free:
-    // ids not kept are written to the spare last slot.
-    constexpr uint32_t kSpare = kMaxBlocksPerWg - 1;
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const uint32_t km = key[j] & pmask;
-      const bool q = j < nv && km == prefix;
-      const bool take = (j < nv && km > prefix) || (q && e < k);
-      e += q ? 1u : 0u;
-      s_out[(take && pos < (uint32_t)a.n_cap) ? pos : kSpare] = id0 + j;
-      pos += take ? 1u : 0u;
+  const uint32_t before = block_exclusive_scan(((uint32_t)__builtin_popcount(take) << 16) | nb, lds32, &tot);
+  uint32_t pos = before >> 16;
+  if (mode == 2) {
+    // Bucket keys kept by earlier threads, then by this one. Written so that
+    // no subtraction can wrap: the form `k > e ? k - e : 0` was compiled into
+    // an unguarded k - e.
+    const uint32_t eb = min(before & 0xFFFFu, k);
+    uint32_t keep = min(k - eb, nb);
+    uint32_t m = inb;
+    for (; keep > 0; --keep) {
+      take |= m & (0u - m);  // lowest remaining bucket id
+      m &= m - 1u;
     }
+    pos += eb;
+  }
+  // Kept ids in ascending order. Rows shorter than the workgroup's score
+  // staging area (free by now) are assembled there and written out coalesced.
+  const bool staged = a.n_cap < kMaxBlocksPerWg;
+  for (uint32_t m = take; m != 0; m &= m - 1u) {
+    const int32_t id = id0 + __builtin_ctz(m);
+    if (pos < (uint32_t)a.n_cap) {  // never past the row, whatever the scores
+      if (staged) s_out[pos] = id;
+      else out[pos] = id;
+    }
+    ++pos;
+  }
+  if (staged) {
     lds_sync();
     for (int i = tid; i < a.n_cap; i += kSelThreads) out[i] = i < n ? s_out[i] : -1;
     return;
-  }
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    const uint32_t km = key[j] & pmask;
-    bool take = false;
-    if (j < nv && km > prefix) {
-      take = true;
-    } else if (j < nv && km == prefix) {
-      take = e < k;
-      ++e;
-    }
-    if (take) {
-      if (pos < (uint32_t)a.n_cap) out[pos] = id0 + j;  // never past the row
-      ++pos;
-    }
   }
   for (int i = n + tid; i < a.n_cap; i += kSelThreads) out[i] = -1;
 }
@@ -703,14 +719,8 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
   __syncthreads();
   if (s_misc[3] != gridDim.x - 1) return;
   const int W = gridDim.x;
-  // Every workgroup of this group has read the old length (all took their
-  // tickets), so the sequence's counter is bumped now; its result is only
-  // looked at after the selection, so the round trip overlaps the tail.
-  uint32_t seq_ticket = 0;
-  if (a.k_new != nullptr && tid == 0)
-    seq_ticket = __hip_atomic_fetch_add(a.seq_counters + bb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   select_tail<NJ>(a, grp, M, forced_from, W, win, s_hist, s_lds32, s_misc,
-                  reinterpret_cast<int32_t*>(s_score), bb, L, seq_ticket);
+                  reinterpret_cast<int32_t*>(s_score), bb, L);
 }
 
 }  // namespace
@@ -748,21 +758,31 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
 int32_t select_fused_max_blocks() { return kSelThreads * kKeysPerLane; }
 
 int32_t select_blocks_per_wg(int32_t batch, int32_t kv_heads, int32_t max_blocks_seq) {
-  // About one 16-wave workgroup per CU (256 CUs) in all, split evenly within
-  // a group, in multiples of 256 blocks (one 16-block tile per wave).
+  // About one 16-wave workgroup per CU (256 CUs) in all: a group's blocks are
+  // cut into equal ranges, in whole 16-block tiles, at least one tile per
+  // wave (256 blocks) and at most the LDS staging area.
   const int64_t groups = (int64_t)batch * kv_heads;
-  int64_t per_group = (256 + groups - 1) / groups;
+  const int64_t per_group = (256 + groups - 1) / groups;
   int64_t bpw = ((int64_t)max_blocks_seq + per_group - 1) / per_group;
-  bpw = (bpw + 255) / 256 * 256;
+  bpw = (bpw + 15) / 16 * 16;
   if (bpw < 256) bpw = 256;
   if (bpw > kMaxBlocksPerWg) bpw = kMaxBlocksPerWg;
   return (int32_t)bpw;
 }
 
 int32_t select_hist_words(int32_t batch, int32_t kv_heads, int32_t max_blocks_seq) {
-  const int32_t bpw = select_blocks_per_wg(batch, kv_heads, max_blocks_seq);
-  const int32_t wgs = (max_blocks_seq + bpw - 1) / bpw;
-  return wgs * kSlotWords;
+  // A bound on the workgroups per group that never decreases as the length
+  // grows (the count itself can, by a few, as the ranges are rounded to
+  // tiles), so a workspace sized for a longer length fits every shorter one:
+  // at most ceil(M / 256) ranges, and at most max(per_group, ceil(M / 8192)).
+  const int64_t groups = (int64_t)batch * kv_heads;
+  const int64_t per_group = (256 + groups - 1) / groups;
+  const int64_t m = max_blocks_seq > 0 ? max_blocks_seq : 0;
+  int64_t wgs = (m + kMaxBlocksPerWg - 1) / kMaxBlocksPerWg;
+  if (wgs < per_group) wgs = per_group;
+  const int64_t most = (m + 255) / 256;
+  if (wgs > most) wgs = most;
+  return (int32_t)(wgs * kSlotWords);
 }
 
 }  // namespace resa
