@@ -12,6 +12,8 @@
  *   resa_append_select    Alg. 1 + Eq. 4-5  append fused with the selection
  *   resa_sparse_decode    Eq. 2, Alg. 2  split flash-decoding over the
  *                                 selected blocks with log-sum-exp combine
+ *   resa_decode_step      Alg. 1 one decode token: append + select +
+ *                                 sparse decode in one persistent launch
  *   resa_dense_rectify    Sec. 2.2  rewrite the last f cache rows, dense
  *                                 causal attention of their queries over the
  *                                 whole cache, refresh the touched summaries
@@ -236,6 +238,44 @@ int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_he
                        const int32_t* num_sel, int32_t n_cap, int32_t num_splits,
                        float sm_scale, float* out, float* lse, void* workspace,
                        size_t workspace_bytes, void* stream);
+
+/* Workspace bytes resa_decode_step needs; max_seq_len and num_splits as
+ * passed to it (num_splits 0 = the automatic count). */
+size_t resa_step_workspace_size(int32_t batch, int32_t num_kv_heads, int32_t num_q_heads,
+                                int32_t max_seq_len, int32_t block_size, int32_t n_cap,
+                                int32_t num_splits);
+
+/*
+ * One decode token of one attention layer (Alg. 1, decoding loop, without
+ * the periodic rectification): resa_append_select followed by
+ * resa_sparse_decode, in one launch. For every sequence b with
+ * p = seq_lens[b] < capacity the token k_new[b], v_new[b] is appended (row p,
+ * block summary updated), the blocks of the p + 1 tokens are scored and
+ * selected (Eq. 4-5; block_idx / num_sel as resa_select_blocks), the g query
+ * heads attend to the selected blocks (Eq. 2, Alg. 2; out / lse as
+ * resa_sparse_decode) and seq_lens[b] becomes p + 1. A sequence already at
+ * capacity is left unchanged and decoded over its stored length.
+ * Arguments as for resa_append_select and resa_sparse_decode: max_seq_len is
+ * a host bound of seq_lens before the call and must be < capacity
+ * (RESA_ERR_CAPACITY otherwise), n_cap >= the Eq. 5 count at max_seq_len + 1
+ * tokens, num_splits 0 (automatic) or in [1, 256]. Groups of more than 32768
+ * blocks are RESA_ERR_UNSUPPORTED.
+ * The selection and the decode are the same computations as the two calls
+ * (selected ids identical, outputs equal up to fp32 summation order: the
+ * split parts are cut the same way but summed by 8 waves instead of 4).
+ * One workgroup per compute unit claims the work: score ranges first, then
+ * decode splits, each waiting for its group's selection (so a group's decode
+ * overlaps the selection of later groups). The workspace
+ * (resa_step_workspace_size) holds claim counters, per-group flags and
+ * tickets and the selection hint: zero-fill it before its first use
+ * (resa_workspace_clear); every call leaves the counters and flags at zero.
+ * Calls sharing a workspace must be ordered on one stream.
+ */
+int resa_decode_step(const resa_kv_cache_t* c, const void* k_new, const void* v_new,
+                     const void* q, int32_t num_q_heads, int32_t* seq_lens, int32_t max_seq_len,
+                     const resa_select_params_t* params, int32_t* block_idx, int32_t* num_sel,
+                     int32_t n_cap, int32_t num_splits, float sm_scale, float* out, float* lse,
+                     void* workspace, size_t workspace_bytes, void* stream);
 
 /* Workspace bytes resa_dense_rectify needs: 0 when one key split covers
  * the window (long windows such as prefill), and then workspace may be NULL. */

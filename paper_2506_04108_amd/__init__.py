@@ -23,7 +23,8 @@ import torch
 from ._lib import KVCacheDesc, ResaError, SelectParams, check, lib
 
 __all__ = ["KVCache", "Workspace", "ResaError", "num_selected", "block_summarize", "append_kv",
-           "select_blocks", "append_select", "sparse_decode", "dense_rectify", "decode_num_splits", "version"]
+           "select_blocks", "append_select", "sparse_decode", "decode_step", "dense_rectify",
+           "decode_num_splits", "version"]
 
 HEAD_DIM = 128
 
@@ -286,6 +287,56 @@ def sparse_decode(cache: KVCache, q: torch.Tensor, seq_lens: torch.Tensor, block
                                    float(sm_scale), out.data_ptr(), _ptr(lse), ws.data_ptr(),
                                    ws.numel(), _stream(stream)))
     return out, lse
+
+
+def decode_step(cache: KVCache, k_new: torch.Tensor, v_new: torch.Tensor, q: torch.Tensor,
+                seq_lens: torch.Tensor, max_seq_len: int, sparsity: float, min_blocks: int,
+                n_local: int = 1, n_cap: int | None = None, num_splits: int = 0,
+                sm_scale: float | None = None, block_idx: torch.Tensor | None = None,
+                num_sel: torch.Tensor | None = None, out: torch.Tensor | None = None,
+                lse: torch.Tensor | None = None, with_lse: bool = True,
+                workspace: Workspace | None = None, stream=None):
+    """One decode token (Alg. 1) in one launch: append (seq_lens incremented
+    in place), Eq. 4-5 selection and Eq. 2 / Alg. 2 sparse decoding.
+    ``max_seq_len`` bounds seq_lens before the call. Returns
+    ``(block_idx, num_sel, out, lse)`` as :func:`append_select` and
+    :func:`sparse_decode`."""
+    B, Hkv = cache.batch, cache.kv_heads
+    hq = q.shape[1]
+    shape = (B, Hkv, HEAD_DIM)
+    _need(k_new, "k_new", torch.bfloat16, shape)
+    _need(v_new, "v_new", torch.bfloat16, shape)
+    _need(q, "q", torch.bfloat16, (B, hq, HEAD_DIM))
+    _need(seq_lens, "seq_lens", torch.int32, (B,))
+    mseq = -(-(max_seq_len + 1) // cache.block_size)
+    if n_cap is None:
+        n_cap = max(num_selected(mseq, sparsity, min_blocks, n_local), 1)
+    if block_idx is None:
+        block_idx = torch.empty((B, Hkv, n_cap), dtype=torch.int32, device=q.device)
+    if num_sel is None:
+        num_sel = torch.empty((B, Hkv), dtype=torch.int32, device=q.device)
+    _need(block_idx, "block_idx", torch.int32, (B, Hkv, n_cap))
+    _need(num_sel, "num_sel", torch.int32, (B, Hkv))
+    if sm_scale is None:
+        sm_scale = 1.0 / math.sqrt(HEAD_DIM)
+    if out is None:
+        out = torch.empty((B, hq, HEAD_DIM), dtype=torch.float32, device=q.device)
+    _need(out, "out", torch.float32, (B, hq, HEAD_DIM))
+    if lse is None and with_lse:
+        lse = torch.empty((B, hq), dtype=torch.float32, device=q.device)
+    if lse is not None:
+        _need(lse, "lse", torch.float32, (B, hq))
+    ws_bytes = lib().resa_step_workspace_size(B, Hkv, hq, max_seq_len, cache.block_size, n_cap,
+                                              num_splits)
+    ws = (workspace or Workspace(q.device)).get(ws_bytes)
+    params = SelectParams(float(sparsity), int(min_blocks), int(n_local))
+    d = cache.desc()
+    check(lib().resa_decode_step(C.byref(d), k_new.data_ptr(), v_new.data_ptr(), q.data_ptr(), hq,
+                                 seq_lens.data_ptr(), max_seq_len, C.byref(params),
+                                 block_idx.data_ptr(), num_sel.data_ptr(), n_cap, num_splits,
+                                 float(sm_scale), out.data_ptr(), _ptr(lse), ws.data_ptr(), ws.numel(),
+                                 _stream(stream)))
+    return block_idx, num_sel, out, lse
 
 
 def dense_rectify(cache: KVCache, q_f: torch.Tensor, k_f: torch.Tensor, v_f: torch.Tensor,

@@ -119,17 +119,22 @@ struct SelectLayout {
 // and one per sequence (zero between calls), one digit-window hint per group
 // (kept from call to call; any value is valid), per-workgroup key-digit
 // counts, and the scores (rows padded to 4 floats).
-SelectLayout select_layout(int32_t batch, int32_t kv_heads, int32_t max_seq_len, int32_t block_size) {
+SelectLayout select_layout_words(int32_t batch, int32_t kv_heads, size_t mseq, size_t hist_words) {
   SelectLayout l;
   const size_t groups = (size_t)batch * kv_heads;
-  const size_t mseq = ((size_t)max_seq_len + block_size - 1) / block_size;
   l.counters = 0;
   l.seq_counters = groups * 4;
   l.window = (groups + (size_t)batch) * 4;
   l.hist = round256((2 * groups + (size_t)batch) * 4);
-  l.scores = l.hist + round256(groups * (size_t)resa::select_hist_words(batch, kv_heads, (int32_t)mseq) * 4);
+  l.scores = l.hist + round256(groups * hist_words * 4);
   l.total = l.scores + groups * ((mseq + 3) & ~size_t(3)) * sizeof(float);
   return l;
+}
+
+SelectLayout select_layout(int32_t batch, int32_t kv_heads, int32_t max_seq_len, int32_t block_size) {
+  const size_t mseq = ((size_t)max_seq_len + block_size - 1) / block_size;
+  return select_layout_words(batch, kv_heads, mseq,
+                             (size_t)resa::select_hist_words(batch, kv_heads, (int32_t)mseq));
 }
 
 struct DecodeLayout {
@@ -144,6 +149,31 @@ DecodeLayout decode_layout(int32_t batch, int32_t kv_heads, int32_t group, int32
   d.o = d.lse + round256(groups * splits * group * 4);
   d.total = d.o + groups * splits * group * RESA_HEAD_DIM * 4;
   return d;
+}
+
+// Workspace of resa_decode_step: claim counters and per-group ready flags,
+// then a selection workspace (score ranges of the step) and a decode
+// workspace.
+struct StepLayout {
+  size_t queue, ready, sel, dec, total;
+  SelectLayout s;
+  DecodeLayout d;
+};
+
+StepLayout step_layout(int32_t batch, int32_t kv_heads, int32_t group, int32_t sel_len,
+                       int32_t block_size, int32_t splits) {
+  StepLayout l;
+  const size_t groups = (size_t)batch * kv_heads;
+  const size_t mseq = ((size_t)sel_len + block_size - 1) / block_size;
+  l.queue = 0;
+  l.ready = 256;
+  l.sel = l.ready + round256(groups * 4);
+  l.s = select_layout_words(batch, kv_heads, mseq,
+                            (size_t)resa::step_hist_words(batch, kv_heads, (int32_t)mseq));
+  l.dec = l.sel + round256(l.s.total);
+  l.d = decode_layout(batch, kv_heads, group, splits);
+  l.total = l.dec + l.d.total;
+  return l;
 }
 
 struct RectifyLayout {
@@ -377,8 +407,128 @@ int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_he
   a.counters = reinterpret_cast<uint32_t*>(ws + lay.counters);
   a.part_lse = reinterpret_cast<float*>(ws + lay.lse);
   a.part_o = reinterpret_cast<float*>(ws + lay.o);
+  a.k_new = nullptr;
+  a.v_new = nullptr;
   hipError_t e = resa::launch_decode(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "resa_sparse_decode launch");
+  return ok();
+}
+
+size_t resa_step_workspace_size(int32_t batch, int32_t num_kv_heads, int32_t num_q_heads,
+                                int32_t max_seq_len, int32_t block_size, int32_t n_cap,
+                                int32_t num_splits) {
+  if (batch < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || max_seq_len < 0 ||
+      block_size < 16 || num_splits < 0)
+    return 0;
+  const int32_t s = num_splits > 0 ? num_splits
+                                   : resa::decode_auto_splits(batch, num_kv_heads, n_cap, block_size);
+  return step_layout(batch, num_kv_heads, num_q_heads / num_kv_heads, max_seq_len + 1, block_size, s)
+      .total;
+}
+
+int resa_decode_step(const resa_kv_cache_t* c, const void* k_new, const void* v_new, const void* q,
+                     int32_t num_q_heads, int32_t* seq_lens, int32_t max_seq_len,
+                     const resa_select_params_t* params, int32_t* block_idx, int32_t* num_sel,
+                     int32_t n_cap, int32_t num_splits, float sm_scale, float* out, float* lse,
+                     void* workspace, size_t workspace_bytes, void* stream) {
+  if (int e = check_cache(c)) return e;
+  int32_t group = 0;
+  if (int e = check_heads(c, num_q_heads, &group)) return e;
+  RESA_CHECK_PTR(k_new, 16);
+  RESA_CHECK_PTR(v_new, 16);
+  RESA_CHECK_PTR(q, 16);
+  RESA_CHECK_PTR(seq_lens, 4);
+  RESA_CHECK_PTR(block_idx, 4);
+  RESA_CHECK_PTR(num_sel, 4);
+  RESA_CHECK_PTR(out, 4);
+  if (lse != nullptr && !aligned(lse, 4)) return fail(RESA_ERR_INVALID_ARG, "lse is not 4-byte aligned");
+  if (max_seq_len < 0) return fail(RESA_ERR_INVALID_ARG, "max_seq_len %d < 0", max_seq_len);
+  if (max_seq_len >= c->capacity)
+    return fail(RESA_ERR_CAPACITY, "cache full: max_seq_len %d, capacity %d", max_seq_len,
+                c->capacity);
+  if (params == nullptr) return fail(RESA_ERR_INVALID_ARG, "params is NULL");
+  int32_t keep = 0;
+  if (!parse_sparsity(params->sparsity, &keep))
+    return fail(RESA_ERR_INVALID_ARG, "sparsity %g outside [0, 1]", params->sparsity);
+  if (params->min_blocks < 0 || params->n_local < 0)
+    return fail(RESA_ERR_INVALID_ARG, "min_blocks (%d) and n_local (%d) must be >= 0",
+                params->min_blocks, params->n_local);
+  if (num_splits < 0 || num_splits > 256)
+    return fail(RESA_ERR_INVALID_ARG, "num_splits %d outside [0, 256]", num_splits);
+  if (!std::isfinite(sm_scale)) return fail(RESA_ERR_INVALID_ARG, "sm_scale is not finite");
+  const int32_t sel_len = max_seq_len + 1;
+  const int32_t mseq = (sel_len + c->block_size - 1) / c->block_size;
+  if (mseq > resa::step_max_blocks())
+    return fail(RESA_ERR_UNSUPPORTED, "%d blocks per sequence exceed the fused step's %d", mseq,
+                resa::step_max_blocks());
+  const int32_t need = resa::count_selected(mseq, keep, params->min_blocks, params->n_local);
+  if (n_cap < need)
+    return fail(RESA_ERR_CAPACITY, "n_cap %d < %d blocks selectable at %d tokens", n_cap, need,
+                sel_len);
+  const int32_t splits = num_splits > 0 ? num_splits
+                                        : resa::decode_auto_splits(c->batch, c->num_kv_heads, n_cap,
+                                                                   c->block_size);
+  const StepLayout lay = step_layout(c->batch, c->num_kv_heads, group, sel_len, c->block_size, splits);
+  if (workspace == nullptr || workspace_bytes < lay.total)
+    return fail(RESA_ERR_WORKSPACE, "step workspace needs %zu bytes, got %zu", lay.total,
+                workspace == nullptr ? (size_t)0 : workspace_bytes);
+  if (!aligned(workspace, 16)) return fail(RESA_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
+  char* ws = static_cast<char*>(workspace);
+  char* wsel = ws + lay.sel;
+  char* wdec = ws + lay.dec;
+  const int64_t groups = (int64_t)c->batch * c->num_kv_heads;
+  resa::StepArgs a;
+  resa::SelectArgs& sa = a.s;
+  sa.c = cache_args(c);
+  sa.q = static_cast<const uint16_t*>(q);
+  sa.q_heads = num_q_heads;
+  sa.group = group;
+  sa.seq_lens = seq_lens;
+  sa.max_blocks_seq = mseq;
+  sa.keep_ppm = keep;
+  sa.min_blocks = params->min_blocks;
+  sa.n_local = params->n_local;
+  sa.scores = reinterpret_cast<float*>(wsel + lay.s.scores);
+  sa.score_stride = (mseq + 3) & ~3;
+  sa.scores_out = nullptr;
+  sa.block_idx = block_idx;
+  sa.num_sel = num_sel;
+  sa.n_cap = n_cap;
+  sa.counters = reinterpret_cast<uint32_t*>(wsel + lay.s.counters);
+  sa.hist = reinterpret_cast<uint32_t*>(wsel + lay.s.hist);
+  sa.blocks_per_wg = resa::step_blocks_per_range(c->batch, c->num_kv_heads, mseq);
+  sa.fused = 1;
+  sa.k_new = static_cast<const uint16_t*>(k_new);
+  sa.v_new = static_cast<const uint16_t*>(v_new);
+  sa.lens_out = seq_lens;
+  sa.seq_counters = reinterpret_cast<uint32_t*>(wsel + lay.s.seq_counters);
+  sa.window = reinterpret_cast<uint32_t*>(wsel + lay.s.window);
+  resa::DecodeArgs& d = a.d;
+  d.c = sa.c;
+  d.q = sa.q;
+  d.q_heads = num_q_heads;
+  d.group = group;
+  d.seq_lens = seq_lens;
+  d.block_idx = block_idx;
+  d.num_sel = num_sel;
+  d.n_cap = n_cap;
+  d.num_splits = splits;
+  d.scale_log2 = sm_scale * 1.4426950408889634f;
+  d.out = out;
+  d.lse = lse;
+  d.counters = reinterpret_cast<uint32_t*>(wdec + lay.d.counters);
+  d.part_lse = reinterpret_cast<float*>(wdec + lay.d.lse);
+  d.part_o = reinterpret_cast<float*>(wdec + lay.d.o);
+  d.k_new = sa.k_new;
+  d.v_new = sa.v_new;
+  a.queue = reinterpret_cast<uint32_t*>(ws + lay.queue);
+  a.ready = reinterpret_cast<uint32_t*>(ws + lay.ready);
+  a.nranges = (mseq + sa.blocks_per_wg - 1) / sa.blocks_per_wg;
+  if (a.nranges < 1) a.nranges = 1;
+  a.score_items = (int32_t)(groups * a.nranges);
+  a.dec_items = (int32_t)(groups * splits);
+  hipError_t e = resa::launch_step(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "resa_decode_step launch");
   return ok();
 }
 

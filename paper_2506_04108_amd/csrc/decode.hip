@@ -1,471 +1,17 @@
-// Group block-sparse flash-decoding (Eq. 2; App. A, Alg. 2) for gfx950.
-//
-// Grid (num_splits, kv_heads, batch); 4 waves per workgroup. The selected
-// blocks of a (sequence, kv head) group are cut into 16-token chunks and the
-// chunks into num_splits contiguous ranges; wave w of split s takes chunks
-// c0 + w, c0 + w + 4, ... of its range.
-//
-// Lane layout inside a wave: lane = 16 * r + c. Lane (r, c) owns dims
-// [8c, 8c + 8) of the chunk's rows r, r + 4, r + 8, r + 12, for K and for V,
-// so every wave-wide 16-byte load covers four consecutive 256-byte rows
-// (1 KiB contiguous) and one chunk is 4 K loads + 4 V loads per lane.
-// q.k partial sums use v_dot2 on bf16 pairs, then a 16-lane DPP reduction.
-// Each row group r keeps its own online-softmax state (running max m, sum l,
-// accumulator over its 8 dims) for the g query heads of the group, in the
-// log2 domain; the four row groups, then the waves are merged by log-sum-exp
-// inside the workgroup, and the last workgroup of each group to finish
-// merges the splits (a single split writes the output directly).
-#include <utility>
-
-#include "resa_device.h"
-#include "resa_internal.h"
+// Group block-sparse flash-decoding (Eq. 2; App. A, Alg. 2) for gfx950:
+// grid (num_splits, kv_heads, batch), one split per workgroup of 4 waves
+// (decode_split).
+#include "decode_impl.h"
 
 namespace resa {
 namespace {
 
 constexpr int kDecodeWaves = 4;
-constexpr int kDepth = 2;  // chunks in flight per wave while one is consumed
-
-constexpr int kIdxBatch = 1024;  // chunk start tokens staged in LDS per pass
-constexpr int kMaxSplits = 256;  // splits per group (bounded by the host)
-
-// One 16-token chunk of K and V for this lane: four K rows (in the lane's
-// permuted order) and V rows r, r+4, r+8, r+12.
-struct Chunk {
-  U4 k[4], v[4];
-};
-
-__device__ __forceinline__ void load_chunk(Chunk& ch, const uint16_t* kp, const uint16_t* vp,
-                                           const int (&krow)[4], int row0) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    ch.k[i] = ld16_stream(kp + (size_t)(row0 + krow[i]) * kHeadDim);
-    ch.v[i] = ld16_stream(vp + (size_t)(row0 + 4 * i) * kHeadDim);
-  }
-}
-
-// Heads padded to GP (4 or 8), so a row group's 4 rows x GP heads are 16 or
-// 32 values: one or two per lane after the transpose-reduce.
-template <int G>
-struct Pad {
-  static constexpr int GP = G <= 4 ? 4 : 8;
-};
-
-// Per-lane online-softmax state: after the transpose-reduce lane c of a row
-// group owns head c % GP, so m and l are one value per lane.
-struct Soft {
-  float m, l;
-};
-
-// The softmax reference m of a head moves only when a chunk's maximum cm
-// exceeds it by more than kRefSlack (log2 domain): weights stay <= 2^kRefSlack
-// and the accumulator rescale (returned factor != 1) is rare. The output is
-// normalised by l under the same reference, so the result does not depend on
-// where m sits.
-constexpr float kRefSlack = 8.f;
-
-__device__ __forceinline__ float move_ref(float& m, float cm) {
-  if (cm > m + kRefSlack) {
-    const float alpha = fast_exp2(m - cm);  // 0 when m was -inf
-    m = cm;
-    return alpha;
-  }
-  return 1.f;
-}
-
-// One chunk for this lane's row group (rows r + 4i of the chunk).
-//   logits: v_dot2 over the lane's 8 dims for 4 rows x GP heads, laid out so
-//           that slot s holds value n = s ^ c (n = row * GP + head), then one
-//           transpose-reduce leaves lane c with the logit of value n = c
-//           (and n = c + 16 when GP = 8);
-//   softmax: max and sum over the 4 rows of a head by row rotations, one
-//           exp per value instead of one per value and lane;
-//   P.V: p and the rescale factor are broadcast from the owning lanes, and
-//        every lane updates its 8 dims of the g heads.
-// Rows with token >= L, every row of an invalid chunk (t0 < 0) and padded
-// heads are excluded.
-template <int G>
-__device__ __forceinline__ void consume_chunk(const Chunk& ch, int t0, int r, int c, int L,
-                                              float scale, const uint32_t (&q)[Pad<G>::GP][4],
-                                              Soft& st, float (&acc)[G][8]) {
-  constexpr int GP = Pad<G>::GP;
-  const float ninf = -__builtin_inff();
-  float val[4 * GP];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-#pragma unroll
-    for (int h = 0; h < GP; ++h) {
-      float d = dot2_bf16(q[h][0], ch.k[i].x, 0.f);
-      d = dot2_bf16(q[h][1], ch.k[i].y, d);
-      d = dot2_bf16(q[h][2], ch.k[i].z, d);
-      d = dot2_bf16(q[h][3], ch.k[i].w, d);
-      val[i * GP + h] = d;
-    }
-  }
-#pragma unroll
-  for (int u = 0; u < GP / 4; ++u) transpose_reduce16(val + 16 * u);
-
-  const int head = c & (GP - 1);
-  float ab[G], pb[4][G], ab_own;
-  if constexpr (GP == 4) {
-    const int row = c >> 2;
-    const bool ok = t0 >= 0 && t0 + r + 4 * row < L && head < G;
-    const float x = ok ? val[0] * scale : ninf;
-    float cm = fmaxf(x, dpp<kDppRor4>(x));
-    cm = fmaxf(cm, dpp<kDppRor8>(cm));
-    const float alpha = move_ref(st.m, cm);
-    ab_own = alpha;
-    const float mref = st.m == ninf ? 0.f : st.m;
-    const float p = fast_exp2(x - mref);
-    float ps = p + dpp<kDppRor4>(p);
-    ps += dpp<kDppRor8>(ps);
-    st.l = fmaf(st.l, alpha, ps);
-    [&]<int... H>(std::integer_sequence<int, H...>) {
-      ((ab[H] = dpp<kDppBcast0 + H>(alpha)), ...);
-      ((pb[0][H] = dpp<kDppBcast0 + H>(p)), ...);
-      ((pb[1][H] = dpp<kDppBcast0 + 4 + H>(p)), ...);
-      ((pb[2][H] = dpp<kDppBcast0 + 8 + H>(p)), ...);
-      ((pb[3][H] = dpp<kDppBcast0 + 12 + H>(p)), ...);
-    }(std::make_integer_sequence<int, G>{});
-  } else {
-    const int row0 = c >> 3;  // rows row0 and row0 + 2
-    const bool ok0 = t0 >= 0 && t0 + r + 4 * row0 < L && head < G;
-    const bool ok1 = t0 >= 0 && t0 + r + 4 * (row0 + 2) < L && head < G;
-    const float x0 = ok0 ? val[0] * scale : ninf;
-    const float x1 = ok1 ? val[16] * scale : ninf;
-    float cm = fmaxf(x0, x1);
-    cm = fmaxf(cm, dpp<kDppRor8>(cm));
-    const float alpha = move_ref(st.m, cm);
-    ab_own = alpha;
-    const float mref = st.m == ninf ? 0.f : st.m;
-    const float p0 = fast_exp2(x0 - mref);
-    const float p1 = fast_exp2(x1 - mref);
-    float ps = p0 + p1;
-    ps += dpp<kDppRor8>(ps);
-    st.l = fmaf(st.l, alpha, ps);
-    [&]<int... H>(std::integer_sequence<int, H...>) {
-      ((ab[H] = dpp<kDppBcast0 + H>(alpha)), ...);
-      ((pb[0][H] = dpp<kDppBcast0 + H>(p0)), ...);
-      ((pb[1][H] = dpp<kDppBcast0 + 8 + H>(p0)), ...);
-      ((pb[2][H] = dpp<kDppBcast0 + H>(p1)), ...);
-      ((pb[3][H] = dpp<kDppBcast0 + 8 + H>(p1)), ...);
-    }(std::make_integer_sequence<int, G>{});
-  }
-
-  // Rescale only when some running max moved (alpha == 1 exactly otherwise);
-  // after the first chunks of a split that is rare, and the test is uniform.
-  if (__any(ab_own != 1.f)) {
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-      for (int d = 0; d < 8; ++d) acc[h][d] *= ab[h];
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    float v[8];
-    v[0] = bf_lo(ch.v[i].x); v[1] = bf_hi(ch.v[i].x);
-    v[2] = bf_lo(ch.v[i].y); v[3] = bf_hi(ch.v[i].y);
-    v[4] = bf_lo(ch.v[i].z); v[5] = bf_hi(ch.v[i].z);
-    v[6] = bf_lo(ch.v[i].w); v[7] = bf_hi(ch.v[i].w);
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-#pragma unroll
-      for (int d = 0; d < 8; ++d) acc[h][d] = fmaf(pb[i][h], v[d], acc[h][d]);
-    }
-  }
-}
-
-// Merge of a group's S split partials by its last workgroup (Alg. 2,
-// "Combine"), in one round of loads: every thread issues its lse loads (kept
-// in LDS) and its 128-bit partial loads together, all with agent scope
-// (buffer loads with the sc1 policy, bounds-checked by the buffer size).
-// Float4 column u of head r = u / 32 gets T = 256 / (32 G) threads, each
-// summing splits ph, ph + T, ...; the T sums are added through LDS.
-constexpr int kTailBatch = 16;    // partial loads per thread per round
-constexpr int kBufWord3 = 0x00020000;  // raw buffer resource, 32-bit data format
-
-template <int G>
-__device__ void merge_tail(const DecodeArgs& a, size_t grp, int S, size_t ob, float* s_lse,
-                           f4_t* s_red) {
-  constexpr int NT = 64 * kDecodeWaves;
-  constexpr int U = G * (kHeadDim / 4);
-  constexpr int T = U >= NT ? 1 : NT / U;
-  constexpr int kLse = (kMaxSplits * G + NT - 1) / NT;
-  const int tid = threadIdx.x;
-  const float ninf = -__builtin_inff();
-  const float* pl = a.part_lse + grp * S * (size_t)G;
-  const float* po = a.part_o + grp * S * (size_t)(G * kHeadDim);
-  const __amdgpu_buffer_rsrc_t rl = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<float*>(pl), (short)0, S * G * 4, kBufWord3);
-  const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<float*>(po), (short)0, S * G * kHeadDim * 4, kBufWord3);
-  constexpr int kSc1 = 16;  // cache policy: agent-scope coherent
-
-  float lreg[kLse];
-#pragma unroll
-  for (int j = 0; j < kLse; ++j) {
-    const int i = tid + NT * j;
-    lreg[j] = i < S * G ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rl, i * 4, 0, kSc1))
-                        : ninf;
-  }
-  const bool active = tid < U * T;
-  const int u = tid % U, ph = tid / U, r = u / (kHeadDim / 4), c4 = u % (kHeadDim / 4);
-  const int nb = (S + T * kTailBatch - 1) / (T * kTailBatch);
-  f4_t part[kTailBatch];
-  auto issue = [&](int b) {
-#pragma unroll
-    for (int k = 0; k < kTailBatch; ++k) {
-      const int sp = b * T * kTailBatch + k * T + ph;
-      // The builtins return integer types: reinterpret the bits, never convert.
-      part[k] = (active && sp < S)
-                    ? __builtin_bit_cast(f4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                                   ro, ((sp * G + r) * kHeadDim + 4 * c4) * 4, 0, kSc1))
-                    : f4_t{0.f, 0.f, 0.f, 0.f};
-    }
-  };
-  issue(0);
-  // Every split has taken its ticket: reset the counter for the next call.
-  // The store goes out after the loads (a wave's memory counter drains in
-  // issue order), so it does not delay their use.
-  if (tid == 0) __hip_atomic_store(a.counters + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-#pragma unroll
-  for (int j = 0; j < kLse; ++j) {
-    const int i = tid + NT * j;
-    if (i < S * G) s_lse[i] = lreg[j];
-  }
-  lds_sync();
-  float mx = ninf, wsum = 0.f;
-  if (active) {
-    for (int sp = 0; sp < S; ++sp) mx = fmaxf(mx, s_lse[sp * G + r]);
-    if (mx != ninf)
-      for (int sp = 0; sp < S; ++sp) {
-        const float l = s_lse[sp * G + r];
-        wsum += l == ninf ? 0.f : fast_exp2(l - mx);
-      }
-  }
-  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-  f4_t acc = {0.f, 0.f, 0.f, 0.f};
-  for (int b = 0; b < nb; ++b) {
-    if (b > 0) issue(b);
-#pragma unroll
-    for (int k = 0; k < kTailBatch; ++k) {
-      const int sp = b * T * kTailBatch + k * T + ph;
-      if (active && sp < S) {
-        const float l = s_lse[sp * G + r];
-        const float wgt = l == ninf ? 0.f : fast_exp2(l - mx) * inv;
-        acc += wgt * part[k];
-      }
-    }
-  }
-  if constexpr (T > 1) {
-    s_red[tid] = acc;
-    lds_sync();
-    if (active && ph == 0) {
-#pragma unroll
-      for (int k = 1; k < T; ++k) acc += s_red[tid + k * U];
-    }
-  }
-  if (active && ph == 0) {
-    *reinterpret_cast<f4_t*>(a.out + (ob + r) * kHeadDim + 4 * c4) = acc;
-    if (c4 == 0 && a.lse) a.lse[ob + r] = wsum > 0.f ? (mx + fast_log2(wsum)) * kLn2 : ninf;
-  }
-}
 
 template <int G, int BS>
 __global__ __launch_bounds__(64 * kDecodeWaves) void k_decode(DecodeArgs a) {
-  __shared__ float sm_acc[kDecodeWaves][G][kHeadDim];
-  __shared__ float sm_m[kDecodeWaves][G], sm_l[kDecodeWaves][G];
-  __shared__ int s_tok[kIdxBatch];
-  __shared__ int s_row[kIdxBatch];
-
-  constexpr int GP = Pad<G>::GP;
-  constexpr int CPB = BS / kChunk;  // chunks per block
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int split = blockIdx.x, hk = blockIdx.y, bb = blockIdx.z;
-  const int S = a.num_splits;
-  const size_t grp = (size_t)bb * a.c.kv_heads + hk;
-  const int L = a.seq_lens[bb];
-  const int M = min((L + BS - 1) / BS, a.c.max_blocks);
-  const int n = max(0, min(a.num_sel[grp], a.n_cap));
-  const int C = n * CPB;
-  const int c0 = (int)((int64_t)split * C / S);
-  const int c1 = (int)((int64_t)(split + 1) * C / S);
-  const int r = lane >> 4, c = lane & 15, col = c * 8;
-  const int32_t* idx = a.block_idx + grp * a.n_cap;
-
-  // Lane c's registers hold K row i ^ rperm and query head h ^ hperm, so
-  // that logit slot s = i * GP + h is value n = s ^ c (see transpose_reduce16).
-  const int hperm = c & (GP - 1);
-  const int rperm = GP == 4 ? (c >> 2) & 3 : (c >> 3) & 1;
-  int krow[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) krow[i] = 4 * (i ^ rperm);
-  uint32_t q[GP][4];
-#pragma unroll
-  for (int h = 0; h < GP; ++h) {
-    const int head = h ^ hperm;
-    U4 t = U4{0, 0, 0, 0};
-    if (head < G) t = ld16(a.q + ((size_t)bb * a.q_heads + (size_t)hk * G + head) * kHeadDim + col);
-    q[h][0] = t.x;
-    q[h][1] = t.y;
-    q[h][2] = t.z;
-    q[h][3] = t.w;
-  }
-  // Contiguous layout: chunk rows are counted from the group's first row;
-  // paged layout: from the start of the pool (the page's row is staged).
-  const bool paged = a.c.table != nullptr;
-  const size_t gbase = (paged ? 0 : grp * (size_t)a.c.capacity * kHeadDim) + (size_t)r * kHeadDim + col;
-  const uint16_t* kp = a.c.k + gbase;
-  const uint16_t* vp = a.c.v + gbase;
-  const float scale = a.scale_log2;
-  const float ninf = -__builtin_inff();
-
-  Soft st{ninf, 0.f};
-  float acc[G][8];
-#pragma unroll
-  for (int h = 0; h < G; ++h)
-#pragma unroll
-    for (int d = 0; d < 8; ++d) acc[h][d] = 0.f;
-
-  for (int cb = c0; cb < c1; cb += kIdxBatch) {
-    const int ce = min(c1, cb + kIdxBatch);
-    // First token of each chunk of this pass (-1 for ids outside [0, M)) and
-    // the row holding it (0 for an invalid chunk: in bounds, masked out).
-    for (int i = threadIdx.x; i < ce - cb; i += 64 * kDecodeWaves) {
-      const int cc = cb + i;
-      const int blk = idx[cc / CPB];
-      int t = (blk < 0 || blk >= M) ? -1 : blk * BS + (cc % CPB) * kChunk;
-      int row = t;
-      if (paged && t >= 0) {
-        const int page = a.c.table[(size_t)bb * a.c.max_blocks + blk];
-        if ((unsigned)page < (unsigned)a.c.num_pages)
-          row = (page * a.c.kv_heads + hk) * BS + (cc % CPB) * kChunk;
-        else
-          t = -1;
-      }
-      s_tok[i] = t;
-      s_row[i] = t < 0 ? 0 : row;
-    }
-    lds_sync();
-    // Wave w takes chunks cb + w, cb + w + W, ... (W waves). A ring of
-    // kDepth + 1 chunk buffers keeps kDepth chunks' loads in flight while one
-    // is consumed; an invalid chunk reads row 0 (in bounds) and is masked out
-    // entirely. The scheduling barriers keep the refills ahead of the compute.
-    auto tok = [&](int cc) -> int { return cc < ce ? __builtin_amdgcn_readfirstlane(s_tok[cc - cb]) : -1; };
-    auto row_of = [&](int cc) -> int { return cc < ce ? __builtin_amdgcn_readfirstlane(s_row[cc - cb]) : 0; };
-    Chunk ring[kDepth + 1];
-    int tring[kDepth + 1];
-    int cc = cb + wave;
-#pragma unroll
-    for (int k = 0; k <= kDepth; ++k) {
-      tring[k] = tok(cc + k * kDecodeWaves);
-      load_chunk(ring[k], kp, vp, krow, row_of(cc + k * kDecodeWaves));
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    while (cc < ce) {
-#pragma unroll
-      for (int k = 0; k <= kDepth; ++k) {
-        if (cc < ce) {
-          consume_chunk<G>(ring[k], tring[k], r, c, L, scale, q, st, acc);
-          __builtin_amdgcn_sched_barrier(0);
-          tring[k] = tok(cc + (kDepth + 1) * kDecodeWaves);
-          load_chunk(ring[k], kp, vp, krow, row_of(cc + (kDepth + 1) * kDecodeWaves));
-          __builtin_amdgcn_sched_barrier(0);
-          cc += kDecodeWaves;
-        }
-      }
-    }
-    lds_sync();
-  }
-
-  // Per-head state of this lane's row group: head h lives in lane 16 r + h.
-  float m_[G], l_[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    m_[h] = __shfl(st.m, 16 * r + h);
-    l_[h] = __shfl(st.l, 16 * r + h);
-  }
-
-  // Merge the four row groups of the wave (lanes c, c+16, c+32, c+48).
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    float mx = fmaxf(m_[h], __shfl_xor(m_[h], 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float w = (m_[h] == ninf) ? 0.f : fast_exp2(m_[h] - mx);
-    float l = l_[h] * w;
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
-    m_[h] = mx;
-    l_[h] = l;
-#pragma unroll
-    for (int d = 0; d < 8; ++d) {
-      float x = acc[h][d] * w;
-      x += __shfl_xor(x, 16);
-      x += __shfl_xor(x, 32);
-      acc[h][d] = x;
-    }
-  }
-  if (r == 0) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-#pragma unroll
-      for (int d = 0; d < 8; ++d) sm_acc[wave][h][col + d] = acc[h][d];
-      if (lane == 0) {
-        sm_m[wave][h] = m_[h];
-        sm_l[wave][h] = l_[h];
-      }
-    }
-  }
-  lds_sync();
-
-  // Merge the waves; store this split's normalised partial and its lse (log2
-  // domain), or the final output directly when there is a single split.
-  const bool single = S == 1;
-  const size_t ob = (size_t)bb * a.q_heads + (size_t)hk * G;
-  float* po = a.part_o + (grp * S + split) * (size_t)(G * kHeadDim);
-  float* pl = a.part_lse + (grp * S + split) * (size_t)G;
-  for (int o = threadIdx.x; o < G * kHeadDim; o += 64 * kDecodeWaves) {
-    const int h = o / kHeadDim, d = o % kHeadDim;
-    float mx = ninf;
-#pragma unroll
-    for (int w = 0; w < kDecodeWaves; ++w) mx = fmaxf(mx, sm_m[w][h]);
-    float lsum = 0.f, x = 0.f;
-#pragma unroll
-    for (int w = 0; w < kDecodeWaves; ++w) {
-      const float f = sm_m[w][h] == ninf ? 0.f : fast_exp2(sm_m[w][h] - mx);
-      lsum = fmaf(sm_l[w][h], f, lsum);
-      x = fmaf(sm_acc[w][h][d], f, x);
-    }
-    const bool any = lsum > 0.f;
-    const float val = any ? x / lsum : 0.f;
-    const float l2 = any ? mx + fast_log2(lsum) : ninf;
-    if (single) {
-      a.out[(ob + h) * kHeadDim + d] = val;
-      if (d == 0 && a.lse) a.lse[ob + h] = any ? l2 * kLn2 : ninf;
-    } else {
-      // Agent-scope stores write through to the level where every L2 slice
-      // sees them, so the partials need no cache writeback before the ticket.
-      __hip_atomic_store(po + o, val, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (d == 0) __hip_atomic_store(pl + h, l2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-  }
-  if (single) return;
-
-  // Alg. 2, "Combine": the last workgroup of the group to finish merges the
-  // splits. Each workgroup waits until its partial stores are acknowledged,
-  // then takes a ticket; the last one reads every partial with agent-scope
-  // loads and resets the counter for the next call.
-  __shared__ float s_w[kMaxSplits * G];
-  __shared__ f4_t s_red[64 * kDecodeWaves];
-  __shared__ uint32_t s_ticket;
-  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  if (threadIdx.x == 0)
-    s_ticket = __hip_atomic_fetch_add(a.counters + grp, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  __syncthreads();
-  if (s_ticket != (uint32_t)(S - 1)) return;
-  merge_tail<G>(a, grp, S, ob, s_w, s_red);
+  __shared__ DecodeLds<G, kDecodeWaves> lds;
+  decode_split<G, BS, kDecodeWaves, false>(a, blockIdx.z, blockIdx.y, blockIdx.x, a.seq_lens[blockIdx.z], -1, lds);
 }
 
 template <int G>

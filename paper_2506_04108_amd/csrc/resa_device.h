@@ -9,6 +9,8 @@ namespace resa {
 constexpr int kHeadDim = 128;
 constexpr int kWave = 64;
 constexpr int kChunk = 16;  // tokens handled per decode step of a wave
+constexpr int kBufWord3 = 0x00020000;  // raw buffer resource word 3: 32-bit data format
+constexpr int kSc1 = 16;              // buffer cache policy: agent-scope coherent
 
 // A 16-byte vector: 8 bf16 values (one lane's share of a 256-byte key row).
 struct __attribute__((aligned(16))) U4 {
@@ -24,6 +26,16 @@ __device__ __forceinline__ void lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// threadIdx.x through an opaque move. A persistent kernel runs several
+// phases in loops; values derived from the thread index (addresses, lane
+// roles) are then computed inside each phase instead of being hoisted to the
+// kernel entry and held in registers across every phase.
+__device__ __forceinline__ int thread_id() {
+  int t = threadIdx.x;
+  __asm__ volatile("" : "+v"(t));
+  return t;
 }
 
 __device__ __forceinline__ U4 ld16(const void* p) {

@@ -82,6 +82,18 @@ struct DecodeArgs {
   float* part_o;               // [B, Hkv, S, G, D]
   float* part_lse;             // [B, Hkv, S, G]
   uint32_t* counters;          // [B, Hkv], zero between calls
+  const uint16_t* k_new;       // fused step: [B, Hkv, D] token appended in the same launch
+  const uint16_t* v_new;
+};
+
+// Fused decode step (append + selection + decode in one persistent launch).
+struct StepArgs {
+  SelectArgs s;
+  DecodeArgs d;
+  uint32_t* queue;             // [4]: score claims, decode claims, exits (zero between calls), error flag
+  uint32_t* ready;             // [B, Hkv]: selection of the group published (zero between calls)
+  int32_t nranges;             // score ranges per group (blocks_per_wg each)
+  int32_t score_items, dec_items;
 };
 
 struct RectifyArgs {
@@ -111,6 +123,7 @@ hipError_t launch_append(const CacheArgs& c, const uint16_t* k_new, const uint16
                          int32_t* seq_lens, hipStream_t stream);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
+hipError_t launch_step(const StepArgs& a, hipStream_t stream);
 hipError_t launch_rectify(const RectifyArgs& a, hipStream_t stream);
 hipError_t launch_clear(void* p, size_t bytes, hipStream_t stream);
 
@@ -119,6 +132,9 @@ int32_t select_fused_max_blocks();
 int32_t select_blocks_per_wg(int32_t batch, int32_t kv_heads, int32_t max_blocks_seq);
 int32_t select_hist_words(int32_t batch, int32_t kv_heads, int32_t max_blocks_seq);
 int32_t decode_auto_splits(int32_t batch, int32_t kv_heads, int32_t n_cap, int32_t block_size);
+int32_t step_blocks_per_range(int32_t batch, int32_t kv_heads, int32_t max_blocks_seq);
+int32_t step_hist_words(int32_t batch, int32_t kv_heads, int32_t max_blocks_seq);
+int32_t step_max_blocks();
 int32_t rectify_num_qblocks(int32_t group, int32_t f);
 int32_t rectify_chunk(int32_t batch, int32_t kv_heads, int32_t nqblk, int32_t max_seq_len);
 

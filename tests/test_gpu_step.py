@@ -1,0 +1,177 @@
+"""GPU parity of the fused decode step (resa_decode_step): the same
+selections, lengths and cache contents as resa_append_select followed by
+resa_sparse_decode, outputs equal up to fp32 summation order, and the oracle
+within the attention bar; repeated calls on one workspace."""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2506_04108_amd as R
+import workloads as W
+from gpu_util import down, i32, make_cache, make_paged_cache, up
+from oracle.compare import check_selection, max_abs_err
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-3
+# The step cuts each group's selected chunks into the same splits as
+# resa_sparse_decode but sums a split with 8 waves instead of 4: fp32
+# rounding order only (values are O(1), sums of a few thousand terms).
+REORDER = 2e-5
+
+
+def clone(cache: R.KVCache) -> R.KVCache:
+    return dataclasses.replace(cache, **{f: getattr(cache, f).clone() for f in ("k", "v", "kmin", "kmax")})
+
+
+def step_error_flag(ws: R.Workspace) -> int:
+    """The guard flag of the fused step (word 3 of its workspace): set only if
+    a decode split gave up waiting for its group's selection."""
+    return int(ws.buf[12:16].view(torch.int32).item())
+
+
+def run_pair(w, cache, lens, steps, num_splits=0, n_cap=None):
+    """Runs `steps` decode tokens through resa_decode_step on `cache` and
+    through append_select + sparse_decode on a copy; checks them against each
+    other every step and yields (step, q, idx, nsel, out) of the fused path."""
+    ref_cache = clone(cache)
+    lt, lr = i32(lens), i32(lens)
+    ws_step, ws_sel, ws_dec = R.Workspace(), R.Workspace(), R.Workspace()
+    L = list(lens)
+    for step in range(steps):
+        kn, vn = W.decode_kv(w, step)
+        q = W.decode_query(w, step)
+        bound = min(max(L), cache.capacity - 1)  # a full sequence is reached through its device length
+        idx, ns, out, lse = R.decode_step(cache, up(kn), up(vn), up(q), lt, bound, w.sparsity,
+                                          w.min_blocks, w.n_local, n_cap=n_cap, num_splits=num_splits,
+                                          workspace=ws_step)
+        ridx, rns = R.append_select(ref_cache, up(kn), up(vn), up(q), lr, bound, w.sparsity,
+                                    w.min_blocks, w.n_local, n_cap=idx.shape[-1], workspace=ws_sel)
+        rout, rlse = R.sparse_decode(ref_cache, up(q), lr, ridx, rns, num_splits=num_splits,
+                                     workspace=ws_dec)
+        torch.cuda.synchronize()
+        assert step_error_flag(ws_step) == 0
+        assert torch.equal(lt, lr)
+        assert torch.equal(ns, rns)
+        assert torch.equal(idx, ridx)
+        assert max_abs_err(out.cpu().numpy(), rout.cpu().numpy()) <= REORDER
+        fin = torch.isfinite(rlse)
+        assert torch.equal(torch.isfinite(lse), fin)
+        assert max_abs_err(lse[fin].cpu().numpy(), rlse[fin].cpu().numpy()) <= REORDER
+        L = [min(x + 1, cache.capacity) for x in L]
+        yield step, kn, vn, q, idx, ns, out
+    torch.cuda.synchronize()
+    for f in ("k", "v", "kmin", "kmax"):
+        assert torch.equal(getattr(cache, f), getattr(ref_cache, f)), f
+
+
+@pytest.mark.parametrize("g,b", [(4, 16), (7, 16), (8, 32), (1, 64), (4, 64)])
+def test_step_matches_separate_calls(g, b):
+    w, cap = W.TINY_4K.with_(batch=3, num_kv_heads=2, num_q_heads=2 * g, seq_len=1500, block_size=b,
+                             min_tokens=8 * b, seed_tag=f"step-{g}-{b}"), 2048
+    K, V = W.kv_cache(w, capacity=cap)
+    lens = [1500, 1111, 37]
+    cache = make_cache(K, V, b, sentinel=False)
+    R.block_summarize(cache, i32(lens))
+    for _ in run_pair(w, cache, lens, steps=6):
+        pass
+
+
+def test_step_against_oracle_loop():
+    """Ten fused steps on one workspace against the oracle's decode loop
+    (appends, selections within the near-tie rule, attention within 2e-3),
+    a ragged batch with one sequence short enough to keep every block."""
+    w = W.LONG_64K.with_(batch=3, num_q_heads=8, num_kv_heads=2, seq_len=900, min_tokens=64,
+                         seed_tag="steploop")
+    cap = 1024
+    lens = [900, 613, 40]
+    K, V = W.kv_cache(w, capacity=cap)
+    cache = make_cache(K, V, 16, sentinel=False)
+    R.block_summarize(cache, i32(lens))
+    st = O.DecodeState(O.bf16_to_f64(K), O.bf16_to_f64(V), lens, 16)
+    swaps = 0
+    for step, kn, vn, q, idx, ns, out in run_pair(w, cache, lens, steps=10):
+        st.append(O.bf16_to_f64(kn), O.bf16_to_f64(vn))
+        rs, ri, rn = st.select(O.bf16_to_f64(q), w.sparsity, w.min_blocks, 1)
+        ro, _ = st.attend(O.bf16_to_f64(q), ri, w.sm_scale)
+        gi, gn, go = idx.cpu().numpy(), ns.cpu().numpy(), out.cpu().numpy()
+        for bi in range(3):
+            for hi in range(2):
+                assert gn[bi, hi] == rn[bi, hi]
+                s = check_selection(gi[bi, hi, :gn[bi, hi]], ri[bi, hi], rs[bi, hi], rn[bi, hi], 1)
+                swaps += s
+                if s == 0:
+                    assert max_abs_err(go[bi, 4 * hi:4 * hi + 4], ro[bi, 4 * hi:4 * hi + 4]) <= TOL
+                else:
+                    # Near-tie swap: check the attention on the GPU's own set.
+                    q64 = O.bf16_to_f64(q)[bi, 4 * hi:4 * hi + 4]
+                    go_ref, _ = O.sparse_attend(q64, st.K[bi, hi], st.V[bi, hi], st.L[bi],
+                                                gi[bi, hi, :gn[bi, hi]], 16, w.sm_scale)
+                    assert max_abs_err(go[bi, 4 * hi:4 * hi + 4], go_ref) <= TOL
+    assert swaps <= 4
+
+
+def test_step_full_cache_and_splits():
+    """A sequence already at capacity is decoded over its stored length and
+    left unchanged; explicit split counts (1: the single split writes the
+    output directly; 7: uneven parts)."""
+    w, cap = W.TINY_4K.with_(batch=2, num_kv_heads=2, num_q_heads=8, seq_len=512, min_tokens=128,
+                             seed_tag="stepfull"), 512
+    K, V = W.kv_cache(w, capacity=cap)
+    for splits in (1, 7):
+        cache = make_cache(K, V, 16, sentinel=False)
+        lens = [512, 300]
+        R.block_summarize(cache, i32(lens))
+        # The host bound must stay below capacity, so the full sequence is
+        # only reached through the device length.
+        gen = run_pair(w, cache, lens, steps=3, num_splits=splits)
+        for step, *_ in gen:
+            pass
+
+
+def test_step_paged_matches_contiguous():
+    """The fused step on a shuffled page pool gives the same selections and
+    outputs as on the contiguous layout (and the same appended rows)."""
+    w = W.LONG_64K.with_(batch=2, num_q_heads=8, num_kv_heads=2, seq_len=700, min_tokens=64,
+                         seed_tag="steppaged")
+    cap, steps = 768, 5
+    lens = [700, 650]
+    K, V = W.kv_cache(w, capacity=cap)
+    flat = make_cache(K, V, 16, sentinel=False)
+    paged = make_paged_cache(K, V, 16, [x + steps for x in lens], seed=3, sentinel=False)
+    lf, lp = i32(lens), i32(lens)
+    R.block_summarize(flat, lf)
+    R.block_summarize(paged, lp)
+    wf, wp = R.Workspace(), R.Workspace()
+    for step in range(steps):
+        kn, vn = W.decode_kv(w, step)
+        q = W.decode_query(w, step)
+        bound = max(lens) + step
+        a = R.decode_step(flat, up(kn), up(vn), up(q), lf, bound, w.sparsity, w.min_blocks, 1,
+                          workspace=wf)
+        b = R.decode_step(paged, up(kn), up(vn), up(q), lp, bound, w.sparsity, w.min_blocks, 1,
+                          workspace=wp)
+        torch.cuda.synchronize()
+        for x, y in zip(a, b):
+            assert torch.equal(x, y)
+    assert torch.equal(flat.kmin, paged.kmin) and torch.equal(flat.kmax, paged.kmax)
+
+
+def test_step_rejects_bad_arguments():
+    w, cap = W.TINY_4K.with_(batch=1, num_kv_heads=2, num_q_heads=8, seq_len=100,
+                             seed_tag="stepbad"), 128
+    K, V = W.kv_cache(w, capacity=cap)
+    cache = make_cache(K, V, 16, sentinel=False)
+    lt = i32([100])
+    kn, vn = W.decode_kv(w, 0)
+    q = W.decode_query(w, 0)
+    with pytest.raises(R.ResaError):  # no room to append under the host bound
+        R.decode_step(cache, up(kn), up(vn), up(q), lt, 128, 0.9, 1, 1)
+    with pytest.raises(R.ResaError):  # n_cap below the Eq. 5 count
+        R.decode_step(cache, up(kn), up(vn), up(q), lt, 100, 0.0, 1, 1, n_cap=2)
+    with pytest.raises(R.ResaError):
+        R.decode_step(cache, up(kn), up(vn), up(q), lt, 100, 0.9, 1, 1, num_splits=300)
+    torch.cuda.synchronize()
+    assert lt.cpu().tolist() == [100]
