@@ -1,25 +1,28 @@
 """Benchmark of the ReSA decode hot path on one MI355X.
 
 A step is one decode token of one attention layer for the whole batch:
-append the token's K/V (online block-summary update) and select blocks
-(pooled query, Quest score, top-n) in one launch (resa_append_select; two
-launches with --separate), then run block-sparse flash-decoding; every f-th
-step of a layer also runs the dense rectification of its last f rows. The
-default workload is the 64K batch-8 decode loop (32 query / 8 kv heads,
-head_dim 128, block 16, sparsity 0.9 with a 2048-token minimum, f = 32,
-LogNormal(0, 0.5) key channels). Steps cycle through `--layers` independent
-layer caches, as a model's layers do, so data reused from one step to the
-next cannot be served by the 256 MB last-level cache.
+append the token's K/V (online block-summary update), select blocks (pooled
+query, Quest score, top-n) and run block-sparse flash-decoding; every f-th
+step of a layer also runs the dense rectification of its last f rows. By
+default the step is resa_append_select then resa_sparse_decode (--mode two);
+--mode step runs one launch of resa_decode_step, --mode three (--separate)
+resa_append_kv, resa_select_blocks and resa_sparse_decode. The default
+workload is the 64K batch-8 decode loop (32 query / 8 kv heads, head_dim 128,
+block 16, sparsity 0.9 with a 2048-token minimum, f = 32, LogNormal(0, 0.5)
+key channels). Steps cycle through `--layers` independent layer caches, as a
+model's layers do, so data reused from one step to the next cannot be served
+by the 256 MB last-level cache.
 
 Prints one JSON line. `value` is the GPU time of the timed steps (HIP events
 on the launch stream around the whole loop). By default the timed steps are
 recorded once into a HIP graph and replayed, as a serving loop would run
 them; `--eager` launches every step from the host instead (the gaps between
-host launches then count too). The
-per-kernel figures come from a second pass that replays every launch of one
-kernel from the timed loop back to back between two events; the sparse-decode
-roofline divides the bytes of the selected K/V blocks per launch by that
-average duration.
+host launches then count too). The per-kernel figures come from a second
+pass that replays every launch of one kernel from the timed loop back to
+back between two events. `roofline` is for the step's dominant kernel: the
+fused step (bytes of the block summaries and of the selected K/V blocks) or,
+with --mode two / three, the sparse decode (selected K/V); `decode_roofline`
+is always the standalone sparse-decode kernel on the same selections.
 """
 from __future__ import annotations
 
@@ -65,8 +68,12 @@ def parse():
                         "from one HIP graph")
     p.add_argument("--prefill", action="store_true",
                    help="time prefill (chunked and whole-prompt) through the rectification call")
-    p.add_argument("--separate", action="store_true",
-                   help="append and select as two launches instead of resa_append_select")
+    p.add_argument("--mode", choices=["step", "two", "three"], default="two",
+                   help="step: resa_decode_step (append + select + decode in one launch); "
+                        "two: resa_append_select then resa_sparse_decode; three: resa_append_kv, "
+                        "resa_select_blocks, resa_sparse_decode")
+    p.add_argument("--separate", dest="mode", action="store_const", const="three",
+                   help="same as --mode three")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work")
     p.add_argument("--copy-probe", type=int, default=0,
@@ -95,13 +102,14 @@ def describe(w, layers, dense):
             + f"rectify every {w.rectify_every} steps, {layers} layer caches in rotation")
 
 
-def traffic_from_profile(kernel_src: str, workload: str | None):
-    """HBM bytes per decode launch measured by rocprofv3 PMC counters for this
-    workload, if a committed profile of it was taken on the current kernel
+def traffic_from_profile(kernel_src: str, stem: str | None):
+    """HBM bytes per launch measured by rocprofv3 PMC counters, read from
+    profiles/<stem>_pmc.md (stem = kernel and workload, e.g.
+    sparse_decode_long64k) if that profile was taken on the current kernel
     source; else None (also for variants: dense, paged, overridden sizes)."""
-    if workload is None:
+    if stem is None:
         return None
-    path = os.path.join(ROOT, "profiles", f"sparse_decode_{workload.replace('_', '')}_pmc.md")
+    path = os.path.join(ROOT, "profiles", f"{stem}_pmc.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -224,6 +232,9 @@ def measure(args, w, dense: bool) -> dict:
                            device=dev) for _ in range(nlay)]
     ws_dec = torch.zeros(lb.resa_decode_workspace_size(B, H, Hq, n_cap, b, splits), dtype=torch.uint8,
                          device=dev)
+    # Fused steps: one workspace per layer as well (it holds the selection hint).
+    ws_steps = [torch.zeros(max(lb.resa_step_workspace_size(B, H, Hq, cap - 1, b, n_cap, splits), 256),
+                            dtype=torch.uint8, device=dev) for _ in range(nlay)] if args.mode == "step" else []
     ws_rec = torch.zeros(lb.resa_rectify_workspace_size(B, H, Hq, f, cap), dtype=torch.uint8, device=dev)
     rout = torch.empty((B, Hq, f, D), dtype=torch.float32, device=dev)
     params = SelectParams(w.sparsity, w.min_blocks, w.n_local)
@@ -253,7 +264,12 @@ def measure(args, w, dense: bool) -> dict:
         ly = layers[li]
         d = C.byref(ly["desc"])
         ids, ns = (idx_all[t], nsel_all[t]) if t >= 0 else (idx, nsel)
-        if phase == "append_select":
+        if phase == "step":
+            check(lb.resa_decode_step(d, ly["k"][s].data_ptr(), ly["v"][s].data_ptr(), ly["q"][s].data_ptr(),
+                                      Hq, ly["lens"].data_ptr(), Lcur, C.byref(params), ids.data_ptr(),
+                                      ns.data_ptr(), n_cap, splits, sm, out.data_ptr(), lse.data_ptr(),
+                                      ws_steps[li].data_ptr(), ws_steps[li].numel(), launch_stream[0]))
+        elif phase == "append_select":
             check(lb.resa_append_select(d, ly["k"][s].data_ptr(), ly["v"][s].data_ptr(), ly["q"][s].data_ptr(),
                                         Hq, ly["lens"].data_ptr(), Lcur, C.byref(params), ids.data_ptr(),
                                         ns.data_ptr(), n_cap, None, ws_sels[li].data_ptr(), ws_sels[li].numel(), launch_stream[0]))
@@ -285,8 +301,10 @@ def measure(args, w, dense: bool) -> dict:
         Lcur = L0 + s
         if dense:
             seq = ["append", "decode"]
-        elif args.separate:
+        elif args.mode == "three":
             seq = ["append", "select", "decode"]
+        elif args.mode == "step":
+            seq = ["step"]
         else:
             seq = ["append_select", "decode"]
         if not dense and (s + 1) % f == 0:
@@ -357,12 +375,15 @@ def measure(args, w, dense: bool) -> dict:
     # event packets between launches). Select, decode and rectify only read
     # the cache (rectify rewrites the rows it was given); the fused
     # append + select replay, last, appends the same tokens once more into the
-    # capacity kept for it. The plain append kernel (--separate, --dense) runs
-    # for less time than one host launch takes, so a replay would time the
-    # host; its duration is taken from a kernel trace instead.
+    # capacity kept for it (so does the fused step's replay). The plain append
+    # kernel (--mode three, --dense) runs for less time than one host launch
+    # takes, so a replay would time the host; its duration is taken from a
+    # kernel trace instead. With fused steps, the standalone decode kernel is
+    # also timed on the selections the steps made ("decode_alone", not part
+    # of the step).
     phase_us = {}
-    for ph in ("select", "decode", "rectify", "append_select"):
-        cs = [c for c in calls if c[0] == ph]
+    for ph in ("select", "decode", "decode_alone", "rectify", "append_select", "step"):
+        cs = [c for c in calls if c[0] == ("step" if ph == "decode_alone" else ph)]
         if not cs:
             continue
         a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -371,28 +392,43 @@ def measure(args, w, dense: bool) -> dict:
         for _, li, s, t, _ in cs:
             # The host length bound must hold for the cache as it is now.
             n = layers[li]["steps"]
-            if ph == "append_select":
+            if ph in ("append_select", "step"):
                 launch(ph, li, s, t, L0 + n)
                 layers[li]["steps"] = n + 1
             else:
-                launch(ph, li, s, t, L0 + n - 1)
+                launch("decode" if ph == "decode_alone" else ph, li, s, t, L0 + n - 1)
         z.record(stream)
         torch.cuda.synchronize()
         phase_us[ph] = a.elapsed_time(z) * 1e3 / len(cs)
 
-    # Algorithmic bytes of each decode launch: the selected blocks' K and V rows.
-    bytes_dec = []
+    # Algorithmic bytes of each launch: the selected blocks' K and V rows
+    # (decode), plus the kmin / kmax summaries of every block (fused step).
+    bytes_dec, bytes_sum = [], []
     for L in lens_seen:
         M = -(-L // b)
         n = M if dense else R.num_selected(M, w.sparsity, w.min_blocks, w.n_local)
         bytes_dec.append(B * H * n * b * D * 2 * 2)
-    avg_dec_us = phase_us["decode"]
+        bytes_sum.append(B * H * M * D * 2 * 2)
     avg_bytes = sum(bytes_dec) / len(bytes_dec)
-    achieved = avg_bytes / (avg_dec_us * 1e-6) / 1e9
-    kernel_src = os.path.join(ROOT, "paper_2506_04108_amd", "csrc", "decode.hip")
+    avg_sum = sum(bytes_sum) / len(bytes_sum)
     import workloads as W
-    plain = w == W.WORKLOADS.get(w.name) and not (dense or args.paged or args.separate)
-    traffic = traffic_from_profile(kernel_src, w.name if plain else None)
+    plain = w == W.WORKLOADS.get(w.name) and not (dense or args.paged or args.mode == "three")
+
+    def roof(kernel, src, profile, nbytes, us):
+        kernel_src = os.path.join(ROOT, "paper_2506_04108_amd", "csrc", src)
+        gbs = nbytes / (us * 1e-6) / 1e9
+        return {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(gbs / HBM_PEAK_GBS, 4),
+                "traffic": traffic_from_profile(kernel_src, f"{profile}_{w.name.replace('_', '')}"
+                                                if plain else None),
+                "kernel": kernel, "avg_launch_us": round(us, 3), "bytes_per_launch": int(nbytes)}
+
+    dec_key = "decode_alone" if "decode_alone" in phase_us else "decode"
+    dec_roof = roof("k_decode", "decode.hip", "sparse_decode", avg_bytes, phase_us[dec_key])
+    if "step" in phase_us:
+        roofline = roof("k_step", "step.hip", "decode_step", avg_bytes + avg_sum, phase_us["step"])
+    else:
+        roofline = dec_roof
     ms_per_step = gpu_ms / args.steps
     n_calls = {ph: sum(1 for c in calls if c[0] == ph) for ph in phase_us}
     res = {
@@ -408,15 +444,14 @@ def measure(args, w, dense: bool) -> dict:
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": describe(w, nlay, dense), "batch": B, "q_heads": Hq, "kv_heads": H,
+        "config": {"workload": describe(w, nlay, dense), "mode": args.mode, "batch": B, "q_heads": Hq,
+                   "kv_heads": H,
                    "head_dim": D, "context_start": L0, "block_size": b,
                    "sparsity": None if dense else w.sparsity, "min_tokens": w.min_tokens,
                    "rectify_every": f, "decode_splits": splits, "layers_rotated": nlay,
                    "hip_graph": bool(args.graph), "paged": bool(args.paged)},
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic, "kernel": "k_decode",
-                     "avg_launch_us": round(avg_dec_us, 3), "bytes_per_launch": int(avg_bytes)},
+        "roofline": roofline,
+        "decode_roofline": dec_roof,
         "kernel_us_per_launch": {k: round(v, 2) for k, v in phase_us.items()},
         "kernel_us_per_step": {k: round(v * n_calls[k] / args.steps, 2) for k, v in phase_us.items()},
         "wall_us_per_step": round(wall * 1e6 / args.steps, 2),
@@ -431,6 +466,7 @@ def breakdown(args) -> dict:
     rectification (one call amortised over f steps)."""
     import workloads as W
     rows = []
+    args.mode = "two"  # estimation and attention as separate kernels
     for L in (16384, 65536, 262144):
         w = W.LONG_64K.with_(seq_len=L)
         sp = measure(args, w, False)

@@ -307,9 +307,12 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
   const size_t grp = (size_t)bb * a.c.kv_heads + hk;
   const int M = min((L + BS - 1) / BS, a.c.max_blocks);
   const int n = max(0, min(ld_i32<kCoherent>(a.num_sel + grp), a.n_cap));
+  // Split s takes chunk slots s, s + S, s + 2 S, ... of the group's n_cap *
+  // CPB slots: the id loads do not wait for the count n, and any n leaves
+  // the splits balanced to one chunk. Slots at or past n * CPB are skipped.
+  const int slots = a.n_cap * CPB > split ? (a.n_cap * CPB - split + S - 1) / S : 0;
   const int C = n * CPB;
-  const int c0 = (int)((int64_t)split * C / S);
-  const int c1 = (int)((int64_t)(split + 1) * C / S);
+  const int valid = C > split ? (C - split + S - 1) / S : 0;
   const int r = lane >> 4, c = lane & 15, col = c * 8;
   const int32_t* idx = a.block_idx + grp * a.n_cap;
 
@@ -347,14 +350,18 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
 #pragma unroll
     for (int d = 0; d < 8; ++d) acc[h][d] = 0.f;
 
-  for (int cb = c0; cb < c1; cb += kIdxBatch) {
-    const int ce = min(c1, cb + kIdxBatch);
-    // First token of each chunk of this pass (-1 for ids outside [0, M)) and
-    // the row holding it (0 for an invalid chunk: in bounds, masked out).
-    for (int i = thread_id(); i < ce - cb; i += 64 * NW) {
-      const int cc = cb + i;
+  // The first pass runs before the count is known (its id loads are issued
+  // first); later passes only while slots with chunks remain.
+  int cb = 0;
+  do {
+    const int ce = min(valid, cb + kIdxBatch);
+    // First token of each chunk of this pass (-1 for ids outside [0, M) and
+    // for slots past the count) and the row holding it (0 for an invalid
+    // chunk: in bounds, masked out).
+    for (int i = thread_id(); i < min(slots, cb + kIdxBatch) - cb; i += 64 * NW) {
+      const int cc = split + (cb + i) * S;
       const int blk = ld_i32<kCoherent>(idx + cc / CPB);
-      int t = (blk < 0 || blk >= M) ? -1 : blk * BS + (cc % CPB) * kChunk;
+      int t = (cb + i >= valid || blk < 0 || blk >= M) ? -1 : blk * BS + (cc % CPB) * kChunk;
       int row = t;
       if (paged && t >= 0) {
         const int page = a.c.table[(size_t)bb * a.c.max_blocks + blk];
@@ -367,10 +374,11 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
       lds.row[i] = t < 0 ? 0 : row;
     }
     lds_sync();
-    // Wave w takes chunks cb + w, cb + w + W, ... (W waves). A ring of
+    // Wave w takes slots cb + w, cb + w + W, ... (W waves). A ring of
     // kDepth + 1 chunk buffers keeps kDepth chunks' loads in flight while one
-    // is consumed; an invalid chunk reads row 0 (in bounds) and is masked out
-    // entirely. The scheduling barriers keep the refills ahead of the compute.
+    // is consumed; an invalid chunk inside the pass reads row 0 (in bounds)
+    // and is masked out entirely, and nothing is loaded past the pass. The
+    // scheduling barriers keep the refills ahead of the compute.
     auto tok = [&](int cc) -> int { return cc < ce ? __builtin_amdgcn_readfirstlane(lds.tok[cc - cb]) : -1; };
     // The chunk holding token pos (appended in this launch) takes that row
     // from k_new / v_new: lane row r + 4 iv of the chunk is K slot iv ^ rperm
@@ -397,8 +405,10 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
 #pragma unroll
     for (int k = 0; k <= kDepth; ++k) {
       tring[k] = tok(cc + k * NW);
-      load_chunk(ring[k], kp, vp, krow, row_of(cc + k * NW));
-      patch(ring[k], tring[k]);
+      if (cc + k * NW < ce) {  // no loads past the pass
+        load_chunk(ring[k], kp, vp, krow, row_of(cc + k * NW));
+        patch(ring[k], tring[k]);
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
     while (cc < ce) {
@@ -408,15 +418,18 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
           consume_chunk<G>(ring[k], tring[k], r, c, L, scale, q, st, acc);
           __builtin_amdgcn_sched_barrier(0);
           tring[k] = tok(cc + (kDepth + 1) * NW);
-          load_chunk(ring[k], kp, vp, krow, row_of(cc + (kDepth + 1) * NW));
-          patch(ring[k], tring[k]);
+          if (cc + (kDepth + 1) * NW < ce) {
+            load_chunk(ring[k], kp, vp, krow, row_of(cc + (kDepth + 1) * NW));
+            patch(ring[k], tring[k]);
+          }
           __builtin_amdgcn_sched_barrier(0);
           cc += NW;
         }
       }
     }
     lds_sync();
-  }
+    cb += kIdxBatch;
+  } while (cb < valid);
 
   // Per-head state of this lane's row group: head h lives in lane 16 r + h.
   float m_[G], l_[G];
