@@ -59,6 +59,8 @@ def parse():
     p.add_argument("--sparsity", type=float, default=None)
     p.add_argument("--rectify-every", type=int, default=None)
     p.add_argument("--dense", action="store_true", help="dense baseline: decode over every block")
+    p.add_argument("--sweep", action="store_true",
+                   help="64K batch-8 sweep: block size x sparsity x rectify interval, and dense decoding")
     p.add_argument("--breakdown", action="store_true",
                    help="latency breakdown at 16K/64K/256K (batch 8) against dense decoding")
     p.add_argument("--paged", action="store_true",
@@ -74,6 +76,8 @@ def parse():
                         "resa_select_blocks, resa_sparse_decode")
     p.add_argument("--separate", dest="mode", action="store_const", const="three",
                    help="same as --mode three")
+    p.add_argument("--splits", type=int, default=0,
+                   help="decode splits per (sequence, kv head); 0 = the library's choice")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work")
     p.add_argument("--copy-probe", type=int, default=0,
@@ -225,7 +229,7 @@ def measure(args, w, dense: bool) -> dict:
     nsel = torch.empty((B, H), dtype=torch.int32, device=dev)
     out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
     lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
-    splits = R.decode_num_splits(B, H, n_cap, b)
+    splits = args.splits if args.splits > 0 else R.decode_num_splits(B, H, n_cap, b)
     # One selection workspace per layer: besides scratch it carries the
     # digit-window hint of the layer's previous call.
     ws_sels = [torch.zeros(max(lb.resa_select_workspace_size(B, H, cap, b), 256), dtype=torch.uint8,
@@ -485,6 +489,38 @@ def breakdown(args) -> dict:
     return {"breakdown": rows, "workload": describe(W.LONG_64K, args.layers, False)}
 
 
+def sweep(args) -> dict:
+    """The 64K batch-8 sweep (block size 16/32/64 x sparsity 0.8/0.9/0.95 x
+    rectify interval 16/32/64, N(0, 1) caches with 1 % planted blocks) and,
+    per block size, dense decoding over every block. Each point runs 2 f
+    timed steps over two layer caches (so each layer is rectified once);
+    us_per_step is the GPU time of those steps, rectification included."""
+    import workloads as W
+    rows = []
+    args.mode, args.layers = "two", 2
+    for w in W.sweep_points():
+        f = w.rectify_every
+        args.steps, args.warmup = 2 * f, 4
+        r = measure(args, w, False)
+        k = r["kernel_us_per_launch"]
+        rows.append({"block_size": w.block_size, "sparsity": w.sparsity, "f": f,
+                     "us_per_step": r["value"],
+                     "estimation_us": round(k["append_select"], 2), "attention_us": round(k["decode"], 2),
+                     "rectification_us_per_step": round(k.get("rectify", 0.0) / f, 2),
+                     "decode_hbm_frac": r["roofline"]["frac"]})
+        log(f"[bench] sweep b={w.block_size} s={w.sparsity} f={f}: {r['value']} us/step")
+    dense = {}
+    for b in (16, 32, 64):
+        w = W.SWEEP_64K.with_(block_size=b, planted_per_head=0)
+        args.steps, args.warmup = 32, 4
+        r = measure(args, w, True)
+        dense[b] = {"us_per_step": r["value"], "decode_us": r["kernel_us_per_launch"]["decode"],
+                    "decode_hbm_frac": r["roofline"]["frac"]}
+    for row in rows:
+        row["speedup_vs_dense"] = round(dense[row["block_size"]]["us_per_step"] / row["us_per_step"], 3)
+    return {"sweep": rows, "dense": dense, "workload": describe(W.SWEEP_64K, 2, False)}
+
+
 MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 / fp16 matrix-core peak
 
 
@@ -554,6 +590,9 @@ def main():
     torch.cuda.set_device(0)
     if args.breakdown:
         print(json.dumps(breakdown(args)), flush=True)
+        return
+    if args.sweep:
+        print(json.dumps(sweep(args)), flush=True)
         return
     if args.prefill:
         print(json.dumps(prefill(args)), flush=True)

@@ -161,7 +161,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
   // Window hint left by the previous call on this workspace (any value is
   // valid: it only chooses which key bits get a second histogram).
   const uint32_t win = a.fused ? a.window[grp] : 0u;
-  score_range<kSelWaves>(a, bb, hk, sl, M, forced_from, b0, b1, blockIdx.x, gridDim.x, win, s_hist, s_score);
+  score_range<kSelWaves, 1>(a, bb, hk, sl, M, forced_from, b0, b1, blockIdx.x, gridDim.x, win, s_hist, s_score);
   if (!a.fused) return;
   __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();

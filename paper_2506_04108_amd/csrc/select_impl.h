@@ -447,7 +447,7 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
 // Pooled query (Fig. 3) and Quest scores (Eq. 4) of blocks [b0, b1) of group
 // (bb, hk), range `range` of the group's `nranges`, by a workgroup of NW
 // waves. Lane (r, c) handles dims [8c, 8c + 8) of 16-block tiles, so each
-// wave-wide load is four whole 256-byte summary rows, and the next tile's
+// wave-wide load is four whole 256-byte summary rows, and the next PF tiles'
 // loads are in flight while one is scored. Per dimension the larger of
 // q*kmax and q*kmin is the product with kmax when q >= 0 and with kmin
 // otherwise (exactly, as fp32 rounding is monotone), so the summary row is
@@ -456,7 +456,7 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
 // workgroup also counts its keys' 8 high bits (and 8 more inside the window
 // hint `win`) into its own histogram slot with agent-scope stores. Returns
 // with those stores issued (the caller waits for them before its ticket).
-template <int NW>
+template <int NW, int PF>
 __device__ __forceinline__ void score_range(const SelectArgs& a, int bb, int hk, const SeqLen& sl, int M,
                                             int forced_from, int b0, int b1, int range, int nranges,
                                             uint32_t win, uint32_t* s_hist, float* s_score) {
@@ -523,16 +523,13 @@ __device__ __forceinline__ void score_range(const SelectArgs& a, int bb, int hk,
         hi4[u] = ld16_stream(kmax + (size_t)m * kHeadDim);
       }
     };
-    U4 lo4[4], hi4[4], nlo[4], nhi[4];
-    int t = wave;
-    load_tile(min(t, ntiles - 1), lo4, hi4);
-    while (t < ntiles) {
-      load_tile(min(t + NW, ntiles - 1), nlo, nhi);
-      __builtin_amdgcn_sched_barrier(0);
+    // Tile t of this wave's tiles t = wave, wave + NW, ...: scored from its
+    // buffers; PF more tiles are in flight meanwhile (a ring of PF + 1).
+    auto score_tile = [&](int t, U4 (&lo4)[4], U4 (&hi4)[4]) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int mu = b0 + 16 * t + 4 * u + r;
-        if (mu == m_new && mu < b1) {
+        const int m = b0 + 16 * t + 4 * u + r;
+        if (m == m_new && m < b1) {
           lo4[u] = opening ? knew : u4_min(lo4[u], knew);
           hi4[u] = opening ? knew : u4_max(hi4[u], knew);
           new_lo = lo4[u];
@@ -550,7 +547,6 @@ __device__ __forceinline__ void score_range(const SelectArgs& a, int bb, int hk,
           s = fmaf(qb[2 * j + 1], a1, s);
         }
         s = row16_sum(s);
-        const int m = b0 + 16 * t + 4 * u + r;
         if (c == 0 && m < b1) {
           s_score[m - b0] = s;
           if (a.fused) {
@@ -560,13 +556,24 @@ __device__ __forceinline__ void score_range(const SelectArgs& a, int bb, int hk,
           }
         }
       }
-      __builtin_amdgcn_sched_barrier(0);
+    };
+    constexpr int P = PF + 1;
+    U4 lo4[P][4], hi4[P][4];
+    int t = wave;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        lo4[u] = nlo[u];
-        hi4[u] = nhi[u];
+    for (int k = 0; k < P; ++k)
+      if (t + k * NW < ntiles) load_tile(t + k * NW, lo4[k], hi4[k]);
+    while (t < ntiles) {
+#pragma unroll
+      for (int k = 0; k < P; ++k) {
+        if (t < ntiles) {
+          score_tile(t, lo4[k], hi4[k]);
+          __builtin_amdgcn_sched_barrier(0);
+          if (t + P * NW < ntiles) load_tile(t + P * NW, lo4[k], hi4[k]);
+          __builtin_amdgcn_sched_barrier(0);
+          t += NW;
+        }
       }
-      t += NW;
     }
   }
   lds_sync();

@@ -76,7 +76,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step(StepArgs) {
     const int b0 = range * sa.blocks_per_wg;
     const int b1 = min(b0 + sa.blocks_per_wg, M);
     const uint32_t win = sa.window[g];
-    score_range<kStepWaves>(sa, bb, hk, sl, M, forced_from, b0, b1, range, a.nranges, win, s_hist, s_score);
+    score_range<kStepWaves, 3>(sa, bb, hk, sl, M, forced_from, b0, b1, range, a.nranges, win, s_hist, s_score);
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     if (tid == 0)
