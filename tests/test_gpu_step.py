@@ -175,3 +175,126 @@ def test_step_rejects_bad_arguments():
         R.decode_step(cache, up(kn), up(vn), up(q), lt, 100, 0.9, 1, 1, num_splits=300)
     torch.cuda.synchronize()
     assert lt.cpu().tolist() == [100]
+
+
+def test_step_graph_replay_matches_eager():
+    """The fused step recorded once in a HIP graph and replayed for several
+    steps (inputs copied in between, eager calls and synchronisations between
+    the replays) matches the same calls made eagerly, bit for bit: its
+    counters and flags return to zero inside the kernel, with no memset."""
+    w = W.LONG_64K.with_(batch=2, num_q_heads=8, num_kv_heads=2, seq_len=600, min_tokens=64,
+                         seed_tag="stepgraph")
+    b, cap, steps = 16, 704, 4
+    B, H, Hq = 2, 2, 8
+    K, V = W.kv_cache(w, capacity=cap)
+    c1 = make_cache(K, V, b, sentinel=False)
+    c2 = make_cache(K, V, b, sentinel=False)
+    lens0 = [600, 555]
+    l1, l2 = i32(lens0), i32(lens0)
+    R.block_summarize(c1, l1)
+    R.block_summarize(c2, l2)
+    bound = max(lens0) + steps
+    n_cap = R.num_selected(-(-(bound + 1) // b), w.sparsity, w.min_blocks, w.n_local)
+    d = torch.device("cuda:0")
+    bf = torch.bfloat16
+    kn_s = torch.zeros((B, H, 128), dtype=bf, device=d)
+    vn_s = torch.zeros((B, H, 128), dtype=bf, device=d)
+    q_s = torch.zeros((B, Hq, 128), dtype=bf, device=d)
+    idx2 = torch.empty((B, H, n_cap), dtype=torch.int32, device=d)
+    ns2 = torch.empty((B, H), dtype=torch.int32, device=d)
+    out2 = torch.empty((B, Hq, 128), dtype=torch.float32, device=d)
+    lse2 = torch.empty((B, Hq), dtype=torch.float32, device=d)
+    w1, w2 = R.Workspace(d), R.Workspace(d)
+    for ws in (w1, w2):
+        ws.get(R.lib().resa_step_workspace_size(B, H, Hq, bound, b, n_cap, 0))
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.graph(graph, stream=side):
+        R.decode_step(c2, kn_s, vn_s, q_s, l2, bound, w.sparsity, w.min_blocks, w.n_local, n_cap=n_cap,
+                      block_idx=idx2, num_sel=ns2, out=out2, lse=lse2, workspace=w2)
+    torch.cuda.synchronize()
+    for step in range(steps):
+        kn, vn = W.decode_kv(w, step)
+        q = W.decode_query(w, step)
+        kn_s.copy_(up(kn))
+        vn_s.copy_(up(vn))
+        q_s.copy_(up(q))
+        graph.replay()
+        torch.cuda.synchronize()
+        i1, n1, o1, s1 = R.decode_step(c1, up(kn), up(vn), up(q), l1, bound, w.sparsity, w.min_blocks,
+                                       w.n_local, n_cap=n_cap, workspace=w1)
+        torch.cuda.synchronize()
+        print(f"step graph replay {step}: n_sel {ns2.cpu().tolist()}", flush=True)
+        assert step_error_flag(w2) == 0
+        assert torch.equal(l1, l2)
+        assert torch.equal(n1, ns2) and torch.equal(i1, idx2)
+        assert torch.equal(o1, out2) and torch.equal(s1, lse2)
+    for f in ("k", "v", "kmin", "kmax"):
+        assert torch.equal(getattr(c1, f), getattr(c2, f)), f
+
+
+@pytest.mark.parametrize("name", ["long_64k", "extreme_256k"])
+def test_step_fullsize(name):
+    """The fused step at the full 64K (8 x 32/8 heads) and 256K (1 x 32/8)
+    shapes against resa_append_select + resa_sparse_decode on a copy of the
+    cache (identical selections, outputs within fp32 reordering), and sampled
+    groups against the oracle."""
+    w = W.WORKLOADS[name]
+    B, H, Hq, D, b, L = w.batch, w.num_kv_heads, w.num_q_heads, w.head_dim, w.block_size, w.seq_len
+    g = w.group_size
+    cap = -(-(L + 64) // b) * b
+    d = torch.device("cuda:0")
+    gen = torch.Generator(device=d)
+    gen.manual_seed(4109)
+    K = torch.randn((B, H, cap, D), generator=gen, device=d).to(torch.bfloat16)
+    V = torch.randn((B, H, cap, D), generator=gen, device=d).to(torch.bfloat16)
+    sampled = [(0, 0), (B - 1, H - 1)]
+    host = {}
+    for bi, hi in sampled:
+        k, v = W.group_kv(w, bi, hi)
+        K[bi, hi, :L] = up(k)
+        V[bi, hi, :L] = up(v)
+        host[bi, hi] = (k, v)
+    mb = cap // b
+    mk = lambda: torch.empty((B, H, mb, D), dtype=torch.bfloat16, device=d)
+    c1 = R.KVCache(K, V, mk(), mk(), b)
+    lens1 = i32([L] * B)
+    R.block_summarize(c1, lens1)
+    c2 = clone(c1)
+    lens2 = lens1.clone()
+    n_cap = R.num_selected(mb, w.sparsity, w.min_blocks, w.n_local)
+    print(f"[step fullsize] {name}: B={B} Hq={Hq} Hkv={H} L={L} n_cap={n_cap}", flush=True)
+    kn, vn = W.decode_kv(w, 0)
+    q = W.decode_query(w, 0)
+    ws = R.Workspace(d)
+    idx, ns, out, lse = R.decode_step(c1, up(kn), up(vn), up(q), lens1, L, w.sparsity, w.min_blocks,
+                                      w.n_local, n_cap=n_cap, workspace=ws)
+    ri, rn = R.append_select(c2, up(kn), up(vn), up(q), lens2, L, w.sparsity, w.min_blocks, w.n_local,
+                             n_cap=n_cap)
+    ro, rl = R.sparse_decode(c2, up(q), lens2, ri, rn)
+    torch.cuda.synchronize()
+    assert step_error_flag(ws) == 0
+    assert torch.equal(lens1, lens2) and torch.equal(ns, rn) and torch.equal(idx, ri)
+    assert max_abs_err(out.cpu().numpy(), ro.cpu().numpy()) <= REORDER
+    assert max_abs_err(lse.cpu().numpy(), rl.cpu().numpy()) <= REORDER
+    gi, gn, go = idx.cpu().numpy(), ns.cpu().numpy(), out.cpu().numpy()
+    q64 = O.bf16_to_f64(q)
+    for bi, hi in sampled:
+        k, v = host[bi, hi]
+        Kg = np.zeros((1, 1, L + 1, D))
+        Vg = np.zeros((1, 1, L + 1, D))
+        Kg[0, 0, :L] = O.bf16_to_f64(k)
+        Vg[0, 0, :L] = O.bf16_to_f64(v)
+        st = O.DecodeState(Kg, Vg, [L], b)
+        st.append(O.bf16_to_f64(kn)[bi:bi + 1, hi:hi + 1], O.bf16_to_f64(vn)[bi:bi + 1, hi:hi + 1])
+        qg = q64[bi:bi + 1, hi * g:(hi + 1) * g]
+        rs_, ri_, rn_ = st.select(qg, w.sparsity, w.min_blocks, w.n_local)
+        assert gn[bi, hi] == rn_[0, 0]
+        ids = gi[bi, hi, :gn[bi, hi]]
+        check_selection(ids, ri_[0, 0], rs_[0, 0], rn_[0, 0], w.n_local)
+        o_ref, _ = O.sparse_attend(qg[0], st.K[0, 0], st.V[0, 0], L + 1, ids, b, w.sm_scale)
+        err = max_abs_err(go[bi, hi * g:(hi + 1) * g], o_ref)
+        print(f"[step fullsize] {name} group ({bi},{hi}): |dO| {err:.2e}", flush=True)
+        assert err <= TOL
