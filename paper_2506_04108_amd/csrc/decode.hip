@@ -11,7 +11,7 @@ constexpr int kDecodeWaves = 4;
 template <int G, int BS>
 __global__ __launch_bounds__(64 * kDecodeWaves) void k_decode(DecodeArgs a) {
   __shared__ DecodeLds<G, kDecodeWaves> lds;
-  decode_split<G, BS, kDecodeWaves, false>(a, blockIdx.z, blockIdx.y, blockIdx.x, a.seq_lens[blockIdx.z], -1, lds);
+  decode_split<G, BS, kDecodeWaves, false>(a, blockIdx.z, blockIdx.y, blockIdx.x, a.seq_lens, false, lds);
 }
 
 template <int G>

@@ -30,6 +30,15 @@ namespace {
 constexpr int kIdxBatch = 1024;  // chunk start tokens staged in LDS per pass
 constexpr int kMaxSplits = 256;  // splits per group (bounded by the host)
 
+// The thread index: opaque in the persistent step kernel (kOpaque, see
+// thread_id), plain otherwise (an opaque move would also keep the compiler
+// from reading uniform data with scalar loads).
+template <bool kOpaque>
+__device__ __forceinline__ int tid_of() {
+  if constexpr (kOpaque) return thread_id();
+  else return (int)threadIdx.x;
+}
+
 // One 16-token chunk of K and V for this lane: four K rows (in the lane's
 // permuted order) and V rows r, r+4, r+8, r+12.
 struct Chunk {
@@ -184,13 +193,13 @@ __device__ __forceinline__ void consume_chunk(const Chunk& ch, int t0, int r, in
 // summing splits ph, ph + T, ...; the T sums are added through LDS.
 constexpr int kTailBatch = 16;    // partial loads per thread per round
 
-template <int G, int NT>
+template <int G, int NT, bool kOpaque>
 __device__ void merge_tail(const DecodeArgs& a, size_t grp, int S, size_t ob, float* s_lse,
                            f4_t* s_red) {
   constexpr int U = G * (kHeadDim / 4);
   constexpr int T = U >= NT ? 1 : NT / U;
   constexpr int kLse = (kMaxSplits * G + NT - 1) / NT;
-  const int tid = thread_id();
+  const int tid = tid_of<kOpaque>();
   const float ninf = -__builtin_inff();
   const float* pl = a.part_lse + grp * S * (size_t)G;
   const float* po = a.part_o + grp * S * (size_t)(G * kHeadDim);
@@ -288,33 +297,58 @@ __device__ __forceinline__ int ld_i32(const int32_t* p) {
   else return *p;
 }
 
+
 // Split `split` of group (bb, hk) by a workgroup of NW waves: wave w takes
-// chunks c0 + w, c0 + w + NW, ... of the split's range. L is the group's
-// length. With pos >= 0 the row of token pos is taken from a.k_new / a.v_new
-// (the token appended in the same launch) instead of the cache. kCoherent:
-// the ids and the count were written by another workgroup of the same
-// launch, so they are read with agent-scope loads. Every workgroup of the
-// group writes its partial (several splits) and the last one to finish
-// merges them; returns true in the workgroup that wrote the group's output.
+// chunks c0 + w, c0 + w + NW, ... of the split's range. The group's length
+// is lens[bb]; with `append` (the fused step) a sequence below capacity has
+// one more token, appended in the same launch at row lens[bb], whose row is
+// taken from a.k_new / a.v_new instead of the cache. kCoherent: the ids and
+// the count were written by another workgroup of the same launch (agent-scope
+// loads; also selects the opaque thread index of the persistent kernel).
+// Every workgroup of the group writes its partial (several splits) and the
+// last one to finish merges them; returns true in the workgroup that wrote
+// the group's output.
+//
+// Start-up: the count, the length, the query rows and the first pass's ids
+// are all requested before anything waits for one of them (vector loads, so
+// one wait covers them), which leaves one memory round trip between the
+// kernel arguments and the first K / V loads.
 template <int G, int BS, int NW, bool kCoherent, int kDepth = 2>
-__device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk, int split, int L, int pos,
-                                             DecodeLds<G, NW>& lds) {
+__device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk, int split,
+                                             const int32_t* lens, bool append, DecodeLds<G, NW>& lds) {
   constexpr int GP = Pad<G>::GP;
   constexpr int CPB = BS / kChunk;  // chunks per block
-  const int lane = thread_id() & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(thread_id() >> 6);
+  constexpr int NT = 64 * NW;
+  constexpr int kPer = kIdxBatch / NT;  // ids per thread per pass
+  const int tid = tid_of<kCoherent>();
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int S = a.num_splits;
   const size_t grp = (size_t)bb * a.c.kv_heads + hk;
-  const int M = min((L + BS - 1) / BS, a.c.max_blocks);
-  const int n = max(0, min(ld_i32<kCoherent>(a.num_sel + grp), a.n_cap));
-  // Split s takes chunk slots s, s + S, s + 2 S, ... of the group's n_cap *
-  // CPB slots: the id loads do not wait for the count n, and any n leaves
-  // the splits balanced to one chunk. Slots at or past n * CPB are skipped.
-  const int slots = a.n_cap * CPB > split ? (a.n_cap * CPB - split + S - 1) / S : 0;
-  const int C = n * CPB;
-  const int valid = C > split ? (C - split + S - 1) / S : 0;
+  // The group's n_cap * CPB chunk slots are dealt to the splits in runs of
+  // NW consecutive slots (run k of split s holds slots (k S + s) NW ..
+  // + NW - 1), so a workgroup's waves read neighbouring chunks (one
+  // contiguous run of K and V for large blocks and dense decoding), the id
+  // loads do not wait for the count n, and any n leaves the splits balanced
+  // to one run. Slots at or past n * CPB are skipped.
+  auto slot_of = [&](int i) { return ((i / NW) * S + split) * NW + i % NW; };
+  auto count_below = [&](int T) {  // this split's slots below slot T
+    const int full = T / (S * NW), rem = T - full * S * NW;
+    return full * NW + min(max(rem - split * NW, 0), NW);
+  };
+  const int slots = count_below(a.n_cap * CPB);
   const int r = lane >> 4, c = lane & 15, col = c * 8;
   const int32_t* idx = a.block_idx + grp * a.n_cap;
+  int blkv[kPer];
+  auto load_ids = [&](int cb) {
+    const int lim = min(slots, cb + kIdxBatch) - cb;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int i = tid + j * NT;
+      blkv[j] = i < lim ? ld_i32<kCoherent>(idx + slot_of(cb + i) / CPB) : -1;
+    }
+  };
+  load_ids(0);
 
   // Lane c's registers hold K row i ^ rperm and query head h ^ hperm, so
   // that logit slot s = i * GP + h is value n = s ^ c (see transpose_reduce16).
@@ -342,6 +376,17 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
   const uint16_t* vp = a.c.v + gbase;
   const float scale = a.scale_log2;
   const float ninf = -__builtin_inff();
+  // The count and the length are requested last: the first use of either
+  // (a move into scalar registers) then waits for everything above at once.
+  const int n_raw = ld_i32<true>(a.num_sel + grp);
+  const int L0 = ld_i32<true>(lens + bb);
+  const bool app = append && L0 >= 0 && L0 < a.c.capacity;
+  const int L = app ? L0 + 1 : L0;
+  const int pos = app ? L0 : -1;
+  const int M = min((L + BS - 1) / BS, a.c.max_blocks);
+  const int n = max(0, min(n_raw, a.n_cap));
+  const int C = n * CPB;
+  const int valid = count_below(C);
 
   Soft st{ninf, 0.f};
   float acc[G][8];
@@ -350,28 +395,49 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
 #pragma unroll
     for (int d = 0; d < 8; ++d) acc[h][d] = 0.f;
 
-  // The first pass runs before the count is known (its id loads are issued
-  // first); later passes only while slots with chunks remain.
+  // The first pass's ids were requested above; later passes (only while
+  // slots with chunks remain) request theirs first thing.
   int cb = 0;
   do {
+    if (cb > 0) load_ids(cb);
     const int ce = min(valid, cb + kIdxBatch);
+    const int lim = min(slots, cb + kIdxBatch) - cb;
     // First token of each chunk of this pass (-1 for ids outside [0, M) and
     // for slots past the count) and the row holding it (0 for an invalid
-    // chunk: in bounds, masked out).
-    for (int i = thread_id(); i < min(slots, cb + kIdxBatch) - cb; i += 64 * NW) {
-      const int cc = split + (cb + i) * S;
-      const int blk = ld_i32<kCoherent>(idx + cc / CPB);
-      int t = (cb + i >= valid || blk < 0 || blk >= M) ? -1 : blk * BS + (cc % CPB) * kChunk;
-      int row = t;
-      if (paged && t >= 0) {
-        const int page = a.c.table[(size_t)bb * a.c.max_blocks + blk];
-        if ((unsigned)page < (unsigned)a.c.num_pages)
-          row = (page * a.c.kv_heads + hk) * BS + (cc % CPB) * kChunk;
-        else
-          t = -1;
+    // chunk: in bounds, masked out). Paged: every table entry of the pass is
+    // requested before any is used.
+    int tk[kPer], rw[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int i = tid + j * NT;
+      const int cc = slot_of(cb + i);
+      const int blk = blkv[j];
+      tk[j] = (i >= lim || cb + i >= valid || blk < 0 || blk >= M) ? -1 : blk * BS + (cc % CPB) * kChunk;
+      rw[j] = tk[j];
+    }
+    if (paged) {
+      int page[kPer];
+#pragma unroll
+      for (int j = 0; j < kPer; ++j)
+        page[j] = tk[j] >= 0 ? a.c.table[(size_t)bb * a.c.max_blocks + blkv[j]] : -1;
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) {
+        const int cc = slot_of(cb + tid + j * NT);
+        if (tk[j] >= 0) {
+          if ((unsigned)page[j] < (unsigned)a.c.num_pages)
+            rw[j] = (page[j] * a.c.kv_heads + hk) * BS + (cc % CPB) * kChunk;
+          else
+            tk[j] = -1;
+        }
       }
-      lds.tok[i] = t;
-      lds.row[i] = t < 0 ? 0 : row;
+    }
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int i = tid + j * NT;
+      if (i < lim) {
+        lds.tok[i] = tk[j];
+        lds.row[i] = tk[j] < 0 ? 0 : rw[j];
+      }
     }
     lds_sync();
     // Wave w takes slots cb + w, cb + w + W, ... (W waves). A ring of
@@ -477,7 +543,7 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
   const size_t ob = (size_t)bb * a.q_heads + (size_t)hk * G;
   float* po = a.part_o + (grp * S + split) * (size_t)(G * kHeadDim);
   float* pl = a.part_lse + (grp * S + split) * (size_t)G;
-  for (int o = thread_id(); o < G * kHeadDim; o += 64 * NW) {
+  for (int o = tid_of<kCoherent>(); o < G * kHeadDim; o += 64 * NW) {
     const int h = o / kHeadDim, d = o % kHeadDim;
     float mx = ninf;
 #pragma unroll
@@ -510,11 +576,11 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
   // loads and resets the counter for the next call.
   __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  if (thread_id() == 0)
+  if (tid_of<kCoherent>() == 0)
     lds.ticket = __hip_atomic_fetch_add(a.counters + grp, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
   if (lds.ticket != (uint32_t)(S - 1)) return false;
-  merge_tail<G, 64 * NW>(a, grp, S, ob, lds.w, lds.red);
+  merge_tail<G, 64 * NW, kCoherent>(a, grp, S, ob, lds.w, lds.red);
   return true;
 }
 

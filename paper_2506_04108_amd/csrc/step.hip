@@ -116,12 +116,11 @@ __global__ __launch_bounds__(kStepThreads) void k_step(StepArgs) {
     if (item >= a.dec_items) break;
     const int g = item / S, split = item - g * S;
     const int bb = g / H, hk = g - bb * H;
-    const SeqLen sl = seq_len_of(sa, bb);
     bool last = false;
     switch (sa.c.block_size) {
-      case 16: last = decode_split<G, 16, kStepWaves, true, kStepDepth<G>>(a.d, bb, hk, split, sl.L, sl.pos, dl); break;
-      case 32: last = decode_split<G, 32, kStepWaves, true, kStepDepth<G>>(a.d, bb, hk, split, sl.L, sl.pos, dl); break;
-      default: last = decode_split<G, 64, kStepWaves, true, kStepDepth<G>>(a.d, bb, hk, split, sl.L, sl.pos, dl); break;
+      case 16: last = decode_split<G, 16, kStepWaves, true, kStepDepth<G>>(a.d, bb, hk, split, sa.seq_lens, true, dl); break;
+      case 32: last = decode_split<G, 32, kStepWaves, true, kStepDepth<G>>(a.d, bb, hk, split, sa.seq_lens, true, dl); break;
+      default: last = decode_split<G, 64, kStepWaves, true, kStepDepth<G>>(a.d, bb, hk, split, sa.seq_lens, true, dl); break;
     }
     // Every split of the group has passed its wait (the merging workgroup
     // holds the last ticket): the flag returns to zero for the next call.
