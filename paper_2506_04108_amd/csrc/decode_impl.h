@@ -30,15 +30,6 @@ namespace {
 constexpr int kIdxBatch = 1024;  // chunk start tokens staged in LDS per pass
 constexpr int kMaxSplits = 256;  // splits per group (bounded by the host)
 
-// The thread index: opaque in the persistent step kernel (kOpaque, see
-// thread_id), plain otherwise (an opaque move would also keep the compiler
-// from reading uniform data with scalar loads).
-template <bool kOpaque>
-__device__ __forceinline__ int tid_of() {
-  if constexpr (kOpaque) return thread_id();
-  else return (int)threadIdx.x;
-}
-
 // One 16-token chunk of K and V for this lane: four K rows (in the lane's
 // permuted order) and V rows r, r+4, r+8, r+12.
 struct Chunk {

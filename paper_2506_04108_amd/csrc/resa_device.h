@@ -9,6 +9,7 @@ namespace resa {
 constexpr int kHeadDim = 128;
 constexpr int kWave = 64;
 constexpr int kChunk = 16;  // tokens handled per decode step of a wave
+constexpr int kMaxGroup = 8;  // query heads per kv head (RESA_MAX_GROUP)
 constexpr int kBufWord3 = 0x00020000;  // raw buffer resource word 3: 32-bit data format
 constexpr int kSc1 = 16;              // buffer cache policy: agent-scope coherent
 
@@ -36,6 +37,15 @@ __device__ __forceinline__ int thread_id() {
   int t = threadIdx.x;
   __asm__ volatile("" : "+v"(t));
   return t;
+}
+
+// The thread index: opaque in the persistent step kernel (kOpaque, see
+// thread_id), plain otherwise (an opaque move would also keep the compiler
+// from reading uniform data with scalar loads).
+template <bool kOpaque>
+__device__ __forceinline__ int tid_of() {
+  if constexpr (kOpaque) return thread_id();
+  else return (int)threadIdx.x;
 }
 
 __device__ __forceinline__ U4 ld16(const void* p) {

@@ -151,17 +151,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
   const int tid = threadIdx.x;
   const int hk = blockIdx.y, bb = blockIdx.z;
   const size_t grp = (size_t)bb * a.c.kv_heads + hk;
-  const SeqLen sl = seq_len_of(a, bb);
-  const int L = sl.L;
-  // Lengths beyond max_seq_len are clamped so every access stays in bounds.
-  const int M = max(0, min(min((L + a.c.block_size - 1) / a.c.block_size, a.max_blocks_seq), a.c.max_blocks));
-  const int forced_from = M - a.n_local;
-  const int b0 = blockIdx.x * a.blocks_per_wg;
-  const int b1 = min(b0 + a.blocks_per_wg, M);
-  // Window hint left by the previous call on this workspace (any value is
-  // valid: it only chooses which key bits get a second histogram).
-  const uint32_t win = a.fused ? a.window[grp] : 0u;
-  score_range<kSelWaves, 1>(a, bb, hk, sl, M, forced_from, b0, b1, blockIdx.x, gridDim.x, win, s_hist, s_score);
+  const RangeInfo ri = score_range<kSelWaves, 1, false>(a, bb, hk, blockIdx.x, gridDim.x, s_hist, s_score);
   if (!a.fused) return;
   __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
@@ -169,8 +159,8 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
     s_misc[3] = __hip_atomic_fetch_add(a.counters + grp, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
   if (s_misc[3] != gridDim.x - 1) return;
-  select_tail<NJ, kSelThreads>(a, grp, M, forced_from, gridDim.x, win, s_hist, s_lds32, s_misc,
-                               reinterpret_cast<int32_t*>(s_score), bb, L, nullptr);
+  select_tail<NJ, kSelThreads>(a, grp, ri.M, ri.forced_from, gridDim.x, ri.win, s_hist, s_lds32, s_misc,
+                               reinterpret_cast<int32_t*>(s_score), bb, ri.sl.L, nullptr);
 }
 
 }  // namespace

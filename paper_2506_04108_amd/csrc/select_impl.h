@@ -456,48 +456,96 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
 // workgroup also counts its keys' 8 high bits (and 8 more inside the window
 // hint `win`) into its own histogram slot with agent-scope stores. Returns
 // with those stores issued (the caller waits for them before its ticket).
-template <int NW, int PF>
-__device__ __forceinline__ void score_range(const SelectArgs& a, int bb, int hk, const SeqLen& sl, int M,
-                                            int forced_from, int b0, int b1, int range, int nranges,
-                                            uint32_t win, uint32_t* s_hist, float* s_score) {
-  const int tid = thread_id(), lane = tid & 63;
+// What the scoring workgroups of a group read of its sequence: the length
+// (with the appended row), its blocks M, the first forced local block, and
+// the window hint. The group's tail takes the same values.
+struct RangeInfo {
+  SeqLen sl;
+  int M, forced_from;
+  uint32_t win;
+};
+
+template <int NW, int PF, bool kOpaque>
+__device__ __forceinline__ RangeInfo score_range(const SelectArgs& a, int bb, int hk, int range, int nranges,
+                                                 uint32_t* s_hist, float* s_score) {
+  const int tid = tid_of<kOpaque>(), lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const size_t grp = (size_t)bb * a.c.kv_heads + hk;
   const int r = lane >> 4, c = lane & 15, col = c * 8;
+  const int b0 = range * a.blocks_per_wg;
+
+  // The first tiles are requested before the sequence length, the query and
+  // the new key have arrived, bounded by the range's end at full length
+  // (b1_cap, rows of the summary array in bounds); rows past the true end
+  // are never scored. Rows past an end read the last row before it.
+  const int b1_cap = min(b0 + a.blocks_per_wg, min(a.max_blocks_seq, a.c.max_blocks));
+  const uint16_t* kmin = a.c.kmin + grp * a.c.max_blocks * kHeadDim + col;
+  const uint16_t* kmax = a.c.kmax + grp * a.c.max_blocks * kHeadDim + col;
+  auto load_tile = [&](int t, int end, U4 (&lo4)[4], U4 (&hi4)[4]) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int m = min(b0 + 16 * t + 4 * u + r, end - 1);
+      lo4[u] = ld16_stream(kmin + (size_t)m * kHeadDim);
+      hi4[u] = ld16_stream(kmax + (size_t)m * kHeadDim);
+    }
+  };
+  constexpr int P = PF + 1;
+  U4 lo4[P][4], hi4[P][4];
+#pragma unroll
+  for (int k = 0; k < P; ++k)
+    if (b0 + 16 * (wave + k * NW) < b1_cap) load_tile(wave + k * NW, b1_cap, lo4[k], hi4[k]);
+
+  RangeInfo info;
+  info.sl = seq_len_of(a, bb);
+  const SeqLen sl = info.sl;
+  // Lengths beyond max_seq_len are clamped so every access stays in bounds.
+  const int M = max(0, min(min((sl.L + a.c.block_size - 1) / a.c.block_size, a.max_blocks_seq), a.c.max_blocks));
+  const int forced_from = M - a.n_local;
+  const int b1 = min(b0 + a.blocks_per_wg, M);
+  // Window hint left by the previous call on this workspace (any value is
+  // valid: it only chooses which key bits get a second histogram).
+  const uint32_t win = a.fused ? a.window[grp] : 0u;
+  info.M = M;
+  info.forced_from = forced_from;
+  info.win = win;
+  const bool win_on = (win >> 31) != 0;
+  const uint32_t w9 = win & 0x1FFu;
 
   // Fused append (Alg. 1): the first workgroup of the group writes the new
   // K and V rows; the workgroup owning block pos / b folds the new key into
   // that block's summary (or starts it) before scoring it, and stores it.
   const int m_new = sl.pos >= 0 ? sl.pos / a.c.block_size : -1;
   const bool opening = sl.pos >= 0 && sl.pos % a.c.block_size == 0;
-  U4 knew = U4{0, 0, 0, 0}, vnew = U4{0, 0, 0, 0};
   const bool row_writer = sl.pos >= 0 && range == 0 && tid < 32;
   const int64_t new_row = row_writer ? kv_row(a.c, bb, hk, sl.pos) : -1;
+  U4 knew = U4{0, 0, 0, 0}, vnew = U4{0, 0, 0, 0};
   if (sl.pos >= 0) {
     knew = ld16(a.k_new + grp * kHeadDim + col);
     if (row_writer && tid >= 16) vnew = ld16(a.v_new + grp * kHeadDim + col);
-  }
-
-  // Window hint left by the previous call on this workspace (any value is
-  // valid: it only chooses which key bits get a second histogram).
-  const bool win_on = (win >> 31) != 0;
-  const uint32_t w9 = win & 0x1FFu;
-  if (a.fused) {
-    for (int i = tid; i < 2 * kSlotWords; i += NW * 64) s_hist[i] = 0;
-    lds_sync();
   }
   // The appended block's updated summary row, held by the lanes that score
   // it and stored after the loop (a store inside it would hold up that
   // wave's next tile: the memory counter drains in issue order).
   U4 new_lo = U4{0, 0, 0, 0}, new_hi = U4{0, 0, 0, 0};
   bool owns_row = false;
-  if (b0 < b1) {
+  {
+    U4 qv[kMaxGroup];
+#pragma unroll
+    for (int h = 0; h < kMaxGroup; ++h)
+      qv[h] = h < a.group ? ld16(a.q + ((size_t)bb * a.q_heads + (size_t)hk * a.group + h) * kHeadDim + col)
+                          : U4{0, 0, 0, 0};
+    if (a.fused) {
+      for (int i = tid; i < 2 * kSlotWords; i += NW * 64) s_hist[i] = 0;
+      lds_sync();
+    }
+    const int ntiles = b1 > b0 ? (b1 - b0 + 15) / 16 : 0;
+    int t = wave;
     float qb[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) qb[j] = 0.f;
-    for (int h = 0; h < a.group; ++h) {
-      const U4 qv = ld16(a.q + ((size_t)bb * a.q_heads + (size_t)hk * a.group + h) * kHeadDim + col);
-      const uint32_t w[4] = {qv.x, qv.y, qv.z, qv.w};
+#pragma unroll
+    for (int h = 0; h < kMaxGroup; ++h) {
+      const uint32_t w[4] = {qv[h].x, qv[h].y, qv[h].z, qv[h].w};
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         qb[2 * j] += bf_lo(w[j]);
@@ -511,18 +559,6 @@ __device__ __forceinline__ void score_range(const SelectArgs& a, int bb, int hk,
       qb[j] *= inv_g;
       use_max[j] = qb[j] >= 0.f;
     }
-    const uint16_t* kmin = a.c.kmin + grp * a.c.max_blocks * kHeadDim + col;
-    const uint16_t* kmax = a.c.kmax + grp * a.c.max_blocks * kHeadDim + col;
-    const int ntiles = (b1 - b0 + 15) / 16;
-    // Rows past b1 read the last valid block (in bounds) and are ignored.
-    auto load_tile = [&](int t, U4 (&lo4)[4], U4 (&hi4)[4]) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int m = min(b0 + 16 * t + 4 * u + r, b1 - 1);
-        lo4[u] = ld16_stream(kmin + (size_t)m * kHeadDim);
-        hi4[u] = ld16_stream(kmax + (size_t)m * kHeadDim);
-      }
-    };
     // Tile t of this wave's tiles t = wave, wave + NW, ...: scored from its
     // buffers; PF more tiles are in flight meanwhile (a ring of PF + 1).
     auto score_tile = [&](int t, U4 (&lo4)[4], U4 (&hi4)[4]) {
@@ -557,19 +593,13 @@ __device__ __forceinline__ void score_range(const SelectArgs& a, int bb, int hk,
         }
       }
     };
-    constexpr int P = PF + 1;
-    U4 lo4[P][4], hi4[P][4];
-    int t = wave;
-#pragma unroll
-    for (int k = 0; k < P; ++k)
-      if (t + k * NW < ntiles) load_tile(t + k * NW, lo4[k], hi4[k]);
     while (t < ntiles) {
 #pragma unroll
       for (int k = 0; k < P; ++k) {
         if (t < ntiles) {
           score_tile(t, lo4[k], hi4[k]);
           __builtin_amdgcn_sched_barrier(0);
-          if (t + P * NW < ntiles) load_tile(t + P * NW, lo4[k], hi4[k]);
+          if (t + P * NW < ntiles) load_tile(t + P * NW, b1, lo4[k], hi4[k]);
           __builtin_amdgcn_sched_barrier(0);
           t += NW;
         }
@@ -606,13 +636,14 @@ __device__ __forceinline__ void score_range(const SelectArgs& a, int bb, int hk,
       for (int i = tid; i < nb; i += NW * 64) so[i] = s_score[i];
     }
   }
-  if (!a.fused) return;
+  if (!a.fused) return info;
   // This workgroup's digit counts go to its own slot: no shared counters.
   // Counts fit in 16 bits (at most kMaxBlocksPerWg per workgroup): two per word.
   uint32_t* slot = a.hist + (grp * nranges + range) * kSlotWords;
   for (int i = tid; i < kSlotWords; i += NW * 64)
     __hip_atomic_store(slot + i, s_hist[2 * i] | (s_hist[2 * i + 1] << 16), __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
+  return info;
 }
 
 }  // namespace

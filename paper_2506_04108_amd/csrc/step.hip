@@ -69,22 +69,15 @@ __global__ __launch_bounds__(kStepThreads) void k_step(StepArgs) {
     if (item >= a.score_items) break;
     const int g = item / a.nranges, range = item - g * a.nranges;
     const int bb = g / H, hk = g - bb * H;
-    const SeqLen sl = seq_len_of(sa, bb);
-    const int M = max(0, min(min((sl.L + sa.c.block_size - 1) / sa.c.block_size, sa.max_blocks_seq),
-                             sa.c.max_blocks));
-    const int forced_from = M - sa.n_local;
-    const int b0 = range * sa.blocks_per_wg;
-    const int b1 = min(b0 + sa.blocks_per_wg, M);
-    const uint32_t win = sa.window[g];
-    score_range<kStepWaves, 3>(sa, bb, hk, sl, M, forced_from, b0, b1, range, a.nranges, win, s_hist, s_score);
+    const RangeInfo ri = score_range<kStepWaves, 3, true>(sa, bb, hk, range, a.nranges, s_hist, s_score);
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     if (tid == 0)
       s_misc[3] = __hip_atomic_fetch_add(sa.counters + g, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
     if (s_misc[3] == (uint32_t)a.nranges - 1)
-      select_tail<NJ, kStepThreads>(sa, g, M, forced_from, a.nranges, win, s_hist, s_lds32, s_misc,
-                                    reinterpret_cast<int32_t*>(s_score), bb, sl.L, a.ready);
+      select_tail<NJ, kStepThreads>(sa, g, ri.M, ri.forced_from, a.nranges, ri.win, s_hist, s_lds32, s_misc,
+                                    reinterpret_cast<int32_t*>(s_score), bb, ri.sl.L, a.ready);
     __syncthreads();  // LDS is reused by the next item
   }
 
