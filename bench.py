@@ -106,11 +106,31 @@ def describe(w, layers, dense):
             + f"rectify every {w.rectify_every} steps, {layers} layer caches in rotation")
 
 
-def traffic_from_profile(kernel_src: str, stem: str | None):
+# The sources each timed kernel is compiled from (its own file and the
+# headers holding its device code): a change to any of them retires the
+# kernel's HBM counter figures.
+KERNEL_SOURCES = {
+    "k_decode": ["decode.hip", "decode_impl.h", "resa_device.h", "resa_internal.h"],
+    "k_step": ["step.hip", "select_impl.h", "decode_impl.h", "resa_device.h", "resa_internal.h"],
+}
+
+
+def kernel_sources_sha256(kernel: str) -> str:
+    """sha256 over the kernel's source files, in KERNEL_SOURCES order (each
+    file's name, a NUL, its bytes)."""
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        h.update(f.encode() + b"\0")
+        with open(os.path.join(ROOT, "paper_2506_04108_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def traffic_from_profile(kernel: str, stem: str | None):
     """HBM bytes per launch measured by rocprofv3 PMC counters, read from
     profiles/<stem>_pmc.md (stem = kernel and workload, e.g.
     sparse_decode_long64k) if that profile was taken on the current kernel
-    source; else None (also for variants: dense, paged, overridden sizes)."""
+    sources; else None (also for variants: dense, paged, overridden sizes)."""
     if stem is None:
         return None
     path = os.path.join(ROOT, "profiles", f"{stem}_pmc.md")
@@ -121,8 +141,7 @@ def traffic_from_profile(kernel_src: str, stem: str | None):
     t = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
     if not m or not t:
         return None
-    cur = hashlib.sha256(open(kernel_src, "rb").read()).hexdigest()
-    return float(t.group(1)) if m.group(1) == cur else None
+    return float(t.group(1)) if m.group(1) == kernel_sources_sha256(kernel) else None
 
 
 def cpu_baseline(w, budget_s):
@@ -418,19 +437,18 @@ def measure(args, w, dense: bool) -> dict:
     import workloads as W
     plain = w == W.WORKLOADS.get(w.name) and not (dense or args.paged or args.mode == "three")
 
-    def roof(kernel, src, profile, nbytes, us):
-        kernel_src = os.path.join(ROOT, "paper_2506_04108_amd", "csrc", src)
+    def roof(kernel, profile, nbytes, us):
         gbs = nbytes / (us * 1e-6) / 1e9
         return {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(gbs / HBM_PEAK_GBS, 4),
-                "traffic": traffic_from_profile(kernel_src, f"{profile}_{w.name.replace('_', '')}"
+                "traffic": traffic_from_profile(kernel, f"{profile}_{w.name.replace('_', '')}"
                                                 if plain else None),
                 "kernel": kernel, "avg_launch_us": round(us, 3), "bytes_per_launch": int(nbytes)}
 
     dec_key = "decode_alone" if "decode_alone" in phase_us else "decode"
-    dec_roof = roof("k_decode", "decode.hip", "sparse_decode", avg_bytes, phase_us[dec_key])
+    dec_roof = roof("k_decode", "sparse_decode", avg_bytes, phase_us[dec_key])
     if "step" in phase_us:
-        roofline = roof("k_step", "step.hip", "decode_step", avg_bytes + avg_sum, phase_us["step"])
+        roofline = roof("k_step", "decode_step", avg_bytes + avg_sum, phase_us["step"])
     else:
         roofline = dec_roof
     ms_per_step = gpu_ms / args.steps
