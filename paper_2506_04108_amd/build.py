@@ -20,13 +20,18 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 # Packed fp32 VALU instructions are kept out of the generated code.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Per-source flags. The selection's top-n tail (select.hip, step.hip) takes
+# one-lane atomics whose results are needed only later; the atomic optimizer
+# would broadcast each result right away, making the wave wait for the atomic
+# and for every load issued before it.
+EXTRA = {src: ["-mllvm", "-amdgpu-atomic-optimizer-strategy=None"] for src in ("select.hip", "step.hip")}
 COMMON = ["-O3", "-std=c++20", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
           "-Wno-unused-command-line-argument", "-I", os.path.join(HERE, "..", "include")]
 
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *COMMON, *DEVICE_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *COMMON, *DEVICE_FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     if src.endswith(".cpp"):
         cmd[1:1] = ["-x", "hip"]
     r = subprocess.run(cmd, capture_output=True, text=True)

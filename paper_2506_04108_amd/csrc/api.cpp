@@ -112,7 +112,7 @@ int hip_fail(hipError_t e, const char* what) {
 }
 
 struct SelectLayout {
-  size_t counters, seq_counters, window, hist, scores, total;
+  size_t counters, seq_counters, window, hist, keys, total;
 };
 
 // Workspace of resa_select_blocks / resa_append_select: one ticket per group
@@ -126,8 +126,8 @@ SelectLayout select_layout_words(int32_t batch, int32_t kv_heads, size_t mseq, s
   l.seq_counters = groups * 4;
   l.window = (groups + (size_t)batch) * 4;
   l.hist = round256((2 * groups + (size_t)batch) * 4);
-  l.scores = l.hist + round256(groups * hist_words * 4);
-  l.total = l.scores + groups * ((mseq + 3) & ~size_t(3)) * sizeof(float);
+  l.keys = l.hist + round256(groups * hist_words * 4);
+  l.total = l.keys + groups * ((mseq + 3) & ~size_t(3)) * sizeof(uint32_t);
   return l;
 }
 
@@ -298,7 +298,7 @@ int select_common(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
   a.keep_ppm = keep;
   a.min_blocks = params->min_blocks;
   a.n_local = params->n_local;
-  a.scores = reinterpret_cast<float*>(ws + lay.scores);
+  a.keys = reinterpret_cast<uint32_t*>(ws + lay.keys);
   a.score_stride = (mseq + 3) & ~3;
   a.scores_out = scores_out;
   a.block_idx = block_idx;
@@ -488,7 +488,7 @@ int resa_decode_step(const resa_kv_cache_t* c, const void* k_new, const void* v_
   sa.keep_ppm = keep;
   sa.min_blocks = params->min_blocks;
   sa.n_local = params->n_local;
-  sa.scores = reinterpret_cast<float*>(wsel + lay.s.scores);
+  sa.keys = reinterpret_cast<uint32_t*>(wsel + lay.s.keys);
   sa.score_stride = (mseq + 3) & ~3;
   sa.scores_out = nullptr;
   sa.block_idx = block_idx;

@@ -124,6 +124,18 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
   return x + (row >= 1 ? r0 : 0u) + (row >= 2 ? r1 : 0u) + (row >= 3 ? r2 : 0u);
 }
 
+// Bitwise OR over the 64 lanes of a wave, which must all be active: each row
+// ORs its 16 lanes by DPP (quad swaps, then the half-row and row mirrors),
+// then the four rows' results are combined. The result is wave-uniform.
+__device__ __forceinline__ uint32_t wave_or(uint32_t x) {
+  x |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, kDppXor1, 0xf, 0xf, true);
+  x |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, kDppXor2, 0xf, 0xf, true);
+  x |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, kDppHalfMirror, 0xf, 0xf, true);
+  x |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, kDppMirror, 0xf, 0xf, true);
+  return (uint32_t)(__builtin_amdgcn_readlane((int)x, 0) | __builtin_amdgcn_readlane((int)x, 16) |
+                    __builtin_amdgcn_readlane((int)x, 32) | __builtin_amdgcn_readlane((int)x, 48));
+}
+
 // Transpose-reduce of 16 values across the 16 lanes of a row. Lane c enters
 // with v[s] holding the lane's partial of value n = s ^ c; it leaves with
 // v[0] = the full 16-lane sum of value n = c. Each step pairs lanes that

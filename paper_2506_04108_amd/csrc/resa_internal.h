@@ -50,7 +50,7 @@ struct SelectArgs {
   const int32_t* seq_lens;
   int32_t max_blocks_seq;      // ceil(max_seq_len / b): row stride of the score array
   int32_t keep_ppm, min_blocks, n_local;
-  float* scores;               // workspace [B, Hkv, score_stride], 16-byte aligned rows
+  uint32_t* keys;              // workspace [B, Hkv, score_stride]: order-preserving keys, 16-byte aligned rows
   int32_t score_stride;        // max_blocks_seq rounded up to a multiple of 4
   float* scores_out;           // optional [B, Hkv, max_blocks_seq]
   int32_t* block_idx;          // [B, Hkv, n_cap]

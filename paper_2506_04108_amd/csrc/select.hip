@@ -29,13 +29,12 @@ __device__ void topn_group(const SelectArgs& a, int L) {
     for (int i = tid; i < a.n_cap; i += kTopnThreads) out[i] = i < n ? i : -1;
     return;
   }
-  const float* sc = a.scores + grp * a.score_stride;
-  const int forced_from = M - a.n_local;
+  // Keys as the scoring stored them (the n_local most recent blocks hold the
+  // largest key).
+  const uint32_t* keys = a.keys + grp * a.score_stride;
   const int E = (M + kTopnThreads - 1) / kTopnThreads;
   const int lo = min(tid * E, M), hi = min(lo + E, M);
-  auto key_of = [&](int m) -> uint32_t {
-    return m >= forced_from ? 0xFFFFFFFFu : order_key(sc[m]);
-  };
+  auto key_of = [&](int m) -> uint32_t { return keys[m]; };
 
   uint32_t prefix = 0, pmask = 0, k = (uint32_t)n;
   for (int shift = 24; shift >= 0; shift -= 8) {

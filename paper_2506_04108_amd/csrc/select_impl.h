@@ -164,34 +164,39 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
   // The row is padded to a multiple of 4 scores, so each 16-byte load is
   // wholly inside the row or wholly past it (then it reads 0); ids past M
   // are never used.
-  const __amdgpu_buffer_rsrc_t rs = buf_rsrc(a.scores + grp * a.score_stride, (uint32_t)((M + 3) & ~3) * 4);
-  // The digit search needs only the group's W slots (word d holds two 16-bit
-  // counts): word d gets 4 threads, each summing every 4th slot. The first
-  // round of slot loads is issued before the key loads, so the slot sums can
-  // be used while the keys are still arriving.
-  const uint32_t* slots = a.hist + grp * W * kSlotWords;
-  const int sd = tid & (kSlotWords - 1), spart = tid / kSlotWords;
-  constexpr int kParts = NT / kSlotWords;
-  uint32_t sv[16];
+  const __amdgpu_buffer_rsrc_t rs = buf_rsrc(a.keys + grp * a.score_stride, (uint32_t)((M + 3) & ~3) * 4);
+  // The digit search needs only the group's W slots, summed as packed words:
+  // word d holds the counts of bins 2d and 2d + 1 in its two halves, and a
+  // bin's total over the group is at most M <= kMaxSelectBlocks < 2^16, so
+  // adding whole words never carries from one half into the other. Wave v
+  // sums slots v, v + NT / 64, ... with one 16-byte load per lane and slot
+  // (slots past W read 0 through the buffer's range check, so the loads go
+  // out back to back). They are issued before the key loads, so the sums can
+  // be formed while the keys are still arriving.
+  constexpr int kWaves = NT / 64;
+  constexpr int kSlotRound = (32 + kWaves - 1) / kWaves;  // slots per wave in the first round (W <= 32)
+  const __amdgpu_buffer_rsrc_t rh = buf_rsrc(a.hist + grp * W * kSlotWords, (uint32_t)W * kSlotWords * 4);
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6), lane4 = (tid & 63) * 4;
+  auto slot_load = [&](int w) -> U4 {
+    return __builtin_bit_cast(U4, __builtin_amdgcn_raw_buffer_load_b128(rh, (w * kSlotWords + lane4) * 4, 0, kSc1));
+  };
+  U4 sv[kSlotRound];
 #pragma unroll
-  for (int j = 0; j < 16; ++j) {
-    const int w = spart + j * kParts;
-    sv[j] = w < W ? __hip_atomic_load(slots + w * kSlotWords + sd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
-  }
-  float raw[NJ];
+  for (int j = 0; j < kSlotRound; ++j) sv[j] = slot_load(wv + j * kWaves);
+  // The keys as the scoring stored them (forced blocks hold the largest key).
+  uint32_t key[NJ];
   if constexpr (NJ % 4 == 0) {
 #pragma unroll
     for (int i = 0; i < NJ / 4; ++i) {
-      const f4_t v = __builtin_bit_cast(f4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (id0 + 4 * i) * 4, 0, kSc1));
-      raw[4 * i] = v.x;
-      raw[4 * i + 1] = v.y;
-      raw[4 * i + 2] = v.z;
-      raw[4 * i + 3] = v.w;
+      const U4 v = __builtin_bit_cast(U4, __builtin_amdgcn_raw_buffer_load_b128(rs, (id0 + 4 * i) * 4, 0, kSc1));
+      key[4 * i] = v.x;
+      key[4 * i + 1] = v.y;
+      key[4 * i + 2] = v.z;
+      key[4 * i + 3] = v.w;
     }
   } else {
 #pragma unroll
-    for (int i = 0; i < NJ; ++i)
-      raw[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (id0 + i) * 4, 0, kSc1));
+    for (int i = 0; i < NJ; ++i) key[i] = __builtin_amdgcn_raw_buffer_load_b32(rs, (id0 + i) * 4, 0, kSc1);
   }
 
   // Stores go out after the loads: a wave's memory counter drains in issue
@@ -210,31 +215,30 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
   }
   {
     // Bins 0..255 of s_hist get the top-byte counts, 256..511 the window
-    // counts.
-    if (tid < 2 * kSlotWords) s_hist[tid] = 0;
+    // counts; words 512..767 collect the packed sums first.
+    uint32_t* packed = s_hist + 2 * kSlotWords;
+    if (tid < kSlotWords) packed[tid] = 0;
     if (tid == 0) misc[4] = 0;  // candidate counter of the ranking step (misc[3] holds the ticket)
     lds_sync();
-    uint32_t lo = 0, hi = 0;
+    U4 acc = sv[0];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      lo += sv[j] & 0xFFFFu;
-      hi += sv[j] >> 16;
+    for (int j = 1; j < kSlotRound; ++j) acc = U4{acc.x + sv[j].x, acc.y + sv[j].y, acc.z + sv[j].z, acc.w + sv[j].w};
+    for (int w = wv + kSlotRound * kWaves; w < W; w += kWaves) {
+      const U4 v = slot_load(w);
+      acc = U4{acc.x + v.x, acc.y + v.y, acc.z + v.z, acc.w + v.w};
     }
-    for (int w0 = spart + 16 * kParts; w0 < W; w0 += 16 * kParts) {
-      uint32_t v[16];
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int w = w0 + j * kParts;
-        v[j] = w < W ? __hip_atomic_load(slots + w * kSlotWords + sd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
-      }
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        lo += v[j] & 0xFFFFu;
-        hi += v[j] >> 16;
-      }
+    if (wv < W) {
+      atomicAdd(&packed[lane4], acc.x);
+      atomicAdd(&packed[lane4 + 1], acc.y);
+      atomicAdd(&packed[lane4 + 2], acc.z);
+      atomicAdd(&packed[lane4 + 3], acc.w);
     }
-    atomicAdd(&s_hist[2 * sd], lo);
-    atomicAdd(&s_hist[2 * sd + 1], hi);
+    lds_sync();
+    if (tid < kSlotWords) {
+      const uint32_t p = packed[tid];
+      s_hist[2 * tid] = p & 0xFFFFu;
+      s_hist[2 * tid + 1] = p >> 16;
+    }
     lds_sync();
   }
 
@@ -288,9 +292,6 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
   k = misc[1];
   uint32_t cnt = misc[2];
   // Keys are first needed here; their loads overlapped the digit search.
-  uint32_t key[NJ];
-#pragma unroll
-  for (int i = 0; i < NJ; ++i) key[i] = block_key(id0 + i, forced_from, raw[i]);
   const int nv = min(max(M - id0, 0), NJ);  // this thread's valid keys: j < nv
   const Mask valid = nv >= kMaskBits ? ~Mask(0) : (Mask(1) << nv) - Mask(1);
   // A bucket too large to rank is narrowed by the next 12 bits (rare once
@@ -346,13 +347,15 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
     uint32_t base = 0;
     if ((tid & 63) == 63 && wave_tot != 0) base = atomicAdd(&misc[4], wave_tot);
     uint32_t at = (uint32_t)__builtin_amdgcn_readlane((int)base, 63) + incl - mine;
-    if (inb != 0) {
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) {
-        if ((inb >> j) & Mask(1)) {
-          cv[at] = ((uint64_t)key[j] << 32) | (uint32_t)~(uint32_t)(id0 + j);
-          ++at;
-        }
+    // Only the key slots j that hold a bucket key in some lane of the wave
+    // are visited (a wave-uniform loop, typically a few passes instead of NJ).
+    Mask wbits = (Mask)wave_or((uint32_t)inb);
+    if constexpr (kMaskBits > 32) wbits |= (Mask)wave_or((uint32_t)(inb >> 32)) << 32;
+    for (Mask wm = wbits; wm != 0; wm &= wm - Mask(1)) {
+      const int j = __builtin_ctzll(wm);
+      if ((inb >> j) & Mask(1)) {
+        cv[at] = ((uint64_t)key[j] << 32) | (uint32_t)~(uint32_t)(id0 + j);
+        ++at;
       }
     }
     lds_sync();
@@ -621,14 +624,19 @@ __device__ __forceinline__ RangeInfo score_range(const SelectArgs& a, int bb, in
     else
       st16(const_cast<uint16_t*>(a.c.v) + row, vnew);
   }
-  // Coalesced write-out of this range's scores: to the workspace rows (16-byte
-  // aligned, write-through at agent scope) and, if asked, to scores_out.
+  // Coalesced write-out of this range: the blocks' order-preserving keys to
+  // the workspace rows (16-byte aligned, write-through at agent scope), so
+  // the top-n reads keys and converts nothing, and, if asked, the scores to
+  // scores_out.
   const int nb = max(b1 - b0, 0);
   if (nb > 0) {
-    const __amdgpu_buffer_rsrc_t rs = buf_rsrc(a.scores + grp * a.score_stride + b0, (uint32_t)nb * 4);
+    const __amdgpu_buffer_rsrc_t rs = buf_rsrc(a.keys + grp * a.score_stride + b0, (uint32_t)nb * 4);
     for (int i = 4 * tid; i < nb; i += 4 * NW * 64) {
       const f4_t v = *reinterpret_cast<const f4_t*>(&s_score[i]);
-      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned, v),
+      const int m = b0 + i;
+      const U4 kv = U4{block_key(m, forced_from, v.x), block_key(m + 1, forced_from, v.y),
+                       block_key(m + 2, forced_from, v.z), block_key(m + 3, forced_from, v.w)};
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned, kv),
                                              rs, i * 4, 0, kSc1);
     }
     if (a.scores_out != nullptr) {
