@@ -107,6 +107,43 @@ __device__ void find_digit(const uint32_t* hist, int nbins, uint32_t k, uint32_t
   lds_sync();
 }
 
+// Sum over the 64 lanes of a wave (every lane active); wave-uniform.
+__device__ __forceinline__ uint32_t wave_sum(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(x), 63);
+}
+
+// The digit of the k-th largest key (1 <= k <= total) among 256 counted
+// digits, by one wave: lane i holds the counts of digits 4i .. 4i + 3 in
+// c[0..3] (a larger digit is a larger key). Returns the digit, k's rank
+// inside it and its count, all wave-uniform.
+struct WaveDigit {
+  uint32_t d = 0, k = 0, cnt = 0;
+};
+__device__ __forceinline__ WaveDigit wave_find_digit(const uint32_t (&c)[4], uint32_t k, int lane) {
+  const uint32_t incl = wave_incl_scan(c[0] + c[1] + c[2] + c[3]);
+  const uint32_t all = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+  uint32_t above = all - incl;  // keys in digits above this lane's
+  uint32_t d = 0, r = 0, cn = 0;
+  bool hit = false;
+#pragma unroll
+  for (int j = 3; j >= 0; --j) {
+    if (!hit && above < k && above + c[j] >= k) {
+      hit = true;
+      d = 4 * lane + j;
+      r = k - above;
+      cn = c[j];
+    }
+    above += c[j];
+  }
+  const unsigned long long b = __ballot(hit);
+  const int src = b != 0ull ? __builtin_ctzll(b) : 0;
+  WaveDigit out;
+  out.d = (uint32_t)__builtin_amdgcn_readlane((int)d, src);
+  out.k = (uint32_t)__builtin_amdgcn_readlane((int)r, src);
+  out.cnt = (uint32_t)__builtin_amdgcn_readlane((int)cn, src);
+  return out;
+}
+
 constexpr uint32_t kMaxCand = 256;  // bucket size resolved by ranking (NT / 256 threads per candidate)
 
 // Exact top-n of one group by its last workgroup (M <= NT * NJ). Thread t
@@ -213,10 +250,11 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
     __hip_atomic_store(a.num_sel + grp, n, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(a.counters + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
+  // The group's packed counts (words 512..767 of s_hist): word d holds the
+  // counts of bins 2d and 2d + 1, bins 0..255 being the top byte and
+  // 256..511 the window.
+  uint32_t* packed = s_hist + 2 * kSlotWords;
   {
-    // Bins 0..255 of s_hist get the top-byte counts, 256..511 the window
-    // counts; words 512..767 collect the packed sums first.
-    uint32_t* packed = s_hist + 2 * kSlotWords;
     if (tid < kSlotWords) packed[tid] = 0;
     if (tid == 0) misc[4] = 0;  // candidate counter of the ranking step (misc[3] holds the ticket)
     lds_sync();
@@ -234,63 +272,59 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
       atomicAdd(&packed[lane4 + 3], acc.w);
     }
     lds_sync();
-    if (tid < kSlotWords) {
-      const uint32_t p = packed[tid];
-      s_hist[2 * tid] = p & 0xFFFFu;
-      s_hist[2 * tid + 1] = p >> 16;
-    }
-    lds_sync();
   }
 
 
   // Window hint: keys whose top 9 bits equal W9 were also counted by bits
   // 22..15. When the n-th largest key falls inside that window, those counts
-  // pin 17 bits at once; otherwise the top-byte counts give 8.
-  uint32_t prefix, pmask, k = (uint32_t)n;
-  int known;
-  bool in_win = false;
-  if (win >> 31) {
-    const uint32_t w9 = win & 0x1FFu, w8 = w9 >> 1;
-    // Keys in the window, and keys above it.
-    uint32_t inw = 0, above = 0;
-    if (tid < 64) {
-      uint32_t x = 0, y = 0;
+  // pin 17 bits at once; otherwise the top-byte counts give 8. One wave reads
+  // the packed counts (lane i: digits 4i .. 4i + 3 of both histograms) and
+  // finds the digit; the workgroup waits for it at one barrier.
+  if (wv == 0) {
+    const int lane = tid;
+    const uint32_t p0 = packed[2 * lane], p1 = packed[2 * lane + 1];
+    const uint32_t q0 = packed[kSlotWords / 2 + 2 * lane], q1 = packed[kSlotWords / 2 + 2 * lane + 1];
+    const uint32_t top[4] = {p0 & 0xFFFFu, p0 >> 16, p1 & 0xFFFFu, p1 >> 16};
+    const uint32_t wnd[4] = {q0 & 0xFFFFu, q0 >> 16, q1 & 0xFFFFu, q1 >> 16};
+    const uint32_t kk = (uint32_t)n;
+    WaveDigit dg;
+    uint32_t pre = 0, kn = 8;
+    bool found = false;
+    if (win >> 31) {
+      const uint32_t w9 = win & 0x1FFu, w8 = w9 >> 1;
+      // Keys in the window, and keys above it (the other half of the
+      // window's top byte lies above it when W9 is even).
+      uint32_t y = 0, t8 = 0;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        x += s_hist[256 + 4 * tid + j];
-        const uint32_t t8 = 4 * tid + j;
-        y += t8 > w8 ? s_hist[t8] : 0u;
+        y += (uint32_t)(4 * lane + j) > w8 ? top[j] : 0u;
+        t8 = (uint32_t)j == (w8 & 3u) ? top[j] : t8;
       }
-      x = wave_incl_scan(x);
-      y = wave_incl_scan(y);
-      inw = (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
-      above = (uint32_t)__builtin_amdgcn_readlane((int)y, 63);
-      // The other half of the window's top byte lies above it when W9 is even.
-      if ((w9 & 1u) == 0) above += s_hist[w8] - inw;
-      if (tid == 0) {
-        misc[5] = inw;
-        misc[6] = above;
+      const uint32_t inw = wave_sum(wnd[0] + wnd[1] + wnd[2] + wnd[3]);
+      uint32_t above = wave_sum(y);
+      if ((w9 & 1u) == 0) above += (uint32_t)__builtin_amdgcn_readlane((int)t8, (int)(w8 >> 2)) - inw;
+      if (above < kk && kk <= above + inw) {
+        dg = wave_find_digit(wnd, kk - above, lane);
+        pre = (w9 << 23) | (dg.d << 15);
+        kn = 17;
+        found = true;
       }
     }
-    lds_sync();
-    inw = misc[5];
-    above = misc[6];
-    in_win = above < k && k <= above + inw;
-    if (in_win) {
-      find_digit<NT>(s_hist + 256, 256, k - above, lds32, misc);
-      prefix = (w9 << 23) | (misc[0] << 15);
-      pmask = 0xFFFF8000u;
-      known = 17;
+    if (!found) {
+      dg = wave_find_digit(top, kk, lane);
+      pre = dg.d << 24;
+    }
+    if (lane == 0) {
+      misc[0] = pre;
+      misc[1] = dg.k;
+      misc[2] = dg.cnt;
+      misc[5] = kn;
     }
   }
-  if (!in_win) {
-    find_digit<NT>(s_hist, kBins1, k, lds32, misc);
-    prefix = misc[0] << 24;
-    pmask = 0xFFu << 24;
-    known = 8;
-  }
-  k = misc[1];
-  uint32_t cnt = misc[2];
+  lds_sync();
+  uint32_t prefix = misc[0], k = misc[1], cnt = misc[2];
+  int known = (int)misc[5];
+  uint32_t pmask = known == 17 ? 0xFFFF8000u : 0xFF000000u;
   // Keys are first needed here; their loads overlapped the digit search.
   const int nv = min(max(M - id0, 0), NJ);  // this thread's valid keys: j < nv
   const Mask valid = nv >= kMaskBits ? ~Mask(0) : (Mask(1) << nv) - Mask(1);
