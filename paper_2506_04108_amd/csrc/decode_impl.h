@@ -488,32 +488,23 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
     cb += kIdxBatch;
   } while (cb < valid);
 
-  // Per-head state of this lane's row group: head h lives in lane 16 r + h.
+  // Per-head state of this lane's row group: head h lives in lane 16 r + h
+  // (a DPP row broadcast).
   float m_[G], l_[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    m_[h] = __shfl(st.m, 16 * r + h);
-    l_[h] = __shfl(st.l, 16 * r + h);
-  }
+  [&]<int... H>(std::integer_sequence<int, H...>) {
+    ((m_[H] = dpp<kDppBcast0 + H>(st.m)), ...);
+    ((l_[H] = dpp<kDppBcast0 + H>(st.l)), ...);
+  }(std::make_integer_sequence<int, G>{});
 
   // Merge the four row groups of the wave (lanes c, c+16, c+32, c+48).
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    float mx = fmaxf(m_[h], __shfl_xor(m_[h], 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mx = max_xor32(max_xor16(m_[h]));
     const float w = (m_[h] == ninf) ? 0.f : fast_exp2(m_[h] - mx);
-    float l = l_[h] * w;
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
     m_[h] = mx;
-    l_[h] = l;
+    l_[h] = sum_xor32(sum_xor16(l_[h] * w));
 #pragma unroll
-    for (int d = 0; d < 8; ++d) {
-      float x = acc[h][d] * w;
-      x += __shfl_xor(x, 16);
-      x += __shfl_xor(x, 32);
-      acc[h][d] = x;
-    }
+    for (int d = 0; d < 8; ++d) acc[h][d] = sum_xor32(sum_xor16(acc[h][d] * w));
   }
   if (r == 0) {
 #pragma unroll

@@ -124,6 +124,28 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
   return x + (row >= 1 ? r0 : 0u) + (row >= 2 ? r1 : 0u) + (row >= 3 ? r2 : 0u);
 }
 
+// Lane pairs (l, l ^ 16) and (l, l ^ 32) through gfx950's VALU lane swaps:
+// with both operands x, permlane16_swap leaves x and x[l ^ 16] in the two
+// results (in an order that depends on the row), so a sum or max of the two
+// equals x op x[l ^ 16] exactly; permlane32_swap does the same for l ^ 32.
+// Every lane must be active.
+__device__ __forceinline__ float sum_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float sum_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float max_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 // Bitwise OR over the 64 lanes of a wave, which must all be active: each row
 // ORs its 16 lanes by DPP (quad swaps, then the half-row and row mirrors),
 // then the four rows' results are combined. The result is wave-uniform.
