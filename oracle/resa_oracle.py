@@ -90,7 +90,16 @@ def block_summaries(K: np.ndarray, seq_len: int, block_size: int,
     D = K.shape[1]
     kmin = np.full((M, D), np.nan)
     kmax = np.full((M, D), np.nan)
-    for m in (range(M) if blocks is None else blocks):
+    if blocks is None:
+        # Every block: the full ones as one [blocks, b, D] view, then the
+        # partial last one (the same element-wise min and max).
+        full = L // b
+        if full:
+            rows = K[:full * b].reshape(full, b, D)
+            kmin[:full] = rows.min(axis=1)
+            kmax[:full] = rows.max(axis=1)
+        blocks = range(full, M)
+    for m in blocks:
         rows = K[m * b:min((m + 1) * b, L)]
         kmin[m] = rows.min(axis=0)
         kmax[m] = rows.max(axis=0)
