@@ -112,13 +112,16 @@ int hip_fail(hipError_t e, const char* what) {
 }
 
 struct SelectLayout {
-  size_t counters, seq_counters, window, hist, keys, total;
+  size_t counters, seq_counters, window, hist, keys, above_bits, win_keys, total;
 };
+
+size_t bits_stride(size_t mseq) { return ((mseq + 31) / 32 + 3) & ~size_t(3); }
 
 // Workspace of resa_select_blocks / resa_append_select: one ticket per group
 // and one per sequence (zero between calls), one digit-window hint per group
 // (kept from call to call; any value is valid), per-workgroup key-digit
-// counts, and the scores (rows padded to 4 floats).
+// counts, the blocks' keys (rows padded to 4 words), and for the top-n's
+// in-window path a bit per block and a (key, id) list per group.
 SelectLayout select_layout_words(int32_t batch, int32_t kv_heads, size_t mseq, size_t hist_words) {
   SelectLayout l;
   const size_t groups = (size_t)batch * kv_heads;
@@ -127,7 +130,9 @@ SelectLayout select_layout_words(int32_t batch, int32_t kv_heads, size_t mseq, s
   l.window = (groups + (size_t)batch) * 4;
   l.hist = round256((2 * groups + (size_t)batch) * 4);
   l.keys = l.hist + round256(groups * hist_words * 4);
-  l.total = l.keys + groups * ((mseq + 3) & ~size_t(3)) * sizeof(uint32_t);
+  l.above_bits = l.keys + round256(groups * ((mseq + 3) & ~size_t(3)) * sizeof(uint32_t));
+  l.win_keys = l.above_bits + round256(groups * bits_stride(mseq) * 4);
+  l.total = l.win_keys + groups * ((mseq + 3) & ~size_t(3)) * sizeof(uint64_t);
   return l;
 }
 
@@ -313,6 +318,9 @@ int select_common(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
   a.lens_out = const_cast<int32_t*>(seq_lens);
   a.seq_counters = reinterpret_cast<uint32_t*>(ws + lay.seq_counters);
   a.window = reinterpret_cast<uint32_t*>(ws + lay.window);
+  a.above_bits = reinterpret_cast<uint32_t*>(ws + lay.above_bits);
+  a.bits_stride = (int32_t)bits_stride(mseq);
+  a.win_keys = reinterpret_cast<uint64_t*>(ws + lay.win_keys);
   hipError_t e = resa::launch_select(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, what);
   return ok();
@@ -503,6 +511,9 @@ int resa_decode_step(const resa_kv_cache_t* c, const void* k_new, const void* v_
   sa.lens_out = seq_lens;
   sa.seq_counters = reinterpret_cast<uint32_t*>(wsel + lay.s.seq_counters);
   sa.window = reinterpret_cast<uint32_t*>(wsel + lay.s.window);
+  sa.above_bits = reinterpret_cast<uint32_t*>(wsel + lay.s.above_bits);
+  sa.bits_stride = (int32_t)bits_stride(mseq);
+  sa.win_keys = reinterpret_cast<uint64_t*>(wsel + lay.s.win_keys);
   resa::DecodeArgs& d = a.d;
   d.c = sa.c;
   d.q = sa.q;

@@ -66,6 +66,12 @@ struct SelectArgs {
   int32_t* lens_out;           // seq_lens, written once every group of the sequence is done
   uint32_t* seq_counters;      // [B], zero between calls
   uint32_t* window;            // [B, Hkv] digit-window hint kept across calls (any value is valid)
+  // Written by the scoring when the hint is set (fused top-n), for the
+  // top-n's in-window path: per block, a bit for a key above the window,
+  // and each range's in-window keys grouped by digit, descending.
+  uint32_t* above_bits;        // [B, Hkv, bits_stride]
+  int32_t bits_stride;         // words per group: ceil(max_blocks_seq / 32) rounded to 4
+  uint64_t* win_keys;          // [B, Hkv, score_stride]: range r's list at its first block
 };
 
 struct DecodeArgs {

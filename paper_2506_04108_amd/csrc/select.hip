@@ -150,7 +150,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
   const int tid = threadIdx.x;
   const int hk = blockIdx.y, bb = blockIdx.z;
   const size_t grp = (size_t)bb * a.c.kv_heads + hk;
-  const RangeInfo ri = score_range<kSelWaves, 1, false>(a, bb, hk, blockIdx.x, gridDim.x, s_hist, s_score);
+  const RangeInfo ri = score_range<kSelWaves, 1, false, window_lists(NJ, kSelThreads)>(a, bb, hk, blockIdx.x, gridDim.x, s_hist, s_score);
   if (!a.fused) return;
   __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
@@ -198,12 +198,13 @@ int32_t select_fused_max_blocks() { return kMaxSelectBlocks; }
 
 int32_t select_blocks_per_wg(int32_t batch, int32_t kv_heads, int32_t max_blocks_seq) {
   // About one 16-wave workgroup per CU (256 CUs) in all: a group's blocks are
-  // cut into equal ranges, in whole 16-block tiles, at least one tile per
+  // cut into equal ranges of whole 32-block words (so a word of the
+  // above-window bits belongs to one range), at least one 16-block tile per
   // wave (256 blocks) and at most the LDS staging area.
   const int64_t groups = (int64_t)batch * kv_heads;
   const int64_t per_group = (256 + groups - 1) / groups;
   int64_t bpw = ((int64_t)max_blocks_seq + per_group - 1) / per_group;
-  bpw = (bpw + 15) / 16 * 16;
+  bpw = (bpw + 31) / 32 * 32;
   if (bpw < 256) bpw = 256;
   if (bpw > kMaxBlocksPerWg) bpw = kMaxBlocksPerWg;
   return (int32_t)bpw;

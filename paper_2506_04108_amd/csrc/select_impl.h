@@ -17,6 +17,12 @@ constexpr int kBins2 = 4096;                      // next digits: bits 23..12, t
 constexpr int kMaxSelectBlocks = 32768;          // fused top-n: M <= 32768 (keys in registers)
 constexpr int kMaxBlocksPerWg = 8192;             // scores staged in LDS per workgroup (32 KiB)
 
+// The top-n's in-window path (and the scoring's above-window bits and
+// in-window lists it reads) is used when its workgroup holds at least 16384
+// keys (NJ keys per thread, NT threads): below that, reading all keys costs
+// less than the lists' extra round trip and their write-through stores.
+__host__ __device__ constexpr bool window_lists(int nj, int nt) { return nj * nt >= 16384; }
+
 __device__ __forceinline__ uint32_t block_key(int m, int forced_from, float s) {
   return m >= forced_from ? 0xFFFFFFFFu : order_key(s);
 }
@@ -144,6 +150,25 @@ __device__ __forceinline__ WaveDigit wave_find_digit(const uint32_t (&c)[4], uin
   return out;
 }
 
+// Keys [id0, id0 + NJ) of a group's key row (agent-scope loads; past the
+// row they read 0).
+template <int NJ>
+__device__ __forceinline__ void load_keys(uint32_t (&key)[NJ], __amdgpu_buffer_rsrc_t rs, int id0) {
+  if constexpr (NJ % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < NJ / 4; ++i) {
+      const U4 v = __builtin_bit_cast(U4, __builtin_amdgcn_raw_buffer_load_b128(rs, (id0 + 4 * i) * 4, 0, kSc1));
+      key[4 * i] = v.x;
+      key[4 * i + 1] = v.y;
+      key[4 * i + 2] = v.z;
+      key[4 * i + 3] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < NJ; ++i) key[i] = __builtin_amdgcn_raw_buffer_load_b32(rs, (id0 + i) * 4, 0, kSc1);
+  }
+}
+
 constexpr uint32_t kMaxCand = 256;  // bucket size resolved by ranking (NT / 256 threads per candidate)
 
 // Exact top-n of one group by its last workgroup (M <= NT * NJ). Thread t
@@ -221,20 +246,14 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
 #pragma unroll
   for (int j = 0; j < kSlotRound; ++j) sv[j] = slot_load(wv + j * kWaves);
   // The keys as the scoring stored them (forced blocks hold the largest key).
+  // With the window hint set and at most 32 ranges (their slots held in sv),
+  // the in-window path below may finish without them: their loads are then
+  // put off until it cannot. (Only where the scoring wrote the lists, and
+  // not with more than 32 keys per thread, whose registers would not last
+  // across that path.)
+  const bool lazy = window_lists(NJ, NT) && NJ <= 32 && (win >> 31) != 0 && W <= kSlotRound * kWaves;
   uint32_t key[NJ];
-  if constexpr (NJ % 4 == 0) {
-#pragma unroll
-    for (int i = 0; i < NJ / 4; ++i) {
-      const U4 v = __builtin_bit_cast(U4, __builtin_amdgcn_raw_buffer_load_b128(rs, (id0 + 4 * i) * 4, 0, kSc1));
-      key[4 * i] = v.x;
-      key[4 * i + 1] = v.y;
-      key[4 * i + 2] = v.z;
-      key[4 * i + 3] = v.w;
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < NJ; ++i) key[i] = __builtin_amdgcn_raw_buffer_load_b32(rs, (id0 + i) * 4, 0, kSc1);
-  }
+  if (!lazy) load_keys<NJ>(key, rs, id0);
 
   // Stores go out after the loads: a wave's memory counter drains in issue
   // order, so a store issued before a load would make the load's consumer
@@ -325,112 +344,219 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
   uint32_t prefix = misc[0], k = misc[1], cnt = misc[2];
   int known = (int)misc[5];
   uint32_t pmask = known == 17 ? 0xFFFF8000u : 0xFF000000u;
-  // Keys are first needed here; their loads overlapped the digit search.
   const int nv = min(max(M - id0, 0), NJ);  // this thread's valid keys: j < nv
   const Mask valid = nv >= kMaskBits ? ~Mask(0) : (Mask(1) << nv) - Mask(1);
-  // A bucket too large to rank is narrowed by the next 12 bits (rare once
-  // the window hint follows the threshold).
-  while (known < 32 && cnt != k && cnt > kMaxCand) {
-    const int width = min(12, 32 - known), shift = 32 - known - width;
-    const uint32_t dmask = (1u << width) - 1u;
-    for (int i = tid; i < (1 << width); i += NT) s_hist[i] = 0;
-    lds_sync();
-#pragma unroll
-    for (int j = 0; j < NJ; ++j)
-      if (j < nv && (key[j] & pmask) == prefix) atomicAdd(&s_hist[(key[j] >> shift) & dmask], 1u);
-    lds_sync();
-    find_digit<NT>(s_hist, 1 << width, k, lds32, misc);
-    prefix |= misc[0] << shift;
-    pmask |= dmask << shift;
-    known += width;
-    k = misc[1];
-    cnt = misc[2];
-  }
-
-  // One pass over the keys: bit j of `take` marks key j above the bucket of
-  // the n-th largest key, bit j of `inb` key j inside it.
   Mask take = 0, inb = 0;
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    const uint32_t km = key[j] & pmask;
-    take |= km > prefix ? Mask(1) << j : Mask(0);
-    inb |= km == prefix ? Mask(1) << j : Mask(0);
-  }
-  take &= valid;
-  inb &= valid;
   uint32_t thr = prefix;  // the threshold key (its known bits), for the next call's window
-  // 0: the whole bucket is kept; 1: its candidates were ranked; 2: every key
-  // of the bucket equals the threshold and the k lowest ids are kept.
-  const int mode = cnt == k ? 0 : (cnt <= kMaxCand ? 1 : 2);
-  if (mode == 0) {
-    take |= inb;
-  } else if (mode == 1) {
-    // Rank the bucket's keys among themselves in (key descending, id
-    // ascending) order: a candidate is kept iff fewer than k candidates come
-    // before it, which keeps every key above the threshold T and the lowest
-    // ids among the keys equal to T. A candidate is stored as
-    // (key << 32 | ~id), so that order is plain 64-bit descending order; the
-    // kept ones set their id's bit in an LDS bitmap (ids < 32768: 1024 words).
-    constexpr int TPC = NT / (int)kMaxCand;  // threads per candidate: 4 or 2
-    uint64_t* cv = reinterpret_cast<uint64_t*>(s_hist);   // words [0, 2 kMaxCand)
-    uint32_t* bits = s_hist + 2048;                       // words [2048, 3072)
-    for (int i = tid; i < 1024; i += NT) bits[i] = 0;
-    const uint32_t mine = __builtin_popcountll(inb);
-    const uint32_t incl = wave_incl_scan(mine);
-    const uint32_t wave_tot = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
-    uint32_t base = 0;
-    if ((tid & 63) == 63 && wave_tot != 0) base = atomicAdd(&misc[4], wave_tot);
-    uint32_t at = (uint32_t)__builtin_amdgcn_readlane((int)base, 63) + incl - mine;
-    // Only the key slots j that hold a bucket key in some lane of the wave
-    // are visited (a wave-uniform loop, typically a few passes instead of NJ).
-    Mask wbits = (Mask)wave_or((uint32_t)inb);
-    if constexpr (kMaskBits > 32) wbits |= (Mask)wave_or((uint32_t)(inb >> 32)) << 32;
-    for (Mask wm = wbits; wm != 0; wm &= wm - Mask(1)) {
-      const int j = __builtin_ctzll(wm);
-      if ((inb >> j) & Mask(1)) {
-        cv[at] = ((uint64_t)key[j] << 32) | (uint32_t)~(uint32_t)(id0 + j);
-        ++at;
-      }
-    }
-    lds_sync();
-    {
-      // TPC threads per candidate (adjacent lanes of one wave), each
-      // counting over its share of the bucket; the shares are added with
-      // DPP quad swaps.
-      const uint32_t cand = (uint32_t)tid / TPC, part = (uint32_t)tid % TPC;
-      uint32_t before = 0;
-      uint64_t vt = 0;
-      if (cand < cnt) {
-        vt = cv[cand];
-        const uint32_t qlen = (cnt + TPC - 1) / TPC;
-        const uint32_t j1 = min((part + 1) * qlen, cnt);
-        uint32_t j = part * qlen;
-        for (; j + 8 <= j1; j += 8) {
-          uint64_t v[8];
+  // Bucket ranking: candidates are stored as (key << 32 | ~id), so (key
+  // descending, id ascending) is plain 64-bit descending order; a candidate
+  // is kept iff fewer than k candidates come before it, which keeps every key
+  // above the threshold T and the lowest ids among the keys equal to T. The
+  // kept ones set their id's bit in an LDS bitmap (ids < 32768: 1024 words);
+  // T goes to misc[0]. TPC threads per candidate (adjacent lanes of one wave)
+  // each count over a share of the bucket; the shares are added with DPP
+  // quad swaps.
+  constexpr int TPC = NT / (int)kMaxCand;  // threads per candidate: 4 or 2
+  uint64_t* cv = reinterpret_cast<uint64_t*>(s_hist);  // words [0, 2 kMaxCand)
+  uint32_t* bits = s_hist + 2048;                      // words [2048, 3072)
+  auto rank_bucket = [&]() {
+    const uint32_t cand = (uint32_t)tid / TPC, part = (uint32_t)tid % TPC;
+    uint32_t before = 0;
+    uint64_t vt = 0;
+    if (cand < cnt) {
+      vt = cv[cand];
+      const uint32_t qlen = (cnt + TPC - 1) / TPC;
+      const uint32_t j1 = min((part + 1) * qlen, cnt);
+      uint32_t j = part * qlen;
+      for (; j + 8 <= j1; j += 8) {
+        uint64_t v[8];
 #pragma unroll
-          for (int u = 0; u < 8; ++u) v[u] = cv[j + u];
+        for (int u = 0; u < 8; ++u) v[u] = cv[j + u];
 #pragma unroll
-          for (int u = 0; u < 8; ++u) before += v[u] > vt;
-        }
-        for (; j < j1; ++j) before += cv[j] > vt;
+        for (int u = 0; u < 8; ++u) before += v[u] > vt;
       }
-      before += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)before, kDppXor1, 0xf, 0xf, true);
-      if constexpr (TPC == 4)
-        before += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)before, kDppXor2, 0xf, 0xf, true);
-      if (cand < cnt && part == 0 && before < k) {
-        const uint32_t id = ~(uint32_t)vt;
-        atomicOr(&bits[id >> 5], 1u << (id & 31u));
-        if (before == k - 1) misc[0] = (uint32_t)(vt >> 32);  // T
-      }
+      for (; j < j1; ++j) before += cv[j] > vt;
     }
-    lds_sync();
-    thr = misc[0];
-    // This thread's ids [id0, id0 + NJ) span at most two bitmap words (for
-    // every instantiated NJ, (id0 mod 32) + NJ <= 64).
+    before += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)before, kDppXor1, 0xf, 0xf, true);
+    if constexpr (TPC == 4)
+      before += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)before, kDppXor2, 0xf, 0xf, true);
+    if (cand < cnt && part == 0 && before < k) {
+      const uint32_t id = ~(uint32_t)vt;
+      atomicOr(&bits[id >> 5], 1u << (id & 31u));
+      if (before == k - 1) misc[0] = (uint32_t)(vt >> 32);  // T
+    }
+  };
+  // This thread's ids [id0, id0 + NJ) from the bitmap: they span at most two
+  // words (for every instantiated NJ, (id0 mod 32) + NJ <= 64).
+  auto bits_of_thread = [&]() -> Mask {
     const uint32_t w0 = (uint32_t)id0 >> 5, sh = (uint32_t)id0 & 31u;
     uint64_t pair = bits[w0];
     if (sh + NJ > 32) pair |= (uint64_t)bits[w0 + 1] << 32;
-    take |= (Mask)(pair >> sh) & valid;
+    return (Mask)(pair >> sh) & valid;
+  };
+  // 0: the whole bucket is kept; 1: its candidates were ranked; 2: every key
+  // of the bucket equals the threshold and the k lowest ids are kept.
+  int mode = 0;
+  bool done = false;
+  if (lazy && known == 17 && cnt <= kMaxCand) {
+    // In-window path: the n-th largest key lies in the window, so every key
+    // above the window is kept (the scoring's above-window bits), and of the
+    // in-window keys (each range's list, digits descending) those with a digit
+    // above d are kept and those with digit d form the bucket. Per range r:
+    // A_r keys with a digit above d and B_r with digit d, from the window
+    // counts of its slot (words 128..255, held by lanes 32..63 of the wave
+    // that loaded it: word 4 l + q holds digits 8 (l - 32) + 2 q and + 1).
+    const uint32_t d = (prefix >> 15) & 0xFFu;
+    uint32_t* ab = s_hist + 3 * kSlotWords;  // words [768, 1024): A, B, prefixes, total
+    const int ln = tid & 63;
+#pragma unroll
+    for (int j = 0; j < kSlotRound; ++j) {
+      const uint32_t wd[4] = {sv[j].x, sv[j].y, sv[j].z, sv[j].w};
+      uint32_t gt = 0, eq = 0;
+      if (ln >= 32) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const uint32_t dg = 8u * (uint32_t)(ln - 32) + 2u * q + h, c = (wd[q] >> (16 * h)) & 0xFFFFu;
+            gt += dg > d ? c : 0u;
+            eq += dg == d ? c : 0u;
+          }
+      }
+      const uint32_t A = wave_sum(gt), B = wave_sum(eq);
+      const int w = wv + j * kWaves;
+      if (ln == 0 && w < W) {
+        ab[w] = A;
+        ab[32 + w] = B;
+      }
+    }
+    lds_sync();
+    if (wv == 0) {
+      const uint32_t A = ln < W ? ab[ln] : 0u, B = ln < W ? ab[32 + ln] : 0u, C = A + B;
+      const uint32_t cpre = wave_incl_scan(C) - C, bpre = wave_incl_scan(B) - B, ctot = wave_sum(C);
+      if (ln < W) {
+        ab[64 + ln] = cpre;
+        ab[96 + ln] = bpre;
+      }
+      if (ln == 0) ab[128] = ctot;
+    }
+    lds_sync();
+    const uint32_t E = ab[128];  // list entries needed: at most one per thread
+    if (E <= (uint32_t)NT) {
+      done = true;
+      // Requests: the group's above-window bits and this thread's entry
+      // (entry e of range r, r the last range with prefix <= e).
+      constexpr int kBitWords = 1024 / NT;
+      const int words = (M + 31) / 32;
+      const uint32_t* gb = a.above_bits + grp * a.bits_stride;
+      uint32_t bw[kBitWords];
+#pragma unroll
+      for (int u = 0; u < kBitWords; ++u) {
+        const int wi = tid + u * NT;
+        bw[u] = wi < words ? __hip_atomic_load(gb + wi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+      }
+      int er = -1;
+      uint32_t ej = 0;
+      uint64_t ent = 0;
+      if ((uint32_t)tid < E) {
+        int r = 0;
+#pragma unroll
+        for (int st = 16; st > 0; st >>= 1)
+          if (r + st < W && ab[64 + r + st] <= (uint32_t)tid) r += st;
+        er = r;
+        ej = (uint32_t)tid - ab[64 + r];
+        ent = __hip_atomic_load(a.win_keys + grp * a.score_stride + (size_t)r * a.blocks_per_wg + ej,
+                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+#pragma unroll
+      for (int u = 0; u < kBitWords; ++u) bits[tid + u * NT] = bw[u];
+      lds_sync();
+      if (er >= 0) {
+        const uint32_t id = (uint32_t)ent;
+        if (ej < ab[er] || cnt == k)  // above the bucket, or the whole bucket is kept
+          atomicOr(&bits[id >> 5], 1u << (id & 31u));
+        else
+          cv[ab[96 + er] + (ej - ab[er])] = (ent & 0xFFFFFFFF00000000ull) | (uint32_t)~id;
+      }
+      lds_sync();
+      if (cnt != k) {
+        rank_bucket();
+        lds_sync();
+        thr = misc[0];
+      }
+      take = bits_of_thread();
+    }
+  }
+  if (!done) {
+    if (lazy) load_keys<NJ>(key, rs, id0);
+    // A bucket too large to rank is narrowed by the next 12 bits (rare once
+    // the window hint follows the threshold).
+    while (known < 32 && cnt != k && cnt > kMaxCand) {
+      const int width = min(12, 32 - known), shift = 32 - known - width;
+      const uint32_t dmask = (1u << width) - 1u;
+      for (int i = tid; i < (1 << width); i += NT) s_hist[i] = 0;
+      lds_sync();
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        if (j < nv && (key[j] & pmask) == prefix) atomicAdd(&s_hist[(key[j] >> shift) & dmask], 1u);
+      lds_sync();
+      find_digit<NT>(s_hist, 1 << width, k, lds32, misc);
+      prefix |= misc[0] << shift;
+      pmask |= dmask << shift;
+      known += width;
+      k = misc[1];
+      cnt = misc[2];
+    }
+
+    // One pass over the keys: bit j of `take` marks key j above the bucket of
+    // the n-th largest key, bit j of `inb` key j inside it.
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const uint32_t km = key[j] & pmask;
+      take |= km > prefix ? Mask(1) << j : Mask(0);
+      inb |= km == prefix ? Mask(1) << j : Mask(0);
+    }
+    take &= valid;
+    inb &= valid;
+    thr = prefix;
+    mode = cnt == k ? 0 : (cnt <= kMaxCand ? 1 : 2);
+    if (mode == 0) {
+      take |= inb;
+    } else if (mode == 1) {
+      for (int i = tid; i < 1024; i += NT) bits[i] = 0;
+      const uint32_t mine = __builtin_popcountll(inb);
+      const uint32_t incl = wave_incl_scan(mine);
+      const uint32_t wave_tot = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+      uint32_t base = 0;
+      if ((tid & 63) == 63 && wave_tot != 0) base = atomicAdd(&misc[4], wave_tot);
+      uint32_t at = (uint32_t)__builtin_amdgcn_readlane((int)base, 63) + incl - mine;
+      if constexpr (NJ <= 32) {
+        // Only the key slots j that hold a bucket key in some lane of the
+        // wave are visited (a wave-uniform loop, typically a few passes
+        // instead of NJ; j indexes the key registers).
+        for (Mask wm = (Mask)wave_or((uint32_t)inb); wm != 0; wm &= wm - Mask(1)) {
+          const int j = __builtin_ctzll(wm);
+          if ((inb >> j) & Mask(1)) {
+            cv[at] = ((uint64_t)key[j] << 32) | (uint32_t)~(uint32_t)(id0 + j);
+            ++at;
+          }
+        }
+      } else {
+        // 64 keys per thread: constant indices keep the keys in registers.
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          if ((inb >> j) & Mask(1)) {
+            cv[at] = ((uint64_t)key[j] << 32) | (uint32_t)~(uint32_t)(id0 + j);
+            ++at;
+          }
+        }
+      }
+      lds_sync();
+      rank_bucket();
+      lds_sync();
+      thr = misc[0];
+      take |= bits_of_thread();
+    }
   }
   // The next call's window: the top 9 bits of this threshold. The stores
   // here go out before the compaction so their latency overlaps it.
@@ -502,7 +628,7 @@ struct RangeInfo {
   uint32_t win;
 };
 
-template <int NW, int PF, bool kOpaque>
+template <int NW, int PF, bool kOpaque, bool kLists>
 __device__ __forceinline__ RangeInfo score_range(const SelectArgs& a, int bb, int hk, int range, int nranges,
                                                  uint32_t* s_hist, float* s_score) {
   const int tid = tid_of<kOpaque>(), lane = tid & 63;
@@ -679,6 +805,51 @@ __device__ __forceinline__ RangeInfo score_range(const SelectArgs& a, int bb, in
     }
   }
   if (!a.fused) return info;
+  if (kLists && win_on && nb > 0) {
+    // For the top-n's in-window path: a bit per block whose key lies above
+    // the window (one ballot per 64 blocks; the range starts on a word), and
+    // the range's in-window keys as (key, id) pairs grouped by digit (bits
+    // 22..15), larger digits first, at the range's first block in the list
+    // row. Wave 0 turns the window counts into each digit's first position.
+    uint32_t* woff = s_hist + 2 * kSlotWords;
+    if (wave == 0) {
+      uint32_t cw[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) cw[j] = s_hist[kSlotWords + 255 - 4 * lane - j];
+      const uint32_t tot = cw[0] + cw[1] + cw[2] + cw[3];
+      uint32_t run = wave_incl_scan(tot) - tot;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        woff[255 - 4 * lane - j] = run;
+        run += cw[j];
+      }
+    }
+    lds_sync();
+    uint64_t* lst = a.win_keys + grp * a.score_stride + b0;
+    uint32_t* bits = a.above_bits + grp * a.bits_stride + b0 / 32;
+    const int words = (nb + 31) / 32;
+    for (int i0 = wave * 64; i0 < nb; i0 += NW * 64) {
+      const int i = i0 + lane;
+      bool above = false;
+      if (i < nb) {
+        const uint32_t key = block_key(b0 + i, forced_from, s_score[i]);
+        above = (key >> 23) > w9;
+        if ((key >> 23) == w9) {
+          const uint32_t at = atomicAdd(&woff[(key >> 15) & 0xFFu], 1u);
+          __hip_atomic_store(lst + at, ((uint64_t)key << 32) | (uint32_t)(b0 + i), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+      const unsigned long long bal = __ballot(above);
+      if (lane == 0) {
+        if (i0 / 32 < words)
+          __hip_atomic_store(bits + i0 / 32, (uint32_t)bal, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (i0 / 32 + 1 < words)
+          __hip_atomic_store(bits + i0 / 32 + 1, (uint32_t)(bal >> 32), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  }
   // This workgroup's digit counts go to its own slot: no shared counters.
   // Counts fit in 16 bits (at most kMaxBlocksPerWg per workgroup): two per word.
   uint32_t* slot = a.hist + (grp * nranges + range) * kSlotWords;

@@ -69,7 +69,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step(StepArgs) {
     if (item >= a.score_items) break;
     const int g = item / a.nranges, range = item - g * a.nranges;
     const int bb = g / H, hk = g - bb * H;
-    const RangeInfo ri = score_range<kStepWaves, 3, true>(sa, bb, hk, range, a.nranges, s_hist, s_score);
+    const RangeInfo ri = score_range<kStepWaves, 3, true, window_lists(NJ, kStepThreads)>(sa, bb, hk, range, a.nranges, s_hist, s_score);
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     if (tid == 0)
@@ -154,12 +154,12 @@ int32_t step_max_blocks() { return kStepThreads * 64; }
 int32_t step_blocks_per_range(int32_t batch, int32_t kv_heads, int32_t max_blocks_seq) {
   // About two score ranges per CU in all (256 CUs), so that groups finish
   // scoring in two rounds and the first round's top-n overlaps the second;
-  // whole 16-block tiles, at least two tiles per wave, at most the LDS
-  // staging area.
+  // whole 32-block words (one word of the above-window bits per range), at
+  // least two 16-block tiles per wave, at most the LDS staging area.
   const int64_t groups = (int64_t)batch * kv_heads;
   const int64_t per_group = (512 + groups - 1) / groups;
   int64_t bpr = ((int64_t)max_blocks_seq + per_group - 1) / per_group;
-  bpr = (bpr + 15) / 16 * 16;
+  bpr = (bpr + 31) / 32 * 32;
   if (bpr < 256) bpr = 256;
   if (bpr > kMaxBlocksPerWg) bpr = kMaxBlocksPerWg;
   return (int32_t)bpr;

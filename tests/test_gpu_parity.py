@@ -288,6 +288,54 @@ def test_select_window_hint_ragged(b):
                 check_selection(gi[bi, hi, :gn[bi, hi]], ri[bi, hi], rs[bi, hi], rn[bi, hi], 1)
 
 
+def _window_lists_calls(w, cap, lens, scales, qstep):
+    """Calls on one workspace against calls on a fresh one and the oracle."""
+    B, H = w.batch, w.num_kv_heads
+    K, _ = W.kv_cache(w, capacity=cap)
+    cache = make_cache(K, K, 16)
+    lt = i32(lens)
+    R.block_summarize(cache, lt)
+    ws = R.Workspace(dev())
+    # The oracle's summaries (Eq. 3) of every group, once: the calls append
+    # nothing.
+    summ = {(bi, hi): O.block_summaries(O.bf16_to_f64(K[bi, hi]), lens[bi], 16)
+            for bi in range(B) for hi in range(H)}
+    q0 = W.bf16_bits_to_f32(W.decode_query(w, qstep))
+    for scale in scales:
+        q = W.f32_to_bf16_bits(q0 * scale)
+        idx, ns = R.select_blocks(cache, up(q), lt, max(lens), 0.9, 4, 1, workspace=ws)
+        idx2, ns2 = R.select_blocks(cache, up(q), lt, max(lens), 0.9, 4, 1)
+        torch.cuda.synchronize()
+        assert torch.equal(idx, idx2) and torch.equal(ns, ns2), scale
+        qg = O.split_heads(O.bf16_to_f64(q), H)
+        gi, gn = idx.cpu().numpy(), ns.cpu().numpy()
+        for bi in range(B):
+            for hi in range(H):
+                kmin, kmax = summ[bi, hi]
+                rs = O.block_scores(O.pooled_query(qg[bi, hi]), kmin, kmax)
+                rn = O.num_selected(kmin.shape[0], 0.9, 4, 1)
+                assert gn[bi, hi] == rn
+                check_selection(gi[bi, hi, :gn[bi, hi]], O.select_blocks(rs, rn, 1), rs, rn, 1)
+
+
+def test_select_window_lists_hint():
+    """Groups of 12500 blocks (16 keys per top-n thread, 8 groups of 31 score
+    ranges): a call whose threshold falls in the window hint takes the
+    in-window path, which reads the scoring's above-window bits and in-window
+    lists instead of every key. Queries scaled by powers of two (and negated)
+    make the hint hit, miss above and miss below; every call must equal a
+    call on a fresh workspace and the oracle."""
+    w, cap = small(g=4, b=16, L=200000, cap=200064, B=1, H=8, tag="wlist")
+    _window_lists_calls(w, cap, [200000], [1.0, 1.0, 4.0, 0.25, -1.0, 1.0, 64.0, 1.0], 0)
+
+
+def test_select_window_lists_ragged():
+    """The in-window path over ragged lengths: groups of 12500, 8126 and 44
+    blocks (28, 19 and 1 score ranges) with a moving score distribution."""
+    w, cap = small(g=4, b=16, L=200000, cap=200064, B=3, H=3, tag="wlong")
+    _window_lists_calls(w, cap, [200000, 130001, 700], [1.0, 1.0, 1.0, 1.25, 1.25, 0.8, 2.0, 1.0], 2)
+
+
 def test_select_planted_blocks_win():
     w = W.TINY_4K.with_(plant_norm=math.sqrt(128), seed_tag="strong")
     q = W.decode_query(w)
