@@ -21,7 +21,13 @@ constexpr int kMaxBlocksPerWg = 8192;             // scores staged in LDS per wo
 // in-window lists it reads) is used when its workgroup holds at least 16384
 // keys (NJ keys per thread, NT threads): below that, reading all keys costs
 // less than the lists' extra round trip and their write-through stores.
+// The lists are also limited to score ranges of at most kListRange blocks:
+// a range's list stores grow with its length (one scattered write-through
+// store per in-window key before its ticket) while the tail's saving does
+// not (256K, batch 8: 4 ranges of 4128 blocks per group, selection 104 ->
+// 108 us with them; batch 1: 31 ranges of 544 blocks, 27.4 -> 25.1 us).
 __host__ __device__ constexpr bool window_lists(int nj, int nt) { return nj * nt >= 16384; }
+constexpr int kListRange = 1024;
 
 __device__ __forceinline__ uint32_t block_key(int m, int forced_from, float s) {
   return m >= forced_from ? 0xFFFFFFFFu : order_key(s);
@@ -251,7 +257,8 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
   // put off until it cannot. (Only where the scoring wrote the lists, and
   // not with more than 32 keys per thread, whose registers would not last
   // across that path.)
-  const bool lazy = window_lists(NJ, NT) && NJ <= 32 && (win >> 31) != 0 && W <= kSlotRound * kWaves;
+  const bool lazy = window_lists(NJ, NT) && NJ <= 32 && a.blocks_per_wg <= kListRange && (win >> 31) != 0 &&
+                    W <= kSlotRound * kWaves;
   uint32_t key[NJ];
   if (!lazy) load_keys<NJ>(key, rs, id0);
 
@@ -805,7 +812,7 @@ __device__ __forceinline__ RangeInfo score_range(const SelectArgs& a, int bb, in
     }
   }
   if (!a.fused) return info;
-  if (kLists && win_on && nb > 0) {
+  if (kLists && win_on && nb > 0 && a.blocks_per_wg <= kListRange) {
     // For the top-n's in-window path: a bit per block whose key lies above
     // the window (one ballot per 64 blocks; the range starts on a word), and
     // the range's in-window keys as (key, id) pairs grouped by digit (bits
