@@ -162,8 +162,8 @@ size_t resa_select_workspace_size(int32_t batch, int32_t num_kv_heads,
  * >= resa_num_selected(ceil(max_seq_len / block_size), ...) (else
  * RESA_ERR_CAPACITY). scores_out (optional, may be NULL): fp32 [batch,
  * num_kv_heads, ceil(max_seq_len / block_size)], receives the Eq. 4 scores
- * before local forcing (entries past M_b are not written); the scores are
- * also kept in the workspace either way.
+ * before local forcing (entries past M_b are not written); the workspace
+ * keeps the blocks' order-preserving keys either way.
  * One kernel scores the blocks and, in the last workgroup of each group to
  * finish, selects them (groups of more than 32768 blocks use a second
  * kernel). The workspace starts with one ticket per group: zero-fill it
