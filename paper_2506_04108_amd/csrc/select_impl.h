@@ -179,9 +179,13 @@ constexpr uint32_t kMaxCand = 256;  // bucket size resolved by ranking (NT / 256
 
 // Exact top-n of one group by its last workgroup (M <= NT * NJ). Thread t
 // holds the keys of ids [t NJ, t NJ + NJ) in registers, so id order is
-// thread order. The key loads are issued first; while they are in flight the
-// workgroup sums the group's slots into the counts of the keys' 8 high bits
-// (or of 8 more bits inside the window hint). A bucket too large to rank is
+// thread order. The slot loads are issued first, then the key loads; while
+// the keys are in flight the workgroup sums the group's slots into the counts
+// of the keys' 8 high bits (or of 8 more bits inside the window hint), and one
+// wave finds the threshold digit. When that digit lies in the window, the
+// in-window path (see below) may finish from the scoring's above-window bits
+// and in-window lists, and the key loads are then put off until it cannot.
+// A bucket too large to rank is
 // narrowed by 12 more bits. Then one pass over the keys marks, per thread,
 // the keys above the bucket of the n-th largest key and the keys inside it
 // (bit masks); the few keys in the bucket are gathered and ranked among
@@ -229,7 +233,7 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
     return;
   }
   const int id0 = tid * NJ;
-  // The row is padded to a multiple of 4 scores, so each 16-byte load is
+  // The row is padded to a multiple of 4 keys, so each 16-byte load is
   // wholly inside the row or wholly past it (then it reads 0); ids past M
   // are never used.
   const __amdgpu_buffer_rsrc_t rs = buf_rsrc(a.keys + grp * a.score_stride, (uint32_t)((M + 3) & ~3) * 4);
@@ -614,18 +618,6 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
   publish();
 }
 
-// Pooled query (Fig. 3) and Quest scores (Eq. 4) of blocks [b0, b1) of group
-// (bb, hk), range `range` of the group's `nranges`, by a workgroup of NW
-// waves. Lane (r, c) handles dims [8c, 8c + 8) of 16-block tiles, so each
-// wave-wide load is four whole 256-byte summary rows, and the next PF tiles'
-// loads are in flight while one is scored. Per dimension the larger of
-// q*kmax and q*kmin is the product with kmax when q >= 0 and with kmin
-// otherwise (exactly, as fp32 rounding is monotone), so the summary row is
-// selected before the multiply. Scores are staged in LDS (s_score) and
-// written out coalesced with write-through stores; with `a.fused` the
-// workgroup also counts its keys' 8 high bits (and 8 more inside the window
-// hint `win`) into its own histogram slot with agent-scope stores. Returns
-// with those stores issued (the caller waits for them before its ticket).
 // What the scoring workgroups of a group read of its sequence: the length
 // (with the appended row), its blocks M, the first forced local block, and
 // the window hint. The group's tail takes the same values.
@@ -635,6 +627,20 @@ struct RangeInfo {
   uint32_t win;
 };
 
+// Pooled query (Fig. 3) and Quest scores (Eq. 4) of the blocks of range
+// `range` of group (bb, hk), one of the group's `nranges`, by a workgroup of
+// NW waves; returns what it read of the sequence. Lane (r, c) handles dims
+// [8c, 8c + 8) of 16-block tiles, so each wave-wide load is four whole
+// 256-byte summary rows, and the next PF tiles' loads are in flight while one
+// is scored. Per dimension the larger of q*kmax and q*kmin is the product
+// with kmax when q >= 0 and with kmin otherwise (exactly, as fp32 rounding is
+// monotone), so the summary row is selected before the multiply. Scores are
+// staged in LDS (s_score) and written out coalesced as order-preserving keys
+// with write-through stores; with `a.fused` the workgroup also counts its
+// keys' 8 high bits (and 8 more inside the window hint) into its own
+// histogram slot, and with kLists writes the in-window path's above-window
+// bits and in-window list, all with agent-scope stores. Returns with those
+// stores issued (the caller waits for them before its ticket).
 template <int NW, int PF, bool kOpaque, bool kLists>
 __device__ __forceinline__ RangeInfo score_range(const SelectArgs& a, int bb, int hk, int range, int nranges,
                                                  uint32_t* s_hist, float* s_score) {
