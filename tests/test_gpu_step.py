@@ -79,6 +79,24 @@ def test_step_matches_separate_calls(g, b):
         pass
 
 
+def test_step_window_lists():
+    """16 groups of 8200 - 8750 blocks (32 keys per thread of the fused
+    step's 512-thread top-n, 31 score ranges of 288 blocks): from the second
+    step on, the window hint is set and the fused step's top-n takes the
+    in-window path (above-window bits and in-window lists written by its score
+    ranges), while append_select (12 keys per thread) reads every key; the
+    selections must be identical and the outputs equal up to summation order."""
+    w = W.LONG_64K.with_(batch=2, num_kv_heads=8, num_q_heads=32, seq_len=140000, seed_tag="steplists")
+    cap = 140064
+    lens = [140000, 131500]
+    K, V = W.kv_cache(w, capacity=cap)
+    cache = make_cache(K, V, 16, sentinel=False)
+    del K, V
+    R.block_summarize(cache, i32(lens))
+    for _ in run_pair(w, cache, lens, steps=4):
+        pass
+
+
 def test_step_against_oracle_loop():
     """Ten fused steps on one workspace against the oracle's decode loop
     (appends, selections within the near-tie rule, attention within 2e-3),
