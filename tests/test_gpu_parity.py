@@ -461,14 +461,16 @@ def test_decode_deterministic():
 
 
 @pytest.mark.parametrize("b,n_local,M", [(16, 1, 40), (16, 0, 40), (32, 1, 40), (64, 0, 40),
-                                         (16, 1, 33000)])
+                                         (16, 1, 12500), (16, 1, 33000)])
 def test_append_select_matches_separate(b, n_local, M):
     """resa_append_select == resa_append_kv then resa_select_blocks, bit for
     bit: ids, counts, scores, cache rows, summaries and lengths, over three
-    steps with appends that open a block and appends inside one (M = 33000
-    takes the standalone top-n kernel)."""
+    steps with appends that open a block and appends inside one, and the ids
+    equal to a selection on a fresh workspace (no window hint) of the same
+    cache (M = 12500 with 8 kv heads takes the in-window top-n path from the
+    second step on; M = 33000 the standalone top-n kernel)."""
     B = 3 if M < 1000 else 1
-    H, g = 2, 4
+    H, g = (8 if M == 12500 else 2), 4
     cap = M * b
     rng = np.random.default_rng(b * 100 + n_local + M)
     lens0 = [cap - 3 * b, cap // 2 - 1, cap // 3 + 5][:B]
@@ -496,9 +498,11 @@ def test_append_select_matches_separate(b, n_local, M):
                                  scores_out=s1, workspace=ws1)
         i2, n2 = R.append_select(c2, up(kn), up(vn), up(q), l2, bound, 0.9, 2, n_local,
                                  n_cap=n_cap, scores_out=s2, workspace=ws2)
+        i3, n3 = R.select_blocks(c2, up(q), l2, bound + 1, 0.9, 2, n_local, n_cap=n_cap)
         torch.cuda.synchronize()
         assert torch.equal(l1, l2)
         assert torch.equal(n1, n2) and torch.equal(i1, i2)
+        assert torch.equal(n3, n2) and torch.equal(i3, i2)
         assert torch.equal(s1.isnan(), s2.isnan())
         assert torch.equal(torch.nan_to_num(s1), torch.nan_to_num(s2))
         bound += 1
