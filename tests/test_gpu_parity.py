@@ -658,6 +658,12 @@ def test_decode_loop_small(fused, paged):
                 swaps += s
                 if s == 0:
                     assert max_abs_err(go[bi, 4 * hi:4 * hi + 4], ro[bi, 4 * hi:4 * hi + 4]) <= TOL
+                else:
+                    # Near-tie swap: the attention on the GPU's own set.
+                    q64 = O.bf16_to_f64(q)[bi, 4 * hi:4 * hi + 4]
+                    own, _ = O.sparse_attend(q64, st.K[bi, hi], st.V[bi, hi], st.L[bi],
+                                             gi[bi, hi, :gn[bi, hi]], 16, w.sm_scale)
+                    assert max_abs_err(go[bi, 4 * hi:4 * hi + 4], own) <= TOL
         if (step + 1) % f == 0:
             # The window is the f rows appended since the last rectification.
             rows = [W.decode_kv(w, s) for s in range(step - f + 1, step + 1)]

@@ -218,6 +218,47 @@ def update_wrong_block(kmin, kmax, pos, b, k_new):
         kmax[m] = np.maximum(kmax[m], k_new)
 
 
+def split_heads_interleaved(q, num_kv_heads):
+    """Query head h taken as a member of kv head h % Hkv (not h // g)."""
+    B, Hq = q.shape[:2]
+    g = Hq // num_kv_heads
+    return np.swapaxes(q.reshape(B, g, num_kv_heads, *q.shape[2:]), 1, 2)
+
+
+class StateAttendScattered(O.DecodeState):
+    """Groups attended correctly but written back at heads i, i + Hkv, ..."""
+
+    def attend(self, q, idx, sm_scale):
+        out, lse = super().attend(q, idx, sm_scale)
+        B, H = self.K.shape[:2]
+        g = out.shape[1] // H
+        return (np.swapaxes(out.reshape(B, H, g, -1), 1, 2).reshape(out.shape),
+                np.swapaxes(lse.reshape(B, H, g), 1, 2).reshape(lse.shape))
+
+
+class StateSelectFirstHead(O.DecodeState):
+    """Each group scored with its first query head instead of the pooled mean."""
+
+    def select(self, q, sparsity, min_blocks, n_local):
+        q = np.asarray(q, dtype=np.float64)
+        B, Hq = q.shape[:2]
+        g = Hq // self.K.shape[1]
+        q1 = np.repeat(q[:, ::g], g, axis=1)
+        return super().select(q1, sparsity, min_blocks, n_local)
+
+
+def with_split_heads(fn, pin):
+    """Runs ``pin`` with the oracle module's split_heads replaced by ``fn``."""
+    def run():
+        saved = O.resa_oracle.split_heads
+        O.resa_oracle.split_heads = fn
+        try:
+            return pin()
+        finally:
+            O.resa_oracle.split_heads = saved
+    return run
+
+
 # ------------------------------------------------------------------- table
 
 S, Q, C, SEL = O.block_summaries, O.pooled_query, O.num_selected, O.select_blocks
@@ -250,6 +291,14 @@ CASES = {
     "rectify_refresh_short": lambda: P.pin_worked_rectify(rectify_refresh_short),
     "update_no_reinit": lambda: P.pin_incremental_summary(update_no_reinit, S),
     "update_wrong_block": lambda: P.pin_incremental_summary(update_wrong_block, S),
+    "split_heads_interleaved_attend": with_split_heads(
+        split_heads_interleaved, lambda: P.pin_gqa_attend(O.DecodeState)),
+    "split_heads_interleaved_select": with_split_heads(
+        split_heads_interleaved, lambda: P.pin_gqa_select(O.DecodeState)),
+    "split_heads_interleaved_rectify": with_split_heads(
+        split_heads_interleaved, lambda: P.pin_gqa_rectify(O.DecodeState)),
+    "state_attend_scattered": lambda: P.pin_gqa_attend(StateAttendScattered),
+    "state_select_first_head": lambda: P.pin_gqa_select(StateSelectFirstHead),
 }
 
 

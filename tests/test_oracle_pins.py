@@ -518,3 +518,140 @@ def test_decode_state_loop_consistent():
                 assert np.array_equal(st.kmin[bi, hi, :M], rmin)
                 assert np.array_equal(st.kmax[bi, hi, :M], rmax)
     assert st.L == [112, 105]
+
+
+# --------------------------------------------------------------------------
+# GQA head mapping (Eq. 1; Sec. 2.1, Fig. 3): query head h = i * g + j belongs
+# to kv head i = h // g, and the g heads of group i share one pooled query
+# and one block set. Checked on the whole-batch DecodeState (which splits
+# heads into groups) against naive per-head loops that index kv head h // g
+# directly, with kv heads whose caches differ so that any other mapping
+# changes the result.
+
+def _gqa_case(seed=11):
+    rng = np.random.default_rng(seed)
+    B, Hkv, g, D, b, cap = 2, 3, 2, 4, 4, 40
+    lens = [23, 18]
+    # Each kv head gets its own offset and scale; whole numbers keep the
+    # summaries and pooled queries exact.
+    K = np.zeros((B, Hkv, cap, D))
+    V = np.zeros((B, Hkv, cap, D))
+    for bi in range(B):
+        for hi in range(Hkv):
+            K[bi, hi] = rng.integers(-6, 7, size=(cap, D)) * (hi + 1) + 3 * hi
+            V[bi, hi] = rng.integers(-6, 7, size=(cap, D)) + 10 * hi + 100 * bi
+    q = rng.integers(-3, 4, size=(B, Hkv * g, D)).astype(np.float64) * 0.25
+    return rng, K, V, q, lens, g, b
+
+
+def pin_gqa_attend(state_cls):
+    """DecodeState.attend: head h of sequence b equals naive attention of
+    q[b, h] over kv head h // g (all blocks selected: every valid token)."""
+    _, K, V, q, lens, g, b = _gqa_case()
+    st = state_cls(K, V, lens, b)
+    B, Hkv = K.shape[:2]
+    idx = {(bi, hi): list(range(-(-lens[bi] // b))) for bi in range(B) for hi in range(Hkv)}
+    out, lse = st.attend(q, idx, 0.3)
+    for bi in range(B):
+        for h in range(Hkv * g):
+            wo, wl = naive_attention(q[bi, h:h + 1], K[bi, h // g], V[bi, h // g],
+                                     list(range(lens[bi])), 0.3)
+            if not (np.allclose(out[bi, h], wo[0], rtol=0, atol=1e-9)
+                    and abs(lse[bi, h] - wl[0]) <= 1e-9):
+                return False
+    return True
+
+
+def pin_gqa_select(state_cls):
+    """DecodeState.select: the scores of group (b, i) are Eq. 4 with the mean
+    of query heads i*g .. i*g + g - 1 (Fig. 3) over kv head i's blocks,
+    written out with loops; the kept ids follow by brute force."""
+    _, K, V, q, lens, g, b = _gqa_case()
+    st = state_cls(K, V, lens, b)
+    B, Hkv, _, D = K.shape
+    scores, idx, ns = st.select(q, 0.5, 1, 1)
+    for bi in range(B):
+        L = lens[bi]
+        M = -(-L // b)
+        for i in range(Hkv):
+            qbar = [sum(q[bi, i * g + j, d] for j in range(g)) / g for d in range(D)]
+            want = []
+            for m in range(M):
+                toks = range(m * b, min(m * b + b, L))
+                s = 0.0
+                for d in range(D):
+                    hi_ = max(K[bi, i, t, d] for t in toks)
+                    lo_ = min(K[bi, i, t, d] for t in toks)
+                    s += max(qbar[d] * hi_, qbar[d] * lo_)
+                want.append(s)
+            if not np.allclose(scores[bi, i], want, rtol=0, atol=1e-12):
+                return False
+            forced = [math.inf if m == M - 1 else want[m] for m in range(M)]
+            n = ns[bi, i]
+            best = sorted(range(M), key=lambda m: (-forced[m], m))[:n]
+            if list(idx[bi, i]) != sorted(best):
+                return False
+    return True
+
+
+def pin_gqa_rectify(state_cls):
+    """DecodeState.rectify: window row r of head h attends causally over kv
+    head h // g after that head's last f rows became k_f / v_f."""
+    rng, K, V, q, lens, g, b = _gqa_case()
+    B, Hkv, _, D = K.shape
+    f = 3
+    qf = rng.integers(-3, 4, size=(B, Hkv * g, f, D)).astype(np.float64) * 0.25
+    kf = rng.integers(-5, 6, size=(B, Hkv, f, D)).astype(np.float64)
+    vf = rng.integers(-5, 6, size=(B, Hkv, f, D)).astype(np.float64) + 50
+    st = state_cls(K, V, lens, b)
+    out, lse = st.rectify(qf, kf, vf, f, 0.3)
+    for bi in range(B):
+        L = lens[bi]
+        for h in range(Hkv * g):
+            Kh = K[bi, h // g].copy()
+            Vh = V[bi, h // g].copy()
+            Kh[L - f:L] = kf[bi, h // g]
+            Vh[L - f:L] = vf[bi, h // g]
+            for r in range(f):
+                wo, wl = naive_attention(qf[bi, h, r:r + 1], Kh, Vh, list(range(L - f + r + 1)), 0.3)
+                if not (np.allclose(out[bi, h, r], wo[0], rtol=0, atol=1e-9)
+                        and abs(lse[bi, h, r] - wl[0]) <= 1e-9):
+                    return False
+    return True
+
+
+def test_gqa_attend_head_mapping():
+    assert pin_gqa_attend(O.DecodeState)
+
+
+def test_gqa_select_head_mapping():
+    assert pin_gqa_select(O.DecodeState)
+
+
+def test_gqa_rectify_head_mapping():
+    assert pin_gqa_rectify(O.DecodeState)
+
+
+# --------------------------------------------------------------------------
+# The comparison rule used by every GPU selection test (oracle/compare.py):
+# exact count, ascending unique ids in range, forced blocks present, and
+# only near-tie swaps at the threshold score.
+
+def test_check_selection_rule():
+    from oracle.compare import check_selection, max_abs_err
+    scores = [5.0, 1.0, 3.0, 2.9995, 0.5, 7.0]   # block 5 is the forced local block
+    ref = [0, 2, 5]                                 # top 2 by score + the forced block
+    assert check_selection([0, 2, 5], ref, scores, 3, 1) == 0
+    # Block 3 is within 1e-3 of the threshold (3.0): a near-tie swap.
+    assert check_selection([0, 3, 5], ref, scores, 3, 1) == 1
+    bad = [
+        [0, 1, 5],        # block 1 is 2.0 below the threshold
+        [0, 2],           # wrong count
+        [2, 0, 5],        # not ascending
+        [0, 2, 3],        # forced block missing
+        [0, 2, 6],        # id out of range
+    ]
+    for dev in bad:
+        with pytest.raises(AssertionError):
+            check_selection(dev, ref, scores, 3, 1)
+    assert max_abs_err([1.0, -np.inf], [1.5, -np.inf]) == 0.5
