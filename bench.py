@@ -13,8 +13,13 @@ key channels). Steps cycle through `--layers` independent layer caches, as a
 model's layers do, so data reused from one step to the next cannot be served
 by the 256 MB last-level cache.
 
-Prints one JSON line. `value` is the GPU time of the timed steps (HIP events
-on the launch stream around the whole loop). By default the timed steps are
+Prints one JSON line. `value` is the GPU time per step of the timed steps
+(HIP events on the launch stream around the whole loop) with rectification
+at its amortised rate of one call per f steps: the calls inside the timed
+window are replaced by their measured per-call duration / f, and a window too
+short to hold any (fewer than f steps per layer) gets one separately timed
+call per layer, so short and long runs measure the same configured step
+(`timed_gpu_us_per_step` is the raw timed figure). By default the timed steps are
 recorded once into a HIP graph and replayed, as a serving loop would run
 them; `--eager` launches every step from the host instead (the gaps between
 host launches then count too). The per-kernel figures come from a second
@@ -22,7 +27,11 @@ pass that replays every launch of one kernel from the timed loop back to
 back between two events. `roofline` is for the step's dominant kernel: the
 fused step (bytes of the block summaries and of the selected K/V blocks) or,
 with --mode two / three, the sparse decode (selected K/V); `decode_roofline`
-is always the standalone sparse-decode kernel on the same selections.
+is always the standalone sparse-decode kernel on the same selections;
+`rectify_roofline` gives the rectification call's HBM fraction (every
+group's K and V read once) and its matrix-core fraction (4 * 128 flops per
+query head, window row and visible key); `stream_read_ceiling` is the read
+bandwidth a plain streaming kernel reaches on the same GPU.
 """
 from __future__ import annotations
 
@@ -40,6 +49,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 / fp16 matrix-core peak
 METRIC = "sparse decode µs/step + achieved HBM GB/s (% roofline) at 64K/256K ctx"
 
 
@@ -80,6 +90,8 @@ def parse():
                    help="decode splits per (sequence, kv head); 0 = the library's choice")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work")
+    p.add_argument("--stream-probe", type=int, default=2 ** 31,
+                   help="bytes of the stream-read ceiling measurement (0: skip)")
     p.add_argument("--copy-probe", type=int, default=0,
                    help="bytes of one plain device copy before the timed steps (counter reference)")
     return p.parse_args()
@@ -424,6 +436,53 @@ def measure(args, w, dense: bool) -> dict:
         torch.cuda.synchronize()
         phase_us[ph] = a.elapsed_time(z) * 1e3 / len(cs)
 
+    # Rectification (Alg. 1: every f-th step of a layer) enters the step at
+    # its amortised rate, one call per f steps (the 1/f term of Eq. 6), for
+    # any number of timed steps: the calls made inside the timed window are
+    # taken out of the timed GPU time at their measured per-call duration and
+    # the per-call duration / f is added back. When the window holds no call
+    # (fewer than f steps per layer), one call per layer is timed on its own,
+    # on the cache as the loop left it, with rows of the layer's decode inputs.
+    n_rect_in = sum(1 for c in calls if c[0] == "rectify")
+    rect_how = None
+    if not dense:
+        if "rectify" in phase_us:
+            rect_how = "inside the timed window"
+        else:
+            reps = 3
+            rin = []
+            for li, ly in enumerate(layers):
+                pick = torch.arange(f, device=dev) % per_layer
+                k_last = ly["k"][pick].permute(1, 2, 0, 3).contiguous()
+                v_last = ly["v"][pick].permute(1, 2, 0, 3).contiguous()
+                rin.append(WD.rectify_rows(w, k_last, v_last, f, 7919 + li, dev))
+            torch.cuda.synchronize()
+
+            def rect_call(li):
+                ly = layers[li]
+                qf, kf, vf = rin[li]
+                Lc = L0 + ly["steps"]
+                check(lb.resa_dense_rectify(C.byref(ly["desc"]), qf.data_ptr(), kf.data_ptr(),
+                                            vf.data_ptr(), Hq, f, ly["lens"].data_ptr(), Lc, sm,
+                                            rout.data_ptr(), None, 1, ws_rec.data_ptr(),
+                                            ws_rec.numel(), sptr))
+            for li in range(nlay):  # untimed warm-up call per layer
+                rect_call(li)
+            torch.cuda.synchronize()
+            a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for _ in range(reps):
+                for li in range(nlay):
+                    rect_call(li)
+            z.record(stream)
+            torch.cuda.synchronize()
+            phase_us["rectify"] = a.elapsed_time(z) * 1e3 / (reps * nlay)
+            rect_how = (f"timed separately ({reps} calls per layer after a warm-up call): fewer than f "
+                        "steps per layer in the window")
+    t_rect = phase_us.get("rectify", 0.0)
+    timed_us = gpu_ms * 1e3 / args.steps
+    step_us = (gpu_ms * 1e3 - n_rect_in * t_rect) / args.steps + (t_rect / f if not dense else 0.0)
+
     # Algorithmic bytes of each launch: the selected blocks' K and V rows
     # (decode), plus the kmin / kmax summaries of every block (fused step).
     bytes_dec, bytes_sum = [], []
@@ -451,11 +510,31 @@ def measure(args, w, dense: bool) -> dict:
         roofline = roof("k_step", "decode_step", avg_bytes + avg_sum, phase_us["step"])
     else:
         roofline = dec_roof
-    ms_per_step = gpu_ms / args.steps
+    ms_per_step = step_us / 1e3
     n_calls = {ph: sum(1 for c in calls if c[0] == ph) for ph in phase_us}
+    per_step = {k: round(v * n_calls[k] / args.steps, 2) for k, v in phase_us.items() if k != "rectify"}
+    rect = None
+    if not dense:
+        per_step["rectify"] = round(t_rect / f, 2)
+        # Rectification roofline: every group's K and V read once (L x 512 B per
+        # group at the mean length of the calls) and the matrix work of causal
+        # attention, 4 * 128 flops per (query head, window row, visible key).
+        Lr = (sum(c[4] + 1 for c in calls if c[0] == "rectify") / n_rect_in) if n_rect_in else \
+            (L0 + sum(ly["steps"] for ly in layers) / nlay)
+        r_bytes = B * H * Lr * D * 2 * 2
+        visible = f * (Lr - f) + f * (f + 1) / 2
+        r_flops = 4.0 * D * Hq * B * visible
+        r_gbs = r_bytes / (t_rect * 1e-6) / 1e9
+        r_tf = r_flops / (t_rect * 1e-6) / 1e12
+        rect = {"us_per_call": round(t_rect, 2), "every": f, "us_per_step": round(t_rect / f, 2),
+                "calls_in_window": n_rect_in, "timing": rect_how,
+                "hbm": {"achieved": round(r_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": round(r_gbs / HBM_PEAK_GBS, 4), "bytes_per_call": int(r_bytes)},
+                "mfma": {"achieved": round(r_tf, 1), "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(r_tf / MFMA_PEAK_TFLOPS, 4), "flops_per_call": r_flops}}
     res = {
         "metric": METRIC,
-        "value": round(ms_per_step * 1e3, 2),
+        "value": round(step_us, 2),
         "unit": "us/step",
         "n_gpus": 1,
         "steps": args.steps,
@@ -475,10 +554,48 @@ def measure(args, w, dense: bool) -> dict:
         "roofline": roofline,
         "decode_roofline": dec_roof,
         "kernel_us_per_launch": {k: round(v, 2) for k, v in phase_us.items()},
-        "kernel_us_per_step": {k: round(v * n_calls[k] / args.steps, 2) for k, v in phase_us.items()},
+        "kernel_us_per_step": per_step,
+        "rectify_roofline": rect,
+        "timed_gpu_us_per_step": round(timed_us, 2),
         "wall_us_per_step": round(wall * 1e6 / args.steps, 2),
     }
+    if args.stream_probe > 0:
+        res["stream_read_ceiling"] = stream_ceiling(lb, check, dev, stream, args.stream_probe)
+        res["decode_roofline"]["frac_of_stream_ceiling"] = round(
+            dec_roof["achieved"] / res["stream_read_ceiling"]["achieved"], 4)
     return res
+
+
+def stream_ceiling(lb, check, dev, stream, nbytes) -> dict:
+    """HBM read ceiling on this GPU: resa_stream_read over a buffer of
+    `nbytes` (larger than the last-level cache) at a few grid sizes, the
+    median of 5 timed reads each; the best grid is reported."""
+    import torch
+    buf = torch.zeros(nbytes // 2, dtype=torch.bfloat16, device=dev)
+    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+    best = None
+    for wgs in (512, 1024, 2048, 4096):
+        def run():
+            check(lb.resa_stream_read(buf.data_ptr(), buf.numel() * 2, sink.data_ptr(), 1, wgs,
+                                      stream.cuda_stream))
+        for _ in range(2):
+            run()
+        times = []
+        for _ in range(5):
+            a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            run()
+            z.record(stream)
+            torch.cuda.synchronize()
+            times.append(a.elapsed_time(z) * 1e3)
+        us = sorted(times)[2]
+        if best is None or us < best[0]:
+            best = (us, wgs)
+    us, wgs = best
+    gbs = buf.numel() * 2 / (us * 1e-6) / 1e9
+    del buf
+    return {"achieved": round(gbs, 1), "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+            "bytes": int(nbytes), "us": round(us, 2), "workgroups": wgs, "kernel": "k_stream_read"}
 
 
 def breakdown(args) -> dict:
@@ -538,8 +655,6 @@ def sweep(args) -> dict:
         row["speedup_vs_dense"] = round(dense[row["block_size"]]["us_per_step"] / row["us_per_step"], 3)
     return {"sweep": rows, "dense": dense, "workload": describe(W.SWEEP_64K, 2, False)}
 
-
-MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 / fp16 matrix-core peak
 
 
 def prefill(args) -> dict:

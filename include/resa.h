@@ -314,6 +314,20 @@ int resa_dense_rectify(const resa_kv_cache_t* c, const void* q_f, const void* k_
 /* Zero-fills a workspace with a kernel (safe under stream capture). */
 int resa_workspace_clear(void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Measurement helper, not part of the attention method: reads every byte of
+ * `buffer` (device, 16-byte aligned, `bytes` a multiple of 16) once with the
+ * 16-byte non-temporal loads the decode kernel uses for K and V, spread over
+ * `workgroups` workgroups of 256 threads (1 .. 65536). The XOR of all words
+ * read is stored to sink[0] (device uint32) only if it equals `match`, so the
+ * loads cannot be elided and the sink is normally untouched. Timing it gives
+ * the HBM read ceiling the decode bandwidth is compared with.
+ * Errors: RESA_ERR_INVALID_ARG for a null or misaligned pointer, a size that
+ * is not a multiple of 16 or a workgroup count out of range.
+ */
+int resa_stream_read(const void* buffer, size_t bytes, uint32_t* sink, uint32_t match,
+                     int32_t workgroups, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -14,7 +14,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libresa.so")
-SOURCES = ["api.cpp", "summarize.hip", "select.hip", "decode.hip", "step.hip", "rectify.hip"]
+SOURCES = ["api.cpp", "summarize.hip", "select.hip", "decode.hip", "step.hip", "rectify.hip",
+           "probe.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -608,4 +608,18 @@ int resa_workspace_clear(void* workspace, size_t workspace_bytes, void* stream) 
   return ok();
 }
 
+int resa_stream_read(const void* buffer, size_t bytes, uint32_t* sink, uint32_t match,
+                     int32_t workgroups, void* stream) {
+  RESA_CHECK_PTR(buffer, 16);
+  RESA_CHECK_PTR(sink, 4);
+  if (bytes % 16 != 0) return fail(RESA_ERR_INVALID_ARG, "bytes %zu is not a multiple of 16", bytes);
+  if (workgroups < 1 || workgroups > 65536)
+    return fail(RESA_ERR_INVALID_ARG, "workgroups %d outside [1, 65536]", workgroups);
+  if (bytes == 0) return ok();
+  hipError_t e = resa::launch_stream_read(buffer, bytes, sink, match, workgroups,
+                                          static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "resa_stream_read launch");
+  return ok();
+}
+
 }  // extern "C"

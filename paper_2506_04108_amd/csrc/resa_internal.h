@@ -132,6 +132,8 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
 hipError_t launch_step(const StepArgs& a, hipStream_t stream);
 hipError_t launch_rectify(const RectifyArgs& a, hipStream_t stream);
 hipError_t launch_clear(void* p, size_t bytes, hipStream_t stream);
+hipError_t launch_stream_read(const void* buf, size_t bytes, uint32_t* sink, uint32_t match,
+                              int32_t workgroups, hipStream_t stream);
 
 // Split-count and chunk heuristics (host).
 int32_t select_fused_max_blocks();
