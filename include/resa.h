@@ -225,7 +225,9 @@ size_t resa_decode_workspace_size(int32_t batch, int32_t num_kv_heads,
  *   out[b, h, :] = sum_t softmax_t(q_h . K_t * sm_scale) V_t     (fp32)
  *   lse[b, h]    = log sum_t exp(q_h . K_t * sm_scale)           (optional)
  * With no token selected, out is 0 and lse is -inf. Passing every block id
- * gives dense decoding. num_splits = 0 picks resa_decode_num_splits();
+ * gives dense decoding. Value range: the fp32 accumulation keeps softmax
+ * weights up to 2^8 over up to 2^20 tokens per split, so results are finite
+ * for |v| <= 2^100. num_splits = 0 picks resa_decode_num_splits();
  * explicit counts must lie in [1, 256].
  * One kernel: each split writes a partial into the workspace and the last
  * split of a group to finish merges them. The workspace starts with one merge
@@ -297,6 +299,13 @@ size_t resa_rectify_workspace_size(int32_t batch, int32_t num_kv_heads,
  * max_seq_len bounds every seq_lens[b] (host side, for launch sizing). A
  * sequence with seq_lens[b] < f is left untouched and its out rows are 0 (lse
  * -inf). The workspace holds split partials and needs no initialisation.
+ * Value range: any finite bf16 V gives a finite out. P . V runs on fp16
+ * matrix cores with P in [0, 2^8]; V enters at its own scale (exact for
+ * |v| in 2^-14 .. 65280, fp16 subnormal spacing 2^-24 below), and a head
+ * dimension holding larger values is scaled by a power of two for the
+ * whole call from the first tile that needs it (its smaller values then lose
+ * the bits below 2^-24 of the scale, far below 2e-3 of the dimension's
+ * largest magnitude).
  * Errors: RESA_ERR_INVALID_ARG for the ranges above or misaligned pointers,
  * RESA_ERR_WORKSPACE when a needed workspace is missing or too small.
  * The same call serves (chunked) prefill (Alg. 1, prefill step): with

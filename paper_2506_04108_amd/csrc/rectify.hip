@@ -15,16 +15,25 @@
 // separates filling a buffer from reading it. Per tile and wave:
 //   S^T = K . Q^T        (keys x queries; lane l holds query l % 16 and keys
 //                          16 kt + 4 (l / 16) + i)
-//   online softmax per query row in the log2 domain; P (in [0, 1]) is
+//   online softmax per query row in the log2 domain against a reference
+//   that moves only in steps of more than 2^8, so P lies in [0, 2^8]; P is
 //   rounded to fp16 (11 significant bits)
 //   O^T += V^T . P^T     (dims x queries, fp16 MFMA; the contraction index is
 //                          ordered so that P^T is already in the B-operand
 //                          layout, and V^T comes from the row-major V tile
 //                          through the LDS transpose read)
-// V tiles are converted from bf16 to fp16 on their way into LDS: every bf16
-// value of magnitude 2^-14 .. 65504 is an fp16 value (8 significant bits
-// fit in 11), so only values below 2^-14 in magnitude, whose products with
-// P in [0, 1] are below 2^-14, lose bits.
+// V tiles are converted from bf16 to fp16 on their way into LDS, each head
+// dimension d multiplied by a power of two 2^-E_d first (E_d = 0 until a
+// value needs it). Every bf16 value of magnitude 2^-14 .. 65280 is an fp16
+// value (8 significant bits fit in 11), so in that range the conversion is
+// exact; smaller values keep fp16's subnormal spacing of 2^-24 (an error of at
+// most 2^-24 * P per key). A thread that finds a scaled value above 65504
+// flags the tile; on a flagged tile every wave reloads the tile's V, raises
+// E_d of the dimensions that need it (so that max |v| 2^-E_d < 2^16),
+// multiplies those accumulator rows by the change, and converts the tile
+// again. Rows are multiplied back by 2^E_d after the normalisation by the
+// softmax sum, so every finite bf16 V gives a finite result (products
+// P V 2^-E_d stay below 2^24 and their sums far below the fp32 range).
 // Masking (causal cut, end of the split) is only evaluated on the tiles that
 // reach it. A second kernel merges the splits by log-sum-exp (Alg. 2,
 // "Combine"), spread over many workgroups.
@@ -61,12 +70,6 @@ __device__ __forceinline__ f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
 }
 __device__ __forceinline__ f32x4_t mfma16(f16x8_t a, f16x8_t b, f32x4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
-}
-
-// Two bf16 (one 32-bit word) -> two fp16 (one 32-bit word).
-__device__ __forceinline__ uint32_t bf2_to_h2(uint32_t w) {
-  const f16x2_t h = {(_Float16)bf_lo(w), (_Float16)bf_hi(w)};
-  return __builtin_bit_cast(uint32_t, h);
 }
 
 // LDS transpose read of a 4-key x 16-dim block of 16-bit values by each
@@ -110,6 +113,13 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
   constexpr int kRowStep = kThreads / 16;           // tile rows covered by one pass of the threads
   __shared__ __attribute__((aligned(16))) uint16_t sK[2][kTileElems];
   __shared__ __attribute__((aligned(16))) uint16_t sV[2][kTileElems];
+  // V range handling: s_flag[buf] = first key of the tile in buffer buf when
+  // one of its scaled values is above the fp16 range (else an older tile's
+  // key, or -1); s_vscale[cur][d] = 2^-E_d; s_vmax[d] = max |v| of dimension
+  // d over a flagged tile (fp32 bits: non-negative values order as integers).
+  __shared__ int s_flag[2];
+  __shared__ __attribute__((aligned(16))) float s_vscale[2][kHeadDim];
+  __shared__ uint32_t s_vmax[kHeadDim];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int split = blockIdx.x, qblk = blockIdx.y, grp = blockIdx.z;
   const int bb = grp / a.c.kv_heads, hk = grp % a.c.kv_heads;
@@ -186,14 +196,103 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
     }
     lookup(t0 + kKeyTile);
   };
-  auto lstore = [&](int buf) {
+  // V scale state, uniform across the workgroup: `scaled` once any E_d > 0,
+  // `cur` the current half of s_vscale.
+  bool scaled = false;
+  int cur = 0;
+  // Converts a 16-byte piece of V (8 bf16 values of dims part*8 ..) to fp16,
+  // times the per-dimension factors when `scaled`; vmax collects the largest
+  // scaled magnitude.
+  auto to_h8 = [&](const U4& w, const float (&sc)[8], bool use_sc, float& vmax) __attribute__((always_inline)) {
+    float x[8] = {bf_lo(w.x), bf_hi(w.x), bf_lo(w.y), bf_hi(w.y),
+                  bf_lo(w.z), bf_hi(w.z), bf_lo(w.w), bf_hi(w.w)};
+    uint32_t h[4];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      if (use_sc) x[i] *= sc[i];
+      vmax = fmaxf(vmax, fabsf(x[i]));
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const f16x2_t p = {(_Float16)x[2 * i], (_Float16)x[2 * i + 1]};
+      h[i] = __builtin_bit_cast(uint32_t, p);
+    }
+    return U4{h[0], h[1], h[2], h[3]};
+  };
+  // Stores the loaded tile (first key `tag`) into buffer buf; a thread with a
+  // scaled V value outside the fp16 range flags the tile.
+  auto lstore = [&](int buf, int tag) __attribute__((always_inline)) {
+    float sc[8];
+    if (scaled) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) sc[i] = s_vscale[cur][part * 8 + i];
+    }
+    float vmax = 0.f;
 #pragma unroll
     for (int e = 0; e < kPieces; ++e) {
       const int off = ((tid >> 4) + kRowStep * e) * kStride + part * 8;
       st16(&sK[buf][off], rk[e]);
-      st16(&sV[buf][off], U4{bf2_to_h2(rv[e].x), bf2_to_h2(rv[e].y), bf2_to_h2(rv[e].z),
-                             bf2_to_h2(rv[e].w)});
+      st16(&sV[buf][off], scaled ? to_h8(rv[e], sc, true, vmax) : to_h8(rv[e], sc, false, vmax));
     }
+    if (!(vmax <= 65504.f)) s_flag[buf] = tag;
+  };
+  // A flagged tile (uniform: every wave reads the same flag). The tile's V is
+  // reloaded, the per-dimension maxima are gathered, E_d rises where
+  // max |v| 2^-E_d would reach 2^16, the accumulator rows of those dimensions
+  // follow, and the tile is converted again into its buffer.
+  auto fix_tile = [&](int t0, int buf) __attribute__((always_inline)) {
+    U4 vv[kPieces];
+#pragma unroll
+    for (int e = 0; e < kPieces; ++e) {
+      const int kk = t0 + (tid >> 4) + kRowStep * e;
+      const int64_t row = kk < k1 ? kv_row(a.c, bb, hk, kk) : -1;
+      vv[e] = row >= 0 ? ld16(a.c.v + (size_t)row * kHeadDim + part * 8) : U4{0, 0, 0, 0};
+    }
+    float dm[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int e = 0; e < kPieces; ++e) {
+      const float x[8] = {bf_lo(vv[e].x), bf_hi(vv[e].x), bf_lo(vv[e].y), bf_hi(vv[e].y),
+                          bf_lo(vv[e].z), bf_hi(vv[e].z), bf_lo(vv[e].w), bf_hi(vv[e].w)};
+#pragma unroll
+      for (int i = 0; i < 8; ++i) dm[i] = fmaxf(dm[i], fabsf(x[i]));
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) atomicMax(&s_vmax[part * 8 + i], __float_as_uint(dm[i]));
+    lds_sync();
+    float ns[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t mb = s_vmax[part * 8 + i];
+      // max |v| < 2^(ex + 1); E = ex - 15 keeps the scaled maximum below 2^16.
+      const int ex = (int)((mb >> 23) & 0xff) - 127;
+      const int E = ex > 15 ? ex - 15 : 0;
+      ns[i] = fminf(s_vscale[cur][part * 8 + i], __uint_as_float((uint32_t)(127 - E) << 23));
+    }
+    if (tid < 16) {  // part == tid: one thread per 8 dimensions publishes them
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s_vscale[cur ^ 1][part * 8 + i] = ns[i];
+    }
+    float unused = 0.f;
+#pragma unroll
+    for (int e = 0; e < kPieces; ++e) {
+      const int off = ((tid >> 4) + kRowStep * e) * kStride + part * 8;
+      st16(&sV[buf][off], to_h8(vv[e], ns, true, unused));
+    }
+    lds_sync();
+    if (tid < kHeadDim) s_vmax[tid] = 0u;
+    // Accumulator row d (lane dims 16 dt + 4 j + i) times 2^(E_old - E_new).
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int d = 16 * dt + 4 * j + i;
+        const float r = s_vscale[cur ^ 1][d] / s_vscale[cur][d];
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) o[dt][qt][i] *= r;
+      }
+    }
+    cur ^= 1;
+    scaled = true;
   };
 
   // One tile: scores, softmax update, P.V. kMasked evaluates the causal cut
@@ -202,6 +301,7 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
     constexpr bool kMasked = decltype(masked)::value;
     const uint16_t* tk = sK[buf];
     const uint16_t* tv = sV[buf];
+    const int flag = s_flag[buf];  // read now, used after the scores
     f32x4_t sacc[4][2];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
@@ -267,6 +367,8 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
       }
     }
 
+    if (__builtin_amdgcn_readfirstlane(flag) == t0) fix_tile(t0, buf);
+
     // P^T for 32-key step ks: lane keys 32 ks + 4 j + (0..3) then
     // 32 ks + 16 + 4 j + (0..3) (S^T tiles kt = 2 ks, 2 ks + 1); V^T rows of
     // the same keys come from two transpose reads.
@@ -287,7 +389,15 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
   if (k0 < k1) {
     lookup(k0);
     gload(k0);
-    lstore(0);
+  }
+  if (tid < kHeadDim) {
+    s_vscale[0][tid] = 1.f;
+    s_vmax[tid] = 0u;
+  }
+  if (tid < 2) s_flag[tid] = -1;
+  lds_sync();
+  if (k0 < k1) {
+    lstore(0, k0);
     if (k0 + kKeyTile < k1) gload(k0 + kKeyTile);
     lds_sync();
   }
@@ -300,7 +410,7 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
     // The other buffer was last read in the previous tile, before the
     // barrier that ended it: fill it with the next tile, start the loads of
     // the one after, and publish.
-    if (t0 + kKeyTile < k1) lstore(buf ^ 1);
+    if (t0 + kKeyTile < k1) lstore(buf ^ 1, t0 + kKeyTile);
     if (t0 + 2 * kKeyTile < k1) gload(t0 + 2 * kKeyTile);
     lds_sync();
     buf ^= 1;
@@ -323,7 +433,11 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
                          : a.part_o + (((size_t)grp * S + split) * R + rho) * kHeadDim;
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) {
-        const f32x4_t y = o[dt][qt] * inv;
+        f32x4_t y = o[dt][qt] * inv;
+        if (scaled) {  // back to the values' own scale: times 2^E_d
+#pragma unroll
+          for (int i = 0; i < 4; ++i) y[i] *= 1.f / s_vscale[cur][16 * dt + 4 * j + i];
+        }
         *reinterpret_cast<f32x4_t*>(po + 16 * dt + 4 * j) = y;
       }
       if (j == 0) {

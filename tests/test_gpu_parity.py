@@ -543,6 +543,60 @@ def test_rectify_vs_oracle(g, f):
         assert np.array_equal(O.bf16_to_f64(down(cache.kmax)[bi, :, :M]), st.kmax[bi, :, :M])
 
 
+@pytest.mark.parametrize("g,f,lens,cap", [
+    (4, 32, [2000, 1500], 2048),    # decode-time window: 4-wave workgroups, several key splits
+    (4, 300, [1000, 777], 1024),    # long window: 8-wave workgroups
+])
+def test_rectify_large_and_tiny_v(g, f, lens, cap):
+    """Rectification is finite and within 2e-3 of the oracle, scaled per head
+    dimension d by max(1, max |V[:, d]|), for every finite bf16 value:
+    planted V entries of +-3e38, 1e5 and 7e4 (above the fp16 range, at the
+    first key of a split, inside a tile and inside the rewritten window) and
+    of 1e-7 (below fp16's normal range), next to N(0, 1) dimensions, which
+    stay within 2e-3 absolutely."""
+    w, cap = small(g=g, L=max(lens), cap=cap, tag=f"bigv{f}")
+    K, V = W.kv_cache(w, capacity=cap)
+    cache_k = K
+    bits = lambda x: int(W.f32_to_bf16_bits(np.array([x], dtype=np.float32))[0])
+    V = V.copy()
+    # (sequence, kv head, row, dim, value): rows below L - f sit in the cache,
+    # rows at or past it in the rewritten window (planted into v_f below).
+    plants = [(0, 0, 3, 5, 3e38), (0, 0, 512 + 5, 5, -2.5e38), (0, 0, 700, 17, 1e5),
+              (0, 1, 0, 100, -1e5), (0, 1, 1200, 101, 7e4), (1, 0, 64, 9, 3.3e38),
+              (1, 1, 400, 33, 1e5), (0, 0, 900, 40, 1e-7), (1, 1, 20, 41, -1e-7)]
+    win = [(0, 0, 2, 6, 3e38), (1, 1, f - 1, 17, -1e5), (0, 1, 0, 70, 6e4), (1, 0, 5, 42, 1e-7)]
+    for bi, hi, row, d, x in plants:
+        if row < lens[bi] - f:
+            V[bi, hi, row, d] = bits(x)
+    cache = make_cache(cache_k, V, 16, sentinel=False)
+    lt = i32(lens)
+    R.block_summarize(cache, lt)
+    base_k = np.stack([np.stack([K[bi, hi, lens[bi] - f:lens[bi]] for hi in range(2)]) for bi in range(2)])
+    base_v = np.stack([np.stack([V[bi, hi, lens[bi] - f:lens[bi]] for hi in range(2)]) for bi in range(2)])
+    qf, kf, vf = W.rectify_inputs(w, 9, base_k, base_v, f)
+    vf = vf.copy()
+    for bi, hi, r, d, x in win:
+        vf[bi, hi, r, d] = bits(x)
+    out, lse = R.dense_rectify(cache, up(qf), up(kf), up(vf), lt, max(lens))
+    torch.cuda.synchronize()
+    go, gl = out.cpu().numpy(), lse.cpu().numpy()
+    assert np.all(np.isfinite(go)), "non-finite rectify output"
+    st = O.DecodeState(O.bf16_to_f64(K), O.bf16_to_f64(V), lens, 16)
+    ro, rl = st.rectify(O.bf16_to_f64(qf), O.bf16_to_f64(kf), O.bf16_to_f64(vf), f, w.sm_scale)
+    assert max_abs_err(gl, rl) <= TOL
+    for bi in range(2):
+        for hi in range(2):
+            L = lens[bi]
+            vmax = np.abs(st.V[bi, hi, :L]).max(axis=0)          # [D], after the rewrite
+            scale = np.maximum(1.0, vmax)
+            heads = slice(hi * g, (hi + 1) * g)
+            err = np.abs(go[bi, heads] - ro[bi, heads]) / scale  # [g, f, D]
+            worst = float(err.max())
+            print(f"large V g={g} f={f} seq {bi} head {hi}: max |dO| / max(1, |V_d|) {worst:.2e}",
+                  flush=True)
+            assert worst <= TOL
+
+
 def test_rectify_tiny4k_full():
     """The tiny 4K layer: f = 16 rows, causal over the whole 4096 cache."""
     w = W.TINY_4K
