@@ -241,6 +241,32 @@ int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_he
                        float sm_scale, float* out, float* lse, void* workspace,
                        size_t workspace_bytes, void* stream);
 
+/*
+ * resa_sparse_decode without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). Same arguments, kernels and results as
+ * resa_sparse_decode (bit-identical for the same split count), minus the
+ * workspace: the split partials and merge counters live in a static device
+ * array of resa_sparse_decode_noalloc_max_bytes() bytes (4 MiB) that each GPU
+ * the library runs on holds until the process ends. The call allocates and
+ * frees nothing; it zero-fills the merge counters with a kernel before the
+ * decode. The first call on a device looks up that device's array address
+ * (hipGetSymbolAddress). Every call on one GPU shares that GPU's array and
+ * the array keeps the last call's contents, so calls that may overlap on one
+ * GPU (different streams without ordering, concurrent host threads) race:
+ * order them on one stream. Errors: as resa_sparse_decode; RESA_ERR_WORKSPACE
+ * when the call's partials (resa_decode_workspace_size for the same shape and
+ * split count) exceed the static array, RESA_ERR_HIP when the array's address
+ * cannot be obtained.
+ */
+int resa_sparse_decode_noalloc(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
+                               const int32_t* seq_lens, const int32_t* block_idx,
+                               const int32_t* num_sel, int32_t n_cap, int32_t num_splits,
+                               float sm_scale, float* out, float* lse, void* stream);
+
+/* Bytes of the static scratch resa_sparse_decode_noalloc works in. */
+size_t resa_sparse_decode_noalloc_max_bytes(void);
+
 /* Workspace bytes resa_decode_step needs; max_seq_len and num_splits as
  * passed to it (num_splits 0 = the automatic count). */
 size_t resa_step_workspace_size(int32_t batch, int32_t num_kv_heads, int32_t num_q_heads,

@@ -55,6 +55,8 @@ SIGNATURES = {
     "resa_decode_num_splits": (_I, [_I, _I, _I, _I]),
     "resa_decode_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I]),
     "resa_sparse_decode": (C.c_int, [_CACHE, _P, _I, _P, _P, _P, _I, _I, _F, _P, _P, _P, _Z, _P]),
+    "resa_sparse_decode_noalloc": (C.c_int, [_CACHE, _P, _I, _P, _P, _P, _I, _I, _F, _P, _P, _P]),
+    "resa_sparse_decode_noalloc_max_bytes": (_Z, []),
     "resa_step_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I, _I]),
     "resa_decode_step": (C.c_int, [_CACHE, _P, _P, _P, _I, _P, _I, C.POINTER(SelectParams), _P, _P, _I,
                                    _I, _F, _P, _P, _P, _Z, _P]),

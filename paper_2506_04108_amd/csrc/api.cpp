@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "resa_internal.h"
@@ -373,13 +374,19 @@ size_t resa_decode_workspace_size(int32_t batch, int32_t num_kv_heads, int32_t n
   return decode_layout(batch, num_kv_heads, num_q_heads / num_kv_heads, s).total;
 }
 
-int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
-                       const int32_t* seq_lens, const int32_t* block_idx, const int32_t* num_sel,
-                       int32_t n_cap, int32_t num_splits, float sm_scale, float* out, float* lse,
-                       void* workspace, size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Argument checks of resa_sparse_decode and resa_sparse_decode_noalloc
+// (everything but the workspace); fills the split count and the workspace
+// layout the call needs.
+int decode_check(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
+                 const int32_t* seq_lens, const int32_t* block_idx, const int32_t* num_sel,
+                 int32_t n_cap, int32_t num_splits, float sm_scale, const float* out,
+                 const float* lse, int32_t* group, int32_t* splits, DecodeLayout* lay) {
   if (int e = check_cache(c)) return e;
-  int32_t group = 0;
-  if (int e = check_heads(c, num_q_heads, &group)) return e;
+  if (int e = check_heads(c, num_q_heads, group)) return e;
   RESA_CHECK_PTR(q, 16);
   RESA_CHECK_PTR(seq_lens, 4);
   RESA_CHECK_PTR(block_idx, 4);
@@ -390,15 +397,20 @@ int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_he
   if (num_splits < 0 || num_splits > 256)
     return fail(RESA_ERR_INVALID_ARG, "num_splits %d outside [0, 256]", num_splits);
   if (!std::isfinite(sm_scale)) return fail(RESA_ERR_INVALID_ARG, "sm_scale is not finite");
-  const int32_t s = num_splits > 0 ? num_splits
-                                   : resa::decode_auto_splits(c->batch, c->num_kv_heads, n_cap,
-                                                              c->block_size);
-  const DecodeLayout lay = decode_layout(c->batch, c->num_kv_heads, group, s);
-  if (workspace == nullptr || workspace_bytes < lay.total)
-    return fail(RESA_ERR_WORKSPACE, "decode workspace needs %zu bytes, got %zu", lay.total,
-                workspace == nullptr ? (size_t)0 : workspace_bytes);
-  if (!aligned(workspace, 16)) return fail(RESA_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
-  char* ws = static_cast<char*>(workspace);
+  *splits = num_splits > 0 ? num_splits
+                           : resa::decode_auto_splits(c->batch, c->num_kv_heads, n_cap, c->block_size);
+  *lay = decode_layout(c->batch, c->num_kv_heads, *group, *splits);
+  return RESA_OK;
+}
+
+// Enqueues the decode on checked arguments with the workspace at `ws`.
+// `clear_counters` first zero-fills the merge counters with a kernel (the
+// allocation-free variant, whose scratch every call on the device shares).
+int decode_launch(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
+                  const int32_t* seq_lens, const int32_t* block_idx, const int32_t* num_sel,
+                  int32_t n_cap, int32_t group, int32_t splits, float sm_scale, float* out,
+                  float* lse, char* ws, const DecodeLayout& lay, bool clear_counters, void* stream,
+                  const char* what) {
   resa::DecodeArgs a;
   a.c = cache_args(c);
   a.q = static_cast<const uint16_t*>(q);
@@ -408,7 +420,7 @@ int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_he
   a.block_idx = block_idx;
   a.num_sel = num_sel;
   a.n_cap = n_cap;
-  a.num_splits = s;
+  a.num_splits = splits;
   a.scale_log2 = sm_scale * 1.4426950408889634f;
   a.out = out;
   a.lse = lse;
@@ -417,9 +429,99 @@ int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_he
   a.part_o = reinterpret_cast<float*>(ws + lay.o);
   a.k_new = nullptr;
   a.v_new = nullptr;
-  hipError_t e = resa::launch_decode(a, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return hip_fail(e, "resa_sparse_decode launch");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (clear_counters) {
+    hipError_t e = resa::launch_clear(ws + lay.counters, lay.lse - lay.counters, st);
+    if (e != hipSuccess) return hip_fail(e, what);
+  }
+  hipError_t e = resa::launch_decode(a, st);
+  if (e != hipSuccess) return hip_fail(e, what);
   return ok();
+}
+
+// Scratch of resa_sparse_decode_noalloc: one array per device, held for the
+// life of the process. In host code `scratch` names a host-side stand-in,
+// never the device memory: its device address comes from
+// hipGetSymbolAddress, once per device, and only that address is passed on.
+constexpr size_t kStaticScratchBytes = size_t(4) << 20;
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array (looked up on the
+// first call on that device); nullptr with an error message on failure.
+void* device_scratch(int* status) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    *status = hip_fail(e, "resa_sparse_decode_noalloc: hipGetDevice");
+    return nullptr;
+  }
+  if (dev < 0 || dev >= kMaxDevices) {
+    *status = fail(RESA_ERR_UNSUPPORTED, "device %d beyond the %d the static scratch serves", dev,
+                   kMaxDevices);
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || ptr == nullptr) {
+      *status = hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol,
+                         "resa_sparse_decode_noalloc: hipGetSymbolAddress(scratch)");
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
+                       const int32_t* seq_lens, const int32_t* block_idx, const int32_t* num_sel,
+                       int32_t n_cap, int32_t num_splits, float sm_scale, float* out, float* lse,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+  int32_t group = 0, splits = 0;
+  DecodeLayout lay;
+  if (int e = decode_check(c, q, num_q_heads, seq_lens, block_idx, num_sel, n_cap, num_splits,
+                           sm_scale, out, lse, &group, &splits, &lay))
+    return e;
+  if (workspace == nullptr || workspace_bytes < lay.total)
+    return fail(RESA_ERR_WORKSPACE, "decode workspace needs %zu bytes, got %zu", lay.total,
+                workspace == nullptr ? (size_t)0 : workspace_bytes);
+  if (!aligned(workspace, 16)) return fail(RESA_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
+  return decode_launch(c, q, num_q_heads, seq_lens, block_idx, num_sel, n_cap, group, splits,
+                       sm_scale, out, lse, static_cast<char*>(workspace), lay, false, stream,
+                       "resa_sparse_decode launch");
+}
+
+size_t resa_sparse_decode_noalloc_max_bytes(void) { return kStaticScratchBytes; }
+
+int resa_sparse_decode_noalloc(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
+                               const int32_t* seq_lens, const int32_t* block_idx,
+                               const int32_t* num_sel, int32_t n_cap, int32_t num_splits,
+                               float sm_scale, float* out, float* lse, void* stream) {
+  int32_t group = 0, splits = 0;
+  DecodeLayout lay;
+  if (int e = decode_check(c, q, num_q_heads, seq_lens, block_idx, num_sel, n_cap, num_splits,
+                           sm_scale, out, lse, &group, &splits, &lay))
+    return e;
+  if (lay.total > kStaticScratchBytes)
+    return fail(RESA_ERR_WORKSPACE,
+                "resa_sparse_decode_noalloc needs %zu bytes of scratch, above its static %zu "
+                "(use resa_sparse_decode with a workspace, or fewer splits)",
+                lay.total, kStaticScratchBytes);
+  int status = RESA_OK;
+  void* ptr = device_scratch(&status);
+  if (ptr == nullptr) return status;
+  return decode_launch(c, q, num_q_heads, seq_lens, block_idx, num_sel, n_cap, group, splits,
+                       sm_scale, out, lse, static_cast<char*>(ptr), lay, true, stream,
+                       "resa_sparse_decode_noalloc launch");
 }
 
 size_t resa_step_workspace_size(int32_t batch, int32_t num_kv_heads, int32_t num_q_heads,
