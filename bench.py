@@ -574,7 +574,7 @@ def stream_ceiling(lb, check, dev, stream, nbytes) -> dict:
     buf = torch.zeros(nbytes // 2, dtype=torch.bfloat16, device=dev)
     sink = torch.zeros(1, dtype=torch.int32, device=dev)
     best = None
-    for wgs in (512, 1024, 2048, 4096):
+    for wgs in (256, 512, 1024, 2048):
         def run():
             check(lb.resa_stream_read(buf.data_ptr(), buf.numel() * 2, sink.data_ptr(), 1, wgs,
                                       stream.cuda_stream))

@@ -21,11 +21,12 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 # Packed fp32 VALU instructions are kept out of the generated code.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
-# Per-source flags. The selection's top-n tail (select.hip, step.hip) takes
-# one-lane atomics whose results are needed only later; the atomic optimizer
-# would broadcast each result right away, making the wave wait for the atomic
-# and for every load issued before it.
-EXTRA = {src: ["-mllvm", "-amdgpu-atomic-optimizer-strategy=None"] for src in ("select.hip", "step.hip")}
+# Per-source flags. The selection's top-n tail (select.hip, step.hip) and the
+# decode's split ticket (decode.hip) take one-lane atomics whose results are
+# needed only later; the atomic optimizer would broadcast each result right
+# away, making the wave wait for the atomic and for every load issued before it.
+EXTRA = {src: ["-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]
+         for src in ("select.hip", "step.hip", "decode.hip")}
 COMMON = ["-O3", "-std=c++20", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
           "-Wno-unused-command-line-argument", "-I", os.path.join(HERE, "..", "include")]
 

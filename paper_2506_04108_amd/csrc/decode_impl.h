@@ -2,9 +2,10 @@
 //
 // Device code shared by the decode kernel and the fused decode step. The
 // selected blocks of a (sequence, kv head) group are cut into 16-token chunks
-// and the chunks into num_splits contiguous ranges (splits); wave w of a
-// split's workgroup of NW waves takes chunks c0 + w, c0 + w + NW, ... of its
-// range, with kDepth chunks' loads in flight per wave while one is consumed.
+// and the chunks are dealt to num_splits splits one by one (split s takes
+// chunk slots s, s + S, ...); wave w of a split's workgroup of NW waves takes
+// the split's slots w, w + NW, ..., with kDepth chunks' loads in flight per
+// wave while one is consumed.
 //
 // Lane layout inside a wave: lane = 16 * r + c. Lane (r, c) owns dims
 // [8c, 8c + 8) of the chunk's rows r, r + 4, r + 8, r + 12, for K and for V,
@@ -13,9 +14,10 @@
 // q.k partial sums use v_dot2 on bf16 pairs, then a 16-lane DPP reduction.
 // Each row group r keeps its own online-softmax state (running max m, sum l,
 // accumulator over its 8 dims) for the g query heads of the group, in the
-// log2 domain; the four row groups, then the waves are merged by log-sum-exp
-// inside the workgroup, and the last workgroup of each group to finish
-// merges the splits (a single split writes the output directly).
+// log2 domain; the row groups and waves of a workgroup are merged by
+// log-sum-exp through LDS, and the split holding the last ticket of its group
+// merges the others' published partials with its own (a single split writes
+// the output directly).
 #pragma once
 
 #include <utility>
@@ -179,14 +181,16 @@ __device__ __forceinline__ void consume_chunk(const Chunk& ch, int t0, int r, in
 // Merge of a group's S split partials by its last workgroup (Alg. 2,
 // "Combine"), in one round of loads: every thread issues its lse loads (kept
 // in LDS) and its 128-bit partial loads together, all with agent scope
-// (buffer loads with the sc1 policy, bounds-checked by the buffer size).
-// Float4 column u of head r = u / 32 gets T = NT / (32 G) threads, each
-// summing splits ph, ph + T, ...; the T sums are added through LDS.
+// (buffer loads with the sc1 policy, bounds-checked by the buffer size). The
+// merging workgroup's own split (`own`) never went to memory: its partial and
+// lse are read from LDS. Float4 column u of head r = u / 32 gets
+// T = NT / (32 G) threads, each summing splits ph, ph + T, ...; the T sums
+// are added through LDS.
 constexpr int kTailBatch = 16;    // partial loads per thread per round
 
 template <int G, int NT, bool kOpaque>
-__device__ void merge_tail(const DecodeArgs& a, size_t grp, int S, size_t ob, float* s_lse,
-                           f4_t* s_red) {
+__device__ void merge_tail(const DecodeArgs& a, size_t grp, int S, int own, size_t ob,
+                           const float* own_o, const float* own_l, float* s_lse, f4_t* s_red) {
   constexpr int U = G * (kHeadDim / 4);
   constexpr int T = U >= NT ? 1 : NT / U;
   constexpr int kLse = (kMaxSplits * G + NT - 1) / NT;
@@ -199,49 +203,62 @@ __device__ void merge_tail(const DecodeArgs& a, size_t grp, int S, size_t ob, fl
   const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<float*>(po), (short)0, S * G * kHeadDim * 4, kBufWord3);
 
-  float lreg[kLse];
+  // Every load is unconditional, so no pending load shares a register with
+  // an LDS read on another path (which would serialise the loads): offsets
+  // past the buffer read 0 through its range check, and the own split's slot
+  // (stale) is replaced by its LDS copy once the values are used.
+  constexpr int kOut = 0x7fffffff;  // an offset past every buffer
+  uint32_t lraw[kLse];
 #pragma unroll
   for (int j = 0; j < kLse; ++j) {
     const int i = tid + NT * j;
-    lreg[j] = i < S * G ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rl, i * 4, 0, kSc1))
-                        : ninf;
+    lraw[j] = __builtin_amdgcn_raw_buffer_load_b32(rl, i < S * G ? i * 4 : kOut, 0, kSc1);
   }
   const bool active = tid < U * T;
   const int u = tid % U, ph = tid / U, r = u / (kHeadDim / 4), c4 = u % (kHeadDim / 4);
   const int nb = (S + T * kTailBatch - 1) / (T * kTailBatch);
+  const f4_t own_v = *reinterpret_cast<const f4_t*>(own_o + r * kHeadDim + 4 * c4);
   f4_t part[kTailBatch];
   auto issue = [&](int b) {
 #pragma unroll
     for (int k = 0; k < kTailBatch; ++k) {
       const int sp = b * T * kTailBatch + k * T + ph;
       // The builtins return integer types: reinterpret the bits, never convert.
-      part[k] = (active && sp < S)
-                    ? __builtin_bit_cast(f4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                                   ro, ((sp * G + r) * kHeadDim + 4 * c4) * 4, 0, kSc1))
-                    : f4_t{0.f, 0.f, 0.f, 0.f};
+      part[k] = __builtin_bit_cast(f4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                    ro, active && sp < S ? ((sp * G + r) * kHeadDim + 4 * c4) * 4 : kOut, 0, kSc1));
     }
   };
   issue(0);
-  // Every split has taken its ticket: reset the counter for the next call.
-  // The store goes out after the loads (a wave's memory counter drains in
-  // issue order), so it does not delay their use.
-  if (tid == 0) __hip_atomic_store(a.counters + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  float lreg[kLse];
 #pragma unroll
   for (int j = 0; j < kLse; ++j) {
     const int i = tid + NT * j;
-    if (i < S * G) s_lse[i] = lreg[j];
+    lreg[j] = i >= S * G ? ninf : i / G == own ? own_l[i % G] : __builtin_bit_cast(float, lraw[j]);
+  }
+  // lse of split sp, head h at s_lse[h * SP + sp] (SP = S rounded up to 4,
+  // padded with -inf), so each head's values are contiguous: after one
+  // barrier every thread reads its head's S values (broadcast 16-byte reads)
+  // and forms the weights itself, with no further barrier.
+  const int SP = (S + 3) & ~3;
+#pragma unroll
+  for (int j = 0; j < kLse; ++j) {
+    const int i = tid + NT * j;
+    if (i < S * G) s_lse[(i % G) * SP + i / G] = lreg[j];
+    else if (i < SP * G) s_lse[(i % G) * SP + i / G] = ninf;
   }
   lds_sync();
-  float mx = ninf, wsum = 0.f;
-  if (active) {
-    for (int sp = 0; sp < S; ++sp) mx = fmaxf(mx, s_lse[sp * G + r]);
-    if (mx != ninf)
-      for (int sp = 0; sp < S; ++sp) {
-        const float l = s_lse[sp * G + r];
-        wsum += l == ninf ? 0.f : fast_exp2(l - mx);
-      }
+  const f4_t* lh = reinterpret_cast<const f4_t*>(s_lse + r * SP);
+  float mx = ninf;
+  for (int v = 0; v < SP / 4; ++v) {
+    const f4_t x = lh[v];
+    mx = fmaxf(fmaxf(mx, fmaxf(x.x, x.y)), fmaxf(x.z, x.w));
   }
-  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+  float wsum = 0.f;
+  if (mx != ninf)
+    for (int v = 0; v < SP / 4; ++v) {
+      const f4_t x = lh[v];
+      wsum += fast_exp2(x.x - mx) + fast_exp2(x.y - mx) + fast_exp2(x.z - mx) + fast_exp2(x.w - mx);
+    }
   f4_t acc = {0.f, 0.f, 0.f, 0.f};
   for (int b = 0; b < nb; ++b) {
     if (b > 0) issue(b);
@@ -249,12 +266,12 @@ __device__ void merge_tail(const DecodeArgs& a, size_t grp, int S, size_t ob, fl
     for (int k = 0; k < kTailBatch; ++k) {
       const int sp = b * T * kTailBatch + k * T + ph;
       if (active && sp < S) {
-        const float l = s_lse[sp * G + r];
-        const float wgt = l == ninf ? 0.f : fast_exp2(l - mx) * inv;
-        acc += wgt * part[k];
+        const float l = s_lse[r * SP + sp];
+        acc += (l == ninf ? 0.f : fast_exp2(l - mx)) * (sp == own ? own_v : part[k]);
       }
     }
   }
+  acc *= wsum > 0.f ? 1.f / wsum : 0.f;
   if constexpr (T > 1) {
     s_red[tid] = acc;
     lds_sync();
@@ -267,20 +284,42 @@ __device__ void merge_tail(const DecodeArgs& a, size_t grp, int S, size_t ob, fl
     *reinterpret_cast<f4_t*>(a.out + (ob + r) * kHeadDim + 4 * c4) = acc;
     if (c4 == 0 && a.lse) a.lse[ob + r] = wsum > 0.f ? (mx + fast_log2(wsum)) * kLn2 : ninf;
   }
+  // Every other split has published (its flag was seen): the flags and the
+  // ticket counter return to zero for the next call.
+  if (tid < S && tid != own)
+    __hip_atomic_store(a.flags + grp * S + tid, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (tid == 0) __hip_atomic_store(a.counters + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // LDS of one split: per-wave softmax states for the wave merge, the staged
 // chunk list, and the merge of the splits.
+// Row-group states kept for the merge of the waves: all four row groups of
+// each wave (RG = 4) or, for 8-wave workgroups, whose LDS is shared with the
+// selection, the two pairs left by one lane swap (RG = 2).
+template <int NW>
+constexpr int kRowGroups = NW <= 4 ? 4 : 2;
+
+// Entry e = w RG + r holds accumulator racc[w][r][h][:] and, per head h, its
+// softmax reference rm[h][e] and sum rl[h][e] (contiguous per head).
 template <int G, int NW>
 struct DecodeLds {
-  float acc[NW][G][kHeadDim];
-  float m[NW][G], l[NW][G];
+  static constexpr int RG = kRowGroups<NW>;
+  __attribute__((aligned(16))) float racc[NW][RG][G][kHeadDim];
+  __attribute__((aligned(16))) float rm[G][NW * RG];
+  __attribute__((aligned(16))) float rl[G][NW * RG];
+  __attribute__((aligned(16))) float own_o[G * kHeadDim];   // the merging split's own partial
+  float own_l[G];
   int tok[kIdxBatch];
   int row[kIdxBatch];
-  float w[kMaxSplits * G];
+  __attribute__((aligned(16))) float w[kMaxSplits * G];
   f4_t red[64 * NW];
   uint32_t ticket;
 };
+
+// Bound of the last split's wait for the other splits' flags (each poll
+// sleeps about 64 cycles): the splits it waits for have taken their tickets
+// and are finishing, so the bound is only a guard.
+constexpr uint32_t kFlagSpins = 1u << 22;
 
 template <bool kCoherent>
 __device__ __forceinline__ int ld_i32(const int32_t* p) {
@@ -316,16 +355,14 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int S = a.num_splits;
   const size_t grp = (size_t)bb * a.c.kv_heads + hk;
-  // The group's n_cap * CPB chunk slots are dealt to the splits in runs of
-  // NW consecutive slots (run k of split s holds slots (k S + s) NW ..
-  // + NW - 1), so a workgroup's waves read neighbouring chunks (one
-  // contiguous run of K and V for large blocks and dense decoding), the id
-  // loads do not wait for the count n, and any n leaves the splits balanced
-  // to one run. Slots at or past n * CPB are skipped.
-  auto slot_of = [&](int i) { return ((i / NW) * S + split) * NW + i % NW; };
+  // The group's n_cap * CPB chunk slots are dealt to the splits one by one
+  // (split s holds slots s, s + S, s + 2 S, ...), so the id loads do not wait
+  // for the count n and any n leaves the splits balanced to one chunk (runs
+  // of several slots per split left up to a run's difference, 14 % of a
+  // split at 256K). Slots at or past n * CPB are skipped.
+  auto slot_of = [&](int i) { return i * S + split; };
   auto count_below = [&](int T) {  // this split's slots below slot T
-    const int full = T / (S * NW), rem = T - full * S * NW;
-    return full * NW + min(max(rem - split * NW, 0), NW);
+    return T > split ? (T - split + S - 1) / S : 0;
   };
   const int slots = count_below(a.n_cap * CPB);
   const int r = lane >> 4, c = lane & 15, col = c * 8;
@@ -488,81 +525,153 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
     cb += kIdxBatch;
   } while (cb < valid);
 
+  // Tail. With several splits, one thread takes the split's ticket first:
+  // its round trip overlaps the merge of the waves below. The ticket only
+  // orders the splits' ends; the split holding the last one waits for the
+  // others' ready flags (their partials are in memory then) and merges.
+  // Every K / V load of the loop has been consumed here; the compiler cannot
+  // see that (refills are conditional), so without this explicit wait it
+  // would place waits in the merge below that also cover the ticket.
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+  const bool single = S == 1;
+  uint32_t ticket = 0;
+  if (!single && tid == 0)
+    ticket = __hip_atomic_fetch_add(a.counters + grp, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
   // Per-head state of this lane's row group: head h lives in lane 16 r + h
-  // (a DPP row broadcast).
+  // (a DPP row broadcast). With RG = 2, row groups r and r + 2 (lanes l and
+  // l + 32) merge through one lane swap first. Every kept row-group state
+  // goes to LDS.
+  constexpr int RG = kRowGroups<NW>;
+  constexpr int NE = NW * RG;
   float m_[G], l_[G];
   [&]<int... H>(std::integer_sequence<int, H...>) {
     ((m_[H] = dpp<kDppBcast0 + H>(st.m)), ...);
     ((l_[H] = dpp<kDppBcast0 + H>(st.l)), ...);
   }(std::make_integer_sequence<int, G>{});
-
-  // Merge the four row groups of the wave (lanes c, c+16, c+32, c+48).
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    const float mx = max_xor32(max_xor16(m_[h]));
-    const float w = (m_[h] == ninf) ? 0.f : fast_exp2(m_[h] - mx);
-    m_[h] = mx;
-    l_[h] = sum_xor32(sum_xor16(l_[h] * w));
-#pragma unroll
-    for (int d = 0; d < 8; ++d) acc[h][d] = sum_xor32(sum_xor16(acc[h][d] * w));
-  }
-  if (r == 0) {
+  if constexpr (RG == 2) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
+      const float mx = max_xor32(m_[h]);
+      const float w = (m_[h] == ninf) ? 0.f : fast_exp2(m_[h] - mx);
+      m_[h] = mx;
+      l_[h] = sum_xor32(l_[h] * w);
 #pragma unroll
-      for (int d = 0; d < 8; ++d) lds.acc[wave][h][col + d] = acc[h][d];
-      if (lane == 0) {
-        lds.m[wave][h] = m_[h];
-        lds.l[wave][h] = l_[h];
+      for (int d = 0; d < 8; ++d) acc[h][d] = sum_xor32(acc[h][d] * w);
+    }
+  }
+  if (r < RG) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      f4_t* dst = reinterpret_cast<f4_t*>(&lds.racc[wave][r][h][col]);
+      dst[0] = f4_t{acc[h][0], acc[h][1], acc[h][2], acc[h][3]};
+      dst[1] = f4_t{acc[h][4], acc[h][5], acc[h][6], acc[h][7]};
+    }
+    if (c == 0) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        lds.rm[h][wave * RG + r] = m_[h];
+        lds.rl[h][wave * RG + r] = l_[h];
       }
     }
   }
   lds_sync();
 
-  // Merge the waves; store this split's normalised partial and its lse (log2
-  // domain), or the final output directly when there is a single split.
-  const bool single = S == 1;
-  const size_t ob = (size_t)bb * a.q_heads + (size_t)hk * G;
-  float* po = a.part_o + (grp * S + split) * (size_t)(G * kHeadDim);
-  float* pl = a.part_lse + (grp * S + split) * (size_t)G;
-  for (int o = tid_of<kCoherent>(); o < G * kHeadDim; o += 64 * NW) {
-    const int h = o / kHeadDim, d = o % kHeadDim;
-    float mx = ninf;
+  // Merge the NE row-group states: this split's normalised partial and its
+  // lse (log2 domain) for items it = tid + k NT of two dims each (head
+  // it / 64, dims 2 (it % 64) ..). A wave's items share one head, so the
+  // per-head references and sums are broadcast vector reads.
+  constexpr int NT2 = 64 * NW;
+  constexpr int kItems = (G * 64 + NT2 - 1) / NT2;
+  f2_t val[kItems];
+  float lg[kItems];
 #pragma unroll
-    for (int w = 0; w < NW; ++w) mx = fmaxf(mx, lds.m[w][h]);
-    float lsum = 0.f, x = 0.f;
+  for (int k = 0; k < kItems; ++k) {
+    const int it = tid + k * NT2;
+    val[k] = f2_t{0.f, 0.f};
+    lg[k] = ninf;
+    if (it < G * 64) {
+      const int h = it / 64, d = 2 * (it % 64);
+      float mv[NE], lv[NE];
 #pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      const float f = lds.m[w][h] == ninf ? 0.f : fast_exp2(lds.m[w][h] - mx);
-      lsum = fmaf(lds.l[w][h], f, lsum);
-      x = fmaf(lds.acc[w][h][d], f, x);
-    }
-    const bool any = lsum > 0.f;
-    const float val = any ? x / lsum : 0.f;
-    const float l2 = any ? mx + fast_log2(lsum) : ninf;
-    if (single) {
-      a.out[(ob + h) * kHeadDim + d] = val;
-      if (d == 0 && a.lse) a.lse[ob + h] = any ? l2 * kLn2 : ninf;
-    } else {
-      // Agent-scope stores write through to the level where every L2 slice
-      // sees them, so the partials need no cache writeback before the ticket.
-      __hip_atomic_store(po + o, val, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (d == 0) __hip_atomic_store(pl + h, l2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      for (int e = 0; e < NE; e += 4) {
+        const f4_t m4 = *reinterpret_cast<const f4_t*>(&lds.rm[h][e]);
+        const f4_t l4 = *reinterpret_cast<const f4_t*>(&lds.rl[h][e]);
+        mv[e] = m4.x; mv[e + 1] = m4.y; mv[e + 2] = m4.z; mv[e + 3] = m4.w;
+        lv[e] = l4.x; lv[e + 1] = l4.y; lv[e + 2] = l4.z; lv[e + 3] = l4.w;
+      }
+      float mx = ninf;
+#pragma unroll
+      for (int e = 0; e < NE; ++e) mx = fmaxf(mx, mv[e]);
+      float lsum = 0.f;
+      f2_t x = {0.f, 0.f};
+#pragma unroll
+      for (int e = 0; e < NE; ++e) {
+        const float f = mv[e] == ninf ? 0.f : fast_exp2(mv[e] - mx);
+        lsum = fmaf(lv[e], f, lsum);
+        x += f * *reinterpret_cast<const f2_t*>(&lds.racc[e / RG][e % RG][h][d]);
+      }
+      if (lsum > 0.f) {
+        val[k] = x * (1.f / lsum);
+        lg[k] = mx + fast_log2(lsum);
+      }
     }
   }
-  if (single) return true;
+  const size_t ob = (size_t)bb * a.q_heads + (size_t)hk * G;
+  if (single) {
+#pragma unroll
+    for (int k = 0; k < kItems; ++k) {
+      const int it = tid + k * NT2;
+      if (it < G * 64) {
+        *reinterpret_cast<f2_t*>(a.out + ob * kHeadDim + 2 * it) = val[k];
+        if (it % 64 == 0 && a.lse) a.lse[ob + it / 64] = lg[k] == ninf ? ninf : lg[k] * kLn2;
+      }
+    }
+    return true;
+  }
+  if (tid == 0) lds.ticket = ticket;
+  lds_sync();
+  if (lds.ticket != (uint32_t)(S - 1)) {
+    // Publish: agent-scope stores write through to the level every L2 slice
+    // reads (sc1), every thread waits for their acknowledgement, then one
+    // thread raises the split's ready flag.
+    float* po = a.part_o + (grp * S + split) * (size_t)(G * kHeadDim);
+    float* pl = a.part_lse + (grp * S + split) * (size_t)G;
+#pragma unroll
+    for (int k = 0; k < kItems; ++k) {
+      const int it = tid + k * NT2;
+      if (it < G * 64) {
+        __hip_atomic_store(po + 2 * it, val[k].x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(po + 2 * it + 1, val[k].y, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (it % 64 == 0) __hip_atomic_store(pl + it / 64, lg[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (tid == 0) __hip_atomic_store(a.flags + grp * S + split, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return false;
+  }
 
-  // Alg. 2, "Combine": the last workgroup of the group to finish merges the
-  // splits. Each workgroup waits until its partial stores are acknowledged,
-  // then takes a ticket; the last one reads every partial with agent-scope
-  // loads and resets the counter for the next call.
-  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  // Alg. 2, "Combine", in the split holding the last ticket: its own partial
+  // stays in LDS; every other split has taken its ticket and is publishing,
+  // so thread t < S waits for split t's flag (agent-scope loads), then the
+  // partials are read with agent-scope loads and merged.
+#pragma unroll
+  for (int k = 0; k < kItems; ++k) {
+    const int it = tid + k * NT2;
+    if (it < G * 64) {
+      *reinterpret_cast<f2_t*>(&lds.own_o[2 * it]) = val[k];
+      if (it % 64 == 0) lds.own_l[it / 64] = lg[k];
+    }
+  }
+  if (tid < S && tid != split) {
+    const uint32_t* fl = a.flags + grp * S + tid;
+    uint32_t spins = 0;
+    while (__hip_atomic_load(fl, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u && ++spins < kFlagSpins)
+      __builtin_amdgcn_s_sleep(1);
+  }
   __syncthreads();
-  if (tid_of<kCoherent>() == 0)
-    lds.ticket = __hip_atomic_fetch_add(a.counters + grp, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  __syncthreads();
-  if (lds.ticket != (uint32_t)(S - 1)) return false;
-  merge_tail<G, 64 * NW, kCoherent>(a, grp, S, ob, lds.w, lds.red);
+  merge_tail<G, 64 * NW, kCoherent>(a, grp, S, split, ob, lds.own_o, lds.own_l, lds.w, lds.red);
   return true;
 }
 

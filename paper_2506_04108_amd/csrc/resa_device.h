@@ -12,6 +12,9 @@ constexpr int kChunk = 16;  // tokens handled per decode step of a wave
 constexpr int kMaxGroup = 8;  // query heads per kv head (RESA_MAX_GROUP)
 constexpr int kBufWord3 = 0x00020000;  // raw buffer resource word 3: 32-bit data format
 constexpr int kSc1 = 16;              // buffer cache policy: agent-scope coherent
+// s_waitcnt immediate that waits for every outstanding vector memory
+// operation (vmcnt 0) and leaves expcnt and lgkmcnt alone (gfx9 encoding).
+constexpr int kWaitVmcnt0 = 0x0F70;
 
 // A 16-byte vector: 8 bf16 values (one lane's share of a 256-byte key row).
 struct __attribute__((aligned(16))) U4 {
@@ -197,6 +200,7 @@ __device__ __forceinline__ uint32_t order_key(float f) {
 }
 
 typedef float f4_t __attribute__((ext_vector_type(4)));
+typedef float f2_t __attribute__((ext_vector_type(2)));
 
 // Log-sum-exp merge of split partials (Alg. 2, "Combine"), for one workgroup.
 //

@@ -87,7 +87,8 @@ struct DecodeArgs {
   float* lse;                  // [B, Hq] or null
   float* part_o;               // [B, Hkv, S, G, D]
   float* part_lse;             // [B, Hkv, S, G]
-  uint32_t* counters;          // [B, Hkv], zero between calls
+  uint32_t* counters;          // [B, Hkv] split tickets, zero between calls
+  uint32_t* flags;             // [B, Hkv, S] split partial published, zero between calls
   const uint16_t* k_new;       // fused step: [B, Hkv, D] token appended in the same launch
   const uint16_t* v_new;
 };
