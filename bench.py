@@ -324,7 +324,7 @@ def measure(args, w, dense: bool) -> dict:
         else:
             qf, kf, vf = rect_inputs[li, s + 1]
             check(lb.resa_dense_rectify(d, qf.data_ptr(), kf.data_ptr(), vf.data_ptr(), Hq, f,
-                                        ly["lens"].data_ptr(), Lcur + 1, sm, rout.data_ptr(), None, 1,
+                                        ly["lens"].data_ptr(), None, Lcur + 1, sm, rout.data_ptr(), None, 1,
                                         ws_rec.data_ptr(), ws_rec.numel(), launch_stream[0]))
 
     def step(t):
@@ -463,7 +463,7 @@ def measure(args, w, dense: bool) -> dict:
                 qf, kf, vf = rin[li]
                 Lc = L0 + ly["steps"]
                 check(lb.resa_dense_rectify(C.byref(ly["desc"]), qf.data_ptr(), kf.data_ptr(),
-                                            vf.data_ptr(), Hq, f, ly["lens"].data_ptr(), Lc, sm,
+                                            vf.data_ptr(), Hq, f, ly["lens"].data_ptr(), None, Lc, sm,
                                             rout.data_ptr(), None, 1, ws_rec.data_ptr(),
                                             ws_rec.numel(), sptr))
             for li in range(nlay):  # untimed warm-up call per layer

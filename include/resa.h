@@ -312,7 +312,9 @@ size_t resa_rectify_workspace_size(int32_t batch, int32_t num_kv_heads,
 
 /*
  * Dense rectification (Sec. 2.2; Alg. 1, "DenseForward" every f steps) of
- * one layer. For every sequence b with length L = seq_lens[b] >= f:
+ * one layer. For every sequence b with length L = seq_lens[b] >= f that the
+ * call covers (seq_mask == NULL: every sequence; else those with
+ * seq_mask[b] != 0):
  *   1. rows [L - f, L) of k and v become k_f[b], v_f[b]
  *      (bf16 [batch, num_kv_heads, f, head_dim]);
  *   2. query row r of q_f[b, h] (bf16 [batch, num_q_heads, f, head_dim]) sits
@@ -325,6 +327,13 @@ size_t resa_rectify_workspace_size(int32_t batch, int32_t num_kv_heads,
  * max_seq_len bounds every seq_lens[b] (host side, for launch sizing). A
  * sequence with seq_lens[b] < f is left untouched and its out rows are 0 (lse
  * -inf). The workspace holds split partials and needs no initialisation.
+ * Per-request phases (Sec. 2.2, compatibility with serving systems: each
+ * request is rectified every f of its own steps, so in a continuous batch
+ * requests reach their rectification at different steps): seq_mask (device
+ * int32 [batch], or NULL) selects the sequences this call rectifies. A
+ * sequence with seq_mask[b] == 0 is not touched at all: its cache rows,
+ * summaries, out and lse rows keep their contents, and its q_f / k_f / v_f
+ * rows are not read.
  * Value range: any finite bf16 V gives a finite out. P . V runs on fp16
  * matrix cores with P in [0, 2^8]; V enters at its own scale (exact for
  * |v| in 2^-14 .. 65280, fp16 subnormal spacing 2^-24 below), and a head
@@ -342,8 +351,8 @@ size_t resa_rectify_workspace_size(int32_t batch, int32_t num_kv_heads,
  */
 int resa_dense_rectify(const resa_kv_cache_t* c, const void* q_f, const void* k_f,
                        const void* v_f, int32_t num_q_heads, int32_t f,
-                       const int32_t* seq_lens, int32_t max_seq_len, float sm_scale,
-                       float* out, float* lse, int32_t refresh_summaries,
+                       const int32_t* seq_lens, const int32_t* seq_mask, int32_t max_seq_len,
+                       float sm_scale, float* out, float* lse, int32_t refresh_summaries,
                        void* workspace, size_t workspace_bytes, void* stream);
 
 /* Zero-fills a workspace with a kernel (safe under stream capture). */

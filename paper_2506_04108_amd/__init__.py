@@ -343,14 +343,18 @@ def dense_rectify(cache: KVCache, q_f: torch.Tensor, k_f: torch.Tensor, v_f: tor
                   seq_lens: torch.Tensor, max_seq_len: int, sm_scale: float | None = None,
                   out: torch.Tensor | None = None, lse: torch.Tensor | None = None,
                   with_lse: bool = True, refresh: bool = True, workspace: Workspace | None = None,
-                  stream=None):
-    """Sec. 2.2 rectification of the last f rows. Returns ``(out fp32 [B, Hq, f, 128], lse)``."""
+                  seq_mask: torch.Tensor | None = None, stream=None):
+    """Sec. 2.2 rectification of the last f rows. Returns ``(out fp32 [B, Hq, f, 128], lse)``.
+    ``seq_mask`` (int32 [B] on the device, or None for every sequence) selects the
+    sequences rectified by this call; the others are left untouched."""
     B, Hkv = cache.batch, cache.kv_heads
     hq, f = q_f.shape[1], q_f.shape[2]
     _need(q_f, "q_f", torch.bfloat16, (B, hq, f, HEAD_DIM))
     _need(k_f, "k_f", torch.bfloat16, (B, Hkv, f, HEAD_DIM))
     _need(v_f, "v_f", torch.bfloat16, (B, Hkv, f, HEAD_DIM))
     _need(seq_lens, "seq_lens", torch.int32, (B,))
+    if seq_mask is not None:
+        _need(seq_mask, "seq_mask", torch.int32, (B,))
     if sm_scale is None:
         sm_scale = 1.0 / math.sqrt(HEAD_DIM)
     if out is None:
@@ -364,7 +368,7 @@ def dense_rectify(cache: KVCache, q_f: torch.Tensor, k_f: torch.Tensor, v_f: tor
     ws = (workspace or Workspace(q_f.device)).get(ws_bytes)
     d = cache.desc()
     check(lib().resa_dense_rectify(C.byref(d), q_f.data_ptr(), k_f.data_ptr(), v_f.data_ptr(), hq, f,
-                                   seq_lens.data_ptr(), max_seq_len, float(sm_scale),
+                                   seq_lens.data_ptr(), _ptr(seq_mask), max_seq_len, float(sm_scale),
                                    out.data_ptr(), _ptr(lse), int(bool(refresh)), ws.data_ptr(),
                                    ws.numel(), _stream(stream)))
     return out, lse

@@ -61,8 +61,8 @@ SIGNATURES = {
     "resa_decode_step": (C.c_int, [_CACHE, _P, _P, _P, _I, _P, _I, C.POINTER(SelectParams), _P, _P, _I,
                                    _I, _F, _P, _P, _P, _Z, _P]),
     "resa_rectify_workspace_size": (_Z, [_I, _I, _I, _I, _I]),
-    "resa_dense_rectify": (C.c_int, [_CACHE, _P, _P, _P, _I, _I, _P, _I, _F, _P, _P, _I, _P, _Z,
-                                     _P]),
+    "resa_dense_rectify": (C.c_int, [_CACHE, _P, _P, _P, _I, _I, _P, _P, _I, _F, _P, _P, _I, _P,
+                                     _Z, _P]),
     "resa_workspace_clear": (C.c_int, [_P, _Z, _P]),
     "resa_stream_read": (C.c_int, [_P, _Z, _P, C.c_uint32, _I, _P]),
 }

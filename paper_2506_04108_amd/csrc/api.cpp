@@ -659,9 +659,9 @@ size_t resa_rectify_workspace_size(int32_t batch, int32_t num_kv_heads, int32_t 
 
 int resa_dense_rectify(const resa_kv_cache_t* c, const void* q_f, const void* k_f,
                        const void* v_f, int32_t num_q_heads, int32_t f, const int32_t* seq_lens,
-                       int32_t max_seq_len, float sm_scale, float* out, float* lse,
-                       int32_t refresh_summaries, void* workspace, size_t workspace_bytes,
-                       void* stream) {
+                       const int32_t* seq_mask, int32_t max_seq_len, float sm_scale, float* out,
+                       float* lse, int32_t refresh_summaries, void* workspace,
+                       size_t workspace_bytes, void* stream) {
   if (int e = check_cache(c)) return e;
   int32_t group = 0;
   if (int e = check_heads(c, num_q_heads, &group)) return e;
@@ -669,6 +669,8 @@ int resa_dense_rectify(const resa_kv_cache_t* c, const void* q_f, const void* k_
   RESA_CHECK_PTR(k_f, 16);
   RESA_CHECK_PTR(v_f, 16);
   RESA_CHECK_PTR(seq_lens, 4);
+  if (seq_mask != nullptr && !aligned(seq_mask, 4))
+    return fail(RESA_ERR_INVALID_ARG, "seq_mask is not 4-byte aligned");
   RESA_CHECK_PTR(out, 16);
   if (lse != nullptr && !aligned(lse, 4)) return fail(RESA_ERR_INVALID_ARG, "lse is not 4-byte aligned");
   if (f < 1 || f > RESA_MAX_RECTIFY_ROWS)
@@ -702,6 +704,7 @@ int resa_dense_rectify(const resa_kv_cache_t* c, const void* q_f, const void* k_
   a.part_lse = reinterpret_cast<float*>(ws + lay.lse);
   a.part_o = reinterpret_cast<float*>(ws + lay.o);
   a.refresh = refresh_summaries ? 1 : 0;
+  a.seq_mask = seq_mask;
   hipError_t e = resa::launch_rectify(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "resa_dense_rectify launch");
   return ok();

@@ -88,6 +88,7 @@ __device__ __forceinline__ f16x4_t lds_read_tr(const uint16_t* p) {
 __global__ __launch_bounds__(256) void k_rectify_rows(RectifyArgs a) {
   const int grp = blockIdx.y;
   const int bb = grp / a.c.kv_heads;
+  if (a.seq_mask != nullptr && a.seq_mask[bb] == 0) return;
   const int L = a.seq_lens[bb];
   if (L < a.f || L > a.c.capacity) return;
   uint16_t* k = const_cast<uint16_t*>(a.c.k);
@@ -123,6 +124,9 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int split = blockIdx.x, qblk = blockIdx.y, grp = blockIdx.z;
   const int bb = grp / a.c.kv_heads, hk = grp % a.c.kv_heads;
+  // A sequence left out of this call: nothing is read or written (uniform
+  // across the workgroup, before any barrier).
+  if (a.seq_mask != nullptr && a.seq_mask[bb] == 0) return;
   const int G = a.group, f = a.f, R = G * f;
   const int S = a.num_splits;
   const int L = a.seq_lens[bb];
@@ -460,6 +464,7 @@ __global__ __launch_bounds__(256) void k_rectify_combine(RectifyArgs a) {
   __shared__ f4_t s_red[256];
   const int grp = blockIdx.y;
   const int bb = grp / a.c.kv_heads, hk = grp % a.c.kv_heads;
+  if (a.seq_mask != nullptr && a.seq_mask[bb] == 0) return;
   const int G = a.group, f = a.f, R = G * f, S = a.num_splits;
   const int rho0 = blockIdx.x * kCombineRows;
   const int rows = min(kCombineRows, R - rho0);
@@ -501,7 +506,7 @@ hipError_t launch_rectify(const RectifyArgs& a, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (a.refresh) {
-    e = launch_summarize_tail(a.c, a.seq_lens, a.f, stream);
+    e = launch_summarize_tail(a.c, a.seq_lens, a.f, a.seq_mask, stream);
     if (e != hipSuccess) return e;
   }
   const int32_t nq = rectify_num_qblocks(a.group, a.f);

@@ -119,13 +119,14 @@ struct RectifyArgs {
   float* part_o;               // [B, Hkv, S, G*f, D]
   float* part_lse;             // [B, Hkv, S, G*f]
   int32_t refresh;
+  const int32_t* seq_mask;     // [B]: sequences with 0 are left untouched (null: every sequence)
 };
 
 // Launchers: enqueue on `stream`; return the hipError_t of the launch.
 hipError_t launch_summarize(const CacheArgs& c, const int32_t* seq_lens, int32_t blk_begin,
                             int32_t blk_end, hipStream_t stream);
 hipError_t launch_summarize_tail(const CacheArgs& c, const int32_t* seq_lens, int32_t f,
-                                 hipStream_t stream);
+                                 const int32_t* seq_mask, hipStream_t stream);
 hipError_t launch_append(const CacheArgs& c, const uint16_t* k_new, const uint16_t* v_new,
                          int32_t* seq_lens, hipStream_t stream);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);

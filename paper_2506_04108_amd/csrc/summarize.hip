@@ -11,13 +11,17 @@ namespace {
 // so each wave-wide load covers four whole 256-byte rows (1 KiB contiguous).
 //
 // With rel_f > 0 the range is per sequence: blocks floor((L - rel_f) / b) ..
-// M - 1, i.e. every block holding one of the last rel_f rows (rectify refresh).
+// M - 1, i.e. every block holding one of the last rel_f rows (rectify
+// refresh); a sequence whose seq_mask entry is 0 is skipped (seq_mask may be
+// null: every sequence).
 template <int BS>
 __global__ __launch_bounds__(256) void k_summarize(CacheArgs c, const int32_t* __restrict__ seq_lens,
-                                                   int32_t blk_begin, int32_t blk_end, int32_t rel_f) {
+                                                   int32_t blk_begin, int32_t blk_end, int32_t rel_f,
+                                                   const int32_t* __restrict__ seq_mask) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int hk = blockIdx.y, bb = blockIdx.z;
+  if (seq_mask != nullptr && seq_mask[bb] == 0) return;
   const int L = seq_lens[bb];
   if (rel_f > 0) {
     if (L < rel_f) return;
@@ -124,13 +128,14 @@ __global__ void k_clear(uint8_t* p, size_t bytes) {
 }  // namespace
 
 static hipError_t summarize_grid(const CacheArgs& c, const int32_t* seq_lens, int32_t blk_begin,
-                                 int32_t blk_end, int32_t rel_f, int32_t nblk, hipStream_t stream) {
+                                 int32_t blk_end, int32_t rel_f, const int32_t* seq_mask, int32_t nblk,
+                                 hipStream_t stream) {
   if (nblk <= 0) return hipSuccess;
   dim3 grid((nblk + 3) / 4, c.kv_heads, c.batch);
   switch (c.block_size) {
-    case 16: hipLaunchKernelGGL(k_summarize<16>, grid, dim3(256), 0, stream, c, seq_lens, blk_begin, blk_end, rel_f); break;
-    case 32: hipLaunchKernelGGL(k_summarize<32>, grid, dim3(256), 0, stream, c, seq_lens, blk_begin, blk_end, rel_f); break;
-    case 64: hipLaunchKernelGGL(k_summarize<64>, grid, dim3(256), 0, stream, c, seq_lens, blk_begin, blk_end, rel_f); break;
+    case 16: hipLaunchKernelGGL(k_summarize<16>, grid, dim3(256), 0, stream, c, seq_lens, blk_begin, blk_end, rel_f, seq_mask); break;
+    case 32: hipLaunchKernelGGL(k_summarize<32>, grid, dim3(256), 0, stream, c, seq_lens, blk_begin, blk_end, rel_f, seq_mask); break;
+    case 64: hipLaunchKernelGGL(k_summarize<64>, grid, dim3(256), 0, stream, c, seq_lens, blk_begin, blk_end, rel_f, seq_mask); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -139,14 +144,14 @@ static hipError_t summarize_grid(const CacheArgs& c, const int32_t* seq_lens, in
 hipError_t launch_summarize(const CacheArgs& c, const int32_t* seq_lens, int32_t blk_begin,
                             int32_t blk_end, hipStream_t stream) {
   const int32_t last = blk_end < 0 ? c.max_blocks : blk_end;
-  return summarize_grid(c, seq_lens, blk_begin, blk_end, 0, last - blk_begin, stream);
+  return summarize_grid(c, seq_lens, blk_begin, blk_end, 0, nullptr, last - blk_begin, stream);
 }
 
 hipError_t launch_summarize_tail(const CacheArgs& c, const int32_t* seq_lens, int32_t f,
-                                 hipStream_t stream) {
+                                 const int32_t* seq_mask, hipStream_t stream) {
   // Rows [L - f, L) touch at most ceil(f / b) + 1 blocks.
   const int32_t nblk = (f + c.block_size - 1) / c.block_size + 1;
-  return summarize_grid(c, seq_lens, 0, -1, f, nblk, stream);
+  return summarize_grid(c, seq_lens, 0, -1, f, seq_mask, nblk, stream);
 }
 
 hipError_t launch_append(const CacheArgs& c, const uint16_t* k_new, const uint16_t* v_new,

@@ -164,8 +164,8 @@ def test_decode_validation():
 
 
 def rectify(**kw):
-    a = dict(c=C.byref(cache()), q=FAKE, k=FAKE, v=FAKE, hq=8, f=16, seq=FAKE, mx=1000, sc=0.088,
-             out=FAKE, lse=None, ref=1, ws=FAKE, wsb=16, st=None)
+    a = dict(c=C.byref(cache()), q=FAKE, k=FAKE, v=FAKE, hq=8, f=16, seq=FAKE, mask=None, mx=1000,
+             sc=0.088, out=FAKE, lse=None, ref=1, ws=FAKE, wsb=16, st=None)
     a.update(kw)
     return L.lib().resa_dense_rectify(*a.values())
 
@@ -176,7 +176,9 @@ def test_rectify_validation():
     expect(rectify(mx=8), 1, "max_seq_len")
     expect(rectify(mx=4096), 1, "max_seq_len")
     expect(rectify(k=None), 1, "k_f")
+    expect(rectify(mask=FAKE + 2), 1, "seq_mask")
     expect(rectify(), 3, "rectify workspace")
+    expect(rectify(mask=FAKE), 3, "rectify workspace")
 
 
 def test_workspace_sizes():

@@ -109,3 +109,95 @@ def test_paged_prefill():
     torch.cuda.synchronize()
     assert torch.equal(i1, i2) and torch.equal(o1, o2)
     _same_cache(c1, c2, [701, 701])
+
+
+# ------------------------------------------------------- per-request rectify
+
+@pytest.mark.parametrize("paged", [False, True])
+def test_rectify_per_request_phases(paged):
+    """Continuous batching (Sec. 2.2: rectification is compatible with serving
+    systems): a ragged batch decodes step by step and each request is
+    rectified every f of its own steps, at its own phase, through the
+    seq_mask of resa_dense_rectify. Checked against the oracle per request
+    (decode within the near-tie rule and 2e-3, rectified rows within 2e-3,
+    caches and summaries equal); sequences left out of a rectification keep
+    their cache rows, summaries and out rows bit for bit."""
+    import oracle as O
+    from oracle.compare import check_selection, max_abs_err
+    g, b, f, steps = 4, 16, 12, 30
+    w = W.LONG_64K.with_(batch=3, num_q_heads=2 * g, num_kv_heads=2, seq_len=700, min_tokens=64,
+                         seed_tag="perreq")
+    cap = 768
+    lens = [700, 455, 233]
+    phase = [0, 5, 9]           # request i rectifies when (step + phase[i]) % f == f - 1
+    K, V = W.kv_cache(w, capacity=cap)
+    if paged:
+        cache = make_paged_cache(K, V, b, [x + steps for x in lens], seed=3, sentinel=False)
+    else:
+        cache = make_cache(K, V, b, sentinel=False)
+    lt = i32(lens)
+    R.block_summarize(cache, lt)
+    st = O.DecodeState(O.bf16_to_f64(K), O.bf16_to_f64(V), lens, b)
+    sm = w.sm_scale
+    rect_done = [0, 0, 0]
+    swaps = 0
+    for step in range(steps):
+        kn, vn = W.decode_kv(w, step)
+        q = W.decode_query(w, step)
+        idx, ns = R.append_select(cache, up(kn), up(vn), up(q), lt, max(st.L), w.sparsity,
+                                  w.min_blocks, 1)
+        st.append(O.bf16_to_f64(kn), O.bf16_to_f64(vn))
+        out, _ = R.sparse_decode(cache, up(q), lt, idx, ns)
+        rs, ri, rn = st.select(O.bf16_to_f64(q), w.sparsity, w.min_blocks, 1)
+        ro, _ = st.attend(O.bf16_to_f64(q), ri, sm)
+        gi, gn, go = idx.cpu().numpy(), ns.cpu().numpy(), out.cpu().numpy()
+        for bi in range(3):
+            for hi in range(2):
+                heads = slice(g * hi, g * hi + g)
+                s = check_selection(gi[bi, hi, :gn[bi, hi]], ri[bi, hi], rs[bi, hi], rn[bi, hi], 1)
+                swaps += s
+                want = ro[bi, heads] if s == 0 else O.sparse_attend(
+                    O.bf16_to_f64(q)[bi, heads], st.K[bi, hi], st.V[bi, hi], st.L[bi],
+                    gi[bi, hi, :gn[bi, hi]], b, sm)[0]
+                assert max_abs_err(go[bi, heads], want) <= 2e-3
+        due = [(step + phase[i]) % f == f - 1 for i in range(3)]
+        if not any(due):
+            continue
+        # Re-encoded rows of every sequence's last f cache rows (exact bf16
+        # values held by the oracle); only the due sequences' rows may be read.
+        bits = lambda x: W.f32_to_bf16_bits(x.astype(np.float32))
+        lastk = np.stack([bits(st.K[i, :, st.L[i] - f:st.L[i]]) for i in range(3)])
+        lastv = np.stack([bits(st.V[i, :, st.L[i] - f:st.L[i]]) for i in range(3)])
+        qf, kf, vf = W.rectify_inputs(w, 100 + step, lastk, lastv, f)
+        mask = i32([int(x) for x in due])
+        before_k = (unpage(cache, st.L)[0] if paged else down(cache.k)).copy()
+        before_min, before_max = down(cache.kmin), down(cache.kmax)
+        rout = torch.full((3, 2 * g, f, 128), float("nan"), dtype=torch.float32, device=lt.device)
+        rlse = torch.full((3, 2 * g, f), float("nan"), dtype=torch.float32, device=lt.device)
+        R.dense_rectify(cache, up(qf), up(kf), up(vf), lt, max(st.L), out=rout, lse=rlse, seq_mask=mask)
+        torch.cuda.synchronize()
+        go, gl = rout.cpu().numpy(), rlse.cpu().numpy()
+        after_k = unpage(cache, st.L)[0] if paged else down(cache.k)
+        qg = O.split_heads(O.bf16_to_f64(qf), 2)
+        for bi in range(3):
+            L = st.L[bi]
+            if not due[bi]:
+                assert np.all(np.isnan(go[bi])) and np.all(np.isnan(gl[bi])), "out rows written"
+                assert np.array_equal(after_k[bi, :, :L], before_k[bi, :, :L])
+                assert np.array_equal(down(cache.kmin)[bi], before_min[bi])
+                assert np.array_equal(down(cache.kmax)[bi], before_max[bi])
+                continue
+            rect_done[bi] += 1
+            for hi in range(2):
+                ro_, rl_ = O.rectify_group(qg[bi, hi], st.K[bi, hi], st.V[bi, hi], st.kmin[bi, hi],
+                                           st.kmax[bi, hi], L, f, b, sm, O.bf16_to_f64(kf[bi, hi]),
+                                           O.bf16_to_f64(vf[bi, hi]))
+                heads = slice(g * hi, g * hi + g)
+                assert max_abs_err(go[bi, heads], ro_) <= 2e-3
+                assert max_abs_err(gl[bi, heads], rl_) <= 2e-3
+                assert np.array_equal(after_k[bi, hi, L - f:L], kf[bi, hi])
+                M = O.num_blocks(L, b)
+                assert np.array_equal(O.bf16_to_f64(down(cache.kmin)[bi, hi, :M]), st.kmin[bi, hi, :M])
+                assert np.array_equal(O.bf16_to_f64(down(cache.kmax)[bi, hi, :M]), st.kmax[bi, hi, :M])
+    assert rect_done == [2, 2, 3], rect_done   # every request rectified at its own steps
+    assert swaps <= 6
