@@ -205,6 +205,17 @@ int resa_append_select(const resa_kv_cache_t* c, const void* k_new, const void* 
                        float* scores_out, void* workspace, size_t workspace_bytes,
                        void* stream);
 
+/*
+ * Diagnostics: byte offset, in a resa_select_blocks / resa_append_select
+ * workspace (resa_select_stats_offset) or a resa_decode_step workspace
+ * (resa_step_stats_offset), of uint32 [batch, num_kv_heads] counters of the
+ * calls whose exact top-n finished on its in-window path (from the window
+ * hint's bits and lists, without reading every key). They only grow (from the
+ * zero-filled workspace) and never change a result.
+ */
+size_t resa_select_stats_offset(int32_t batch, int32_t num_kv_heads);
+size_t resa_step_stats_offset(int32_t batch, int32_t num_kv_heads);
+
 /* Split count resa_sparse_decode uses when num_splits = 0. */
 int32_t resa_decode_num_splits(int32_t batch, int32_t num_kv_heads, int32_t n_cap,
                                int32_t block_size);
@@ -298,6 +309,11 @@ size_t resa_step_workspace_size(int32_t batch, int32_t num_kv_heads, int32_t num
  * tickets and the selection hint: zero-fill it before its first use
  * (resa_workspace_clear); every call leaves the counters and flags at zero.
  * Calls sharing a workspace must be ordered on one stream.
+ * Status: the uint32 at byte offset 12 of the workspace becomes 1 if a decode
+ * split gave up waiting for its group's selection (a bounded wait, a guard
+ * that a correct launch never trips); that split then decodes nothing and the
+ * outputs of that call are unspecified. The word is sticky: zero-fill the
+ * workspace to clear it.
  */
 int resa_decode_step(const resa_kv_cache_t* c, const void* k_new, const void* v_new,
                      const void* q, int32_t num_q_heads, int32_t* seq_lens, int32_t max_seq_len,

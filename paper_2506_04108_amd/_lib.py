@@ -52,6 +52,8 @@ SIGNATURES = {
                                      _P, _P, _Z, _P]),
     "resa_append_select": (C.c_int, [_CACHE, _P, _P, _P, _I, _P, _I, C.POINTER(SelectParams), _P, _P,
                                      _I, _P, _P, _Z, _P]),
+    "resa_select_stats_offset": (_Z, [_I, _I]),
+    "resa_step_stats_offset": (_Z, [_I, _I]),
     "resa_decode_num_splits": (_I, [_I, _I, _I, _I]),
     "resa_decode_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I]),
     "resa_sparse_decode": (C.c_int, [_CACHE, _P, _I, _P, _P, _P, _I, _I, _F, _P, _P, _P, _Z, _P]),

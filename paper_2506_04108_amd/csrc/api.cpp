@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
+#include <cstdlib>
 #include <mutex>
 #include <string>
 
@@ -113,23 +114,25 @@ int hip_fail(hipError_t e, const char* what) {
 }
 
 struct SelectLayout {
-  size_t counters, seq_counters, window, hist, keys, above_bits, win_keys, total;
+  size_t counters, seq_counters, window, stats, hist, keys, above_bits, win_keys, total;
 };
 
 size_t bits_stride(size_t mseq) { return ((mseq + 31) / 32 + 3) & ~size_t(3); }
 
 // Workspace of resa_select_blocks / resa_append_select: one ticket per group
 // and one per sequence (zero between calls), one digit-window hint per group
-// (kept from call to call; any value is valid), per-workgroup key-digit
-// counts, the blocks' keys (rows padded to 4 words), and for the top-n's
-// in-window path a bit per block and a (key, id) list per group.
+// (kept from call to call; any value is valid), one diagnostic counter per
+// group (calls whose top-n finished on the in-window path), per-workgroup
+// key-digit counts, the blocks' keys (rows padded to 4 words), and for the
+// top-n's in-window path a bit per block and a (key, id) list per group.
 SelectLayout select_layout_words(int32_t batch, int32_t kv_heads, size_t mseq, size_t hist_words) {
   SelectLayout l;
   const size_t groups = (size_t)batch * kv_heads;
   l.counters = 0;
   l.seq_counters = groups * 4;
   l.window = (groups + (size_t)batch) * 4;
-  l.hist = round256((2 * groups + (size_t)batch) * 4);
+  l.stats = (2 * groups + (size_t)batch) * 4;
+  l.hist = round256((3 * groups + (size_t)batch) * 4);
   l.keys = l.hist + round256(groups * hist_words * 4);
   l.above_bits = l.keys + round256(groups * ((mseq + 3) & ~size_t(3)) * sizeof(uint32_t));
   l.win_keys = l.above_bits + round256(groups * bits_stride(mseq) * 4);
@@ -322,6 +325,7 @@ int select_common(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
   a.lens_out = const_cast<int32_t*>(seq_lens);
   a.seq_counters = reinterpret_cast<uint32_t*>(ws + lay.seq_counters);
   a.window = reinterpret_cast<uint32_t*>(ws + lay.window);
+  a.stats = reinterpret_cast<uint32_t*>(ws + lay.stats);
   a.above_bits = reinterpret_cast<uint32_t*>(ws + lay.above_bits);
   a.bits_stride = (int32_t)bits_stride(mseq);
   a.win_keys = reinterpret_cast<uint64_t*>(ws + lay.win_keys);
@@ -361,6 +365,16 @@ int resa_append_select(const resa_kv_cache_t* c, const void* k_new, const void* 
   return select_common(c, q, num_q_heads, seq_lens, max_seq_len + 1, params, block_idx, num_sel,
                        n_cap, scores_out, workspace, workspace_bytes, k_new, v_new, stream,
                        "resa_append_select launch");
+}
+
+size_t resa_select_stats_offset(int32_t batch, int32_t num_kv_heads) {
+  if (batch < 1 || num_kv_heads < 1) return 0;
+  return select_layout_words(batch, num_kv_heads, 1, 1).stats;
+}
+
+size_t resa_step_stats_offset(int32_t batch, int32_t num_kv_heads) {
+  if (batch < 1 || num_kv_heads < 1) return 0;
+  return step_layout(batch, num_kv_heads, 1, 1, 16, 1).sel + select_layout_words(batch, num_kv_heads, 1, 1).stats;
 }
 
 int32_t resa_decode_num_splits(int32_t batch, int32_t num_kv_heads, int32_t n_cap,
@@ -617,6 +631,7 @@ int resa_decode_step(const resa_kv_cache_t* c, const void* k_new, const void* v_
   sa.lens_out = seq_lens;
   sa.seq_counters = reinterpret_cast<uint32_t*>(wsel + lay.s.seq_counters);
   sa.window = reinterpret_cast<uint32_t*>(wsel + lay.s.window);
+  sa.stats = reinterpret_cast<uint32_t*>(wsel + lay.s.stats);
   sa.above_bits = reinterpret_cast<uint32_t*>(wsel + lay.s.above_bits);
   sa.bits_stride = (int32_t)bits_stride(mseq);
   sa.win_keys = reinterpret_cast<uint64_t*>(wsel + lay.s.win_keys);
@@ -645,6 +660,11 @@ int resa_decode_step(const resa_kv_cache_t* c, const void* k_new, const void* v_
   if (a.nranges < 1) a.nranges = 1;
   a.score_items = (int32_t)(groups * a.nranges);
   a.dec_items = (int32_t)(groups * splits);
+  // Bound of a decode split's wait for its group's selection (polls of about
+  // 128 cycles each, ~1 s): a guard a correct launch never reaches. Tests of
+  // the guard lower it through RESA_STEP_MAX_SPINS.
+  a.max_spins = 1u << 20;
+  if (const char* env = std::getenv("RESA_STEP_MAX_SPINS")) a.max_spins = (uint32_t)std::strtoul(env, nullptr, 10);
   hipError_t e = resa::launch_step(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "resa_decode_step launch");
   return ok();

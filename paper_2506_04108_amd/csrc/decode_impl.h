@@ -337,7 +337,8 @@ __device__ __forceinline__ int ld_i32(const int32_t* p) {
 // loads; also selects the opaque thread index of the persistent kernel).
 // Every workgroup of the group writes its partial (several splits) and the
 // last one to finish merges them; returns true in the workgroup that wrote
-// the group's output.
+// the group's output. `empty`: the split decodes no chunk (it still takes
+// part in the merge).
 //
 // Start-up: the count, the length, the query rows and the first pass's ids
 // are all requested before anything waits for one of them (vector loads, so
@@ -345,7 +346,8 @@ __device__ __forceinline__ int ld_i32(const int32_t* p) {
 // kernel arguments and the first K / V loads.
 template <int G, int BS, int NW, bool kCoherent, int kDepth = 2>
 __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk, int split,
-                                             const int32_t* lens, bool append, DecodeLds<G, NW>& lds) {
+                                             const int32_t* lens, bool append, DecodeLds<G, NW>& lds,
+                                             bool empty = false) {
   constexpr int GP = Pad<G>::GP;
   constexpr int CPB = BS / kChunk;  // chunks per block
   constexpr int NT = 64 * NW;
@@ -412,7 +414,7 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
   const int L = app ? L0 + 1 : L0;
   const int pos = app ? L0 : -1;
   const int M = min((L + BS - 1) / BS, a.c.max_blocks);
-  const int n = max(0, min(n_raw, a.n_cap));
+  const int n = empty ? 0 : max(0, min(n_raw, a.n_cap));
   const int C = n * CPB;
   const int valid = count_below(C);
 

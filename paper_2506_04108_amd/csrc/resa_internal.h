@@ -66,6 +66,7 @@ struct SelectArgs {
   int32_t* lens_out;           // seq_lens, written once every group of the sequence is done
   uint32_t* seq_counters;      // [B], zero between calls
   uint32_t* window;            // [B, Hkv] digit-window hint kept across calls (any value is valid)
+  uint32_t* stats;             // [B, Hkv] calls whose top-n finished on the in-window path (diagnostic)
   // Written by the scoring when the hint is set (fused top-n), for the
   // top-n's in-window path: per block, a bit for a key above the window,
   // and each range's in-window keys grouped by digit, descending.
@@ -101,6 +102,7 @@ struct StepArgs {
   uint32_t* ready;             // [B, Hkv]: selection of the group published (zero between calls)
   int32_t nranges;             // score ranges per group (blocks_per_wg each)
   int32_t score_items, dec_items;
+  uint32_t max_spins;          // bound of a decode split's wait for its group's selection
 };
 
 struct RectifyArgs {

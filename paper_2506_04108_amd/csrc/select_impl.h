@@ -455,6 +455,8 @@ __device__ __forceinline__ void select_tail(const SelectArgs& a, size_t grp, int
     const uint32_t E = ab[128];  // list entries needed: at most one per thread
     if (E <= (uint32_t)NT) {
       done = true;
+      // Diagnostic: calls of this group whose top-n finished on this path.
+      if (tid == 0) __hip_atomic_fetch_add(a.stats + grp, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       // Requests: the group's above-window bits and this thread's entry
       // (entry e of range r, r the last range with prefix <= e).
       constexpr int kBitWords = 1024 / NT;

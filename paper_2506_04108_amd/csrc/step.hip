@@ -12,8 +12,10 @@
 // splits once every score range has been claimed, and a claimed score range
 // belongs to a running workgroup that waits on nothing, so every flag a
 // decode split waits for gets set: the waits end without any assumption on
-// how many workgroups run at once. (A bounded spin records an error flag and
-// continues rather than hang, as a guard.)
+// how many workgroups run at once. (A bounded spin records an error flag, and
+// the split decodes nothing rather than hang or read unpublished ids, as a
+// guard; the last workgroup to exit clears every ready flag, so a late flag
+// cannot leak into the next call.)
 //
 // The appended token's K and V rows are taken from k_new / v_new by the
 // decode splits (the cache rows written in this launch are not read back),
@@ -32,7 +34,6 @@ constexpr int kStepThreads = 64 * kStepWaves;
 // the register budget, so wide groups keep one chunk fewer in flight.
 template <int G>
 constexpr int kStepDepth = G <= 4 ? 2 : 1;
-constexpr uint32_t kMaxSpins = 1u << 20;  // ~1 s of polling: a guard, never reached in a correct launch
 
 // The kernel arguments through a pointer the compiler cannot follow from
 // one call to the next: each phase loads the fields it uses where it uses
@@ -55,7 +56,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step(StepArgs) {
   __shared__ uint32_t s_lds32[32];
   __shared__ uint32_t s_misc[8];
   __shared__ DecodeLds<G, kStepWaves> dl;
-  __shared__ uint32_t s_item;
+  __shared__ uint32_t s_item, s_skip;
   // Score ranges, then the group's top-n in the workgroup that completes it.
   for (;;) {
     const StepArgs& a = launder();
@@ -91,12 +92,15 @@ __global__ __launch_bounds__(kStepThreads) void k_step(StepArgs) {
     if (tid == 0) {
       const uint32_t item = claim(a.queue + 1);
       s_item = item;
+      s_skip = 0;
       if ((int)item < a.dec_items) {
         const uint32_t* flag = a.ready + item / S;
         uint32_t spins = 0;
         while (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u) {
-          if (++spins > kMaxSpins) {
+          if (++spins > a.max_spins) {
+            // Guard: record it and decode nothing (the ids are not published).
             __hip_atomic_store(a.queue + 3, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            s_skip = 1;
             break;
           }
           __builtin_amdgcn_s_sleep(2);
@@ -105,15 +109,16 @@ __global__ __launch_bounds__(kStepThreads) void k_step(StepArgs) {
     }
     __syncthreads();
     const int item = (int)s_item;
+    const bool skip = s_skip != 0;
     __syncthreads();  // every thread has read s_item before thread 0 writes it again
     if (item >= a.dec_items) break;
     const int g = item / S, split = item - g * S;
     const int bb = g / H, hk = g - bb * H;
     bool last = false;
     switch (sa.c.block_size) {
-      case 16: last = decode_split<G, 16, kStepWaves, true, kStepDepth<G>>(a.d, bb, hk, split, sa.seq_lens, true, dl); break;
-      case 32: last = decode_split<G, 32, kStepWaves, true, kStepDepth<G>>(a.d, bb, hk, split, sa.seq_lens, true, dl); break;
-      default: last = decode_split<G, 64, kStepWaves, true, kStepDepth<G>>(a.d, bb, hk, split, sa.seq_lens, true, dl); break;
+      case 16: last = decode_split<G, 16, kStepWaves, true, kStepDepth<G>>(a.d, bb, hk, split, sa.seq_lens, true, dl, skip); break;
+      case 32: last = decode_split<G, 32, kStepWaves, true, kStepDepth<G>>(a.d, bb, hk, split, sa.seq_lens, true, dl, skip); break;
+      default: last = decode_split<G, 64, kStepWaves, true, kStepDepth<G>>(a.d, bb, hk, split, sa.seq_lens, true, dl, skip); break;
     }
     // Every split of the group has passed its wait (the merging workgroup
     // holds the last ticket): the flag returns to zero for the next call.
@@ -121,15 +126,22 @@ __global__ __launch_bounds__(kStepThreads) void k_step(StepArgs) {
     __syncthreads();
   }
 
-  // The last workgroup to finish returns the claim counters to zero and
-  // stores the new lengths (every item of the launch read the old ones).
+  // The last workgroup to finish returns the claim counters and every ready
+  // flag to zero (a flag set late, after a guard gave up on it, included)
+  // and stores the new lengths (every item of the launch read the old ones).
+  // Each workgroup's stores are acknowledged before it claims its exit.
   const StepArgs& a = launder();
   const SelectArgs& sa = a.s;
   const int tid = thread_id();
+  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
   if (tid == 0) s_item = claim(a.queue + 2);
   __syncthreads();
   if (s_item != gridDim.x - 1) return;
   if (tid < 3) __hip_atomic_store(a.queue + tid, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const int groups = sa.c.batch * sa.c.kv_heads;
+  for (int g = tid; g < groups; g += kStepThreads)
+    __hip_atomic_store(a.ready + g, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   for (int b = tid; b < sa.c.batch; b += kStepThreads) {
     const int L0 = sa.seq_lens[b];
     if (L0 >= 0 && L0 < sa.c.capacity) sa.lens_out[b] = L0 + 1;

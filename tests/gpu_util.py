@@ -99,3 +99,12 @@ def unpage(cache: R.KVCache, lens):
         K[bi, :, lens[bi]:] = 0
         V[bi, :, lens[bi]:] = 0
     return K, V
+
+
+def select_stats(ws, batch, kv_heads, step=False) -> np.ndarray:
+    """The per-group diagnostic counters of a selection (or fused step)
+    workspace: calls whose top-n finished on its in-window path."""
+    from paper_2506_04108_amd._lib import lib
+    off = (lib().resa_step_stats_offset if step else lib().resa_select_stats_offset)(batch, kv_heads)
+    n = batch * kv_heads
+    return ws.buf[off:off + 4 * n].view(torch.int32).cpu().numpy().reshape(batch, kv_heads)

@@ -15,6 +15,7 @@ import oracle as O
 import paper_2506_04108_amd as R
 import workloads as W
 from gpu_util import (SENTINEL, dev, down, i32, make_cache, make_paged_cache, oracle_summaries,
+                      select_stats,
                       padded_idx, unpage, up)
 from oracle.compare import check_selection, max_abs_err
 
@@ -288,8 +289,9 @@ def test_select_window_hint_ragged(b):
                 check_selection(gi[bi, hi, :gn[bi, hi]], ri[bi, hi], rs[bi, hi], rn[bi, hi], 1)
 
 
-def _window_lists_calls(w, cap, lens, scales, qstep):
-    """Calls on one workspace against calls on a fresh one and the oracle."""
+def _window_lists_calls(w, cap, lens, scales, qstep, sparsity=0.9):
+    """Calls on one workspace against calls on a fresh one and the oracle;
+    returns the workspace's in-window top-n counters."""
     B, H = w.batch, w.num_kv_heads
     K, _ = W.kv_cache(w, capacity=cap)
     cache = make_cache(K, K, 16)
@@ -303,8 +305,8 @@ def _window_lists_calls(w, cap, lens, scales, qstep):
     q0 = W.bf16_bits_to_f32(W.decode_query(w, qstep))
     for scale in scales:
         q = W.f32_to_bf16_bits(q0 * scale)
-        idx, ns = R.select_blocks(cache, up(q), lt, max(lens), 0.9, 4, 1, workspace=ws)
-        idx2, ns2 = R.select_blocks(cache, up(q), lt, max(lens), 0.9, 4, 1)
+        idx, ns = R.select_blocks(cache, up(q), lt, max(lens), sparsity, 4, 1, workspace=ws)
+        idx2, ns2 = R.select_blocks(cache, up(q), lt, max(lens), sparsity, 4, 1)
         torch.cuda.synchronize()
         assert torch.equal(idx, idx2) and torch.equal(ns, ns2), scale
         qg = O.split_heads(O.bf16_to_f64(q), H)
@@ -313,27 +315,36 @@ def _window_lists_calls(w, cap, lens, scales, qstep):
             for hi in range(H):
                 kmin, kmax = summ[bi, hi]
                 rs = O.block_scores(O.pooled_query(qg[bi, hi]), kmin, kmax)
-                rn = O.num_selected(kmin.shape[0], 0.9, 4, 1)
+                rn = O.num_selected(kmin.shape[0], sparsity, 4, 1)
                 assert gn[bi, hi] == rn
                 check_selection(gi[bi, hi, :gn[bi, hi]], O.select_blocks(rs, rn, 1), rs, rn, 1)
+    return select_stats(ws, B, H)
 
 
 def test_select_window_lists_hint():
     """Groups of 12500 blocks (16 keys per top-n thread, 8 groups of 31 score
-    ranges): a call whose threshold falls in the window hint takes the
+    ranges) at sparsity 0.95 (n = 625, so the list entries fit the tail's
+    1024 threads): a call whose threshold falls in the window hint takes the
     in-window path, which reads the scoring's above-window bits and in-window
-    lists instead of every key. Queries scaled by powers of two (and negated)
-    make the hint hit, miss above and miss below; every call must equal a
-    call on a fresh workspace and the oracle."""
+    lists instead of every key (the workspace counter of such calls must
+    grow). Queries scaled by powers of two (and negated) make the hint hit,
+    miss above and miss below; every call must equal a call on a fresh
+    workspace and the oracle."""
     w, cap = small(g=4, b=16, L=200000, cap=200064, B=1, H=8, tag="wlist")
-    _window_lists_calls(w, cap, [200000], [1.0, 1.0, 4.0, 0.25, -1.0, 1.0, 64.0, 1.0], 0)
+    stats = _window_lists_calls(w, cap, [200000], [1.0, 1.0, 4.0, 0.25, -1.0, 1.0, 64.0, 1.0], 0,
+                                sparsity=0.95)
+    print(f"in-window top-n calls per group: {stats.ravel().tolist()}", flush=True)
+    assert stats.sum() > 0
 
 
 def test_select_window_lists_ragged():
     """The in-window path over ragged lengths: groups of 12500, 8126 and 44
-    blocks (28, 19 and 1 score ranges) with a moving score distribution."""
+    blocks (28, 19 and 1 score ranges) with a moving score distribution; at
+    sparsity 0.9 the 8126-block groups (n = 813) take the path."""
     w, cap = small(g=4, b=16, L=200000, cap=200064, B=3, H=3, tag="wlong")
-    _window_lists_calls(w, cap, [200000, 130001, 700], [1.0, 1.0, 1.0, 1.25, 1.25, 0.8, 2.0, 1.0], 2)
+    stats = _window_lists_calls(w, cap, [200000, 130001, 700], [1.0, 1.0, 1.0, 1.25, 1.25, 0.8, 2.0, 1.0], 2)
+    print(f"in-window top-n calls per group: {stats.ravel().tolist()}", flush=True)
+    assert stats[1].sum() > 0
 
 
 def test_select_planted_blocks_win():
@@ -468,9 +479,12 @@ def test_append_select_matches_separate(b, n_local, M):
     steps with appends that open a block and appends inside one, and the ids
     equal to a selection on a fresh workspace (no window hint) of the same
     cache (M = 12500 with 8 kv heads takes the in-window top-n path from the
-    second step on; M = 33000 the standalone top-n kernel)."""
+    second step on: at sparsity 0.95 its n = 625 list entries fit the tail's
+    1024 threads, and the workspace counters of such calls must grow; M = 33000
+    the standalone top-n kernel)."""
     B = 3 if M < 1000 else 1
     H, g = (8 if M == 12500 else 2), 4
+    sp = 0.95 if M == 12500 else 0.9
     cap = M * b
     rng = np.random.default_rng(b * 100 + n_local + M)
     lens0 = [cap - 3 * b, cap // 2 - 1, cap // 3 + 5][:B]
@@ -490,15 +504,15 @@ def test_append_select_matches_separate(b, n_local, M):
         vn = W.f32_to_bf16_bits(rng.standard_normal((B, H, 128)).astype(np.float32))
         q = W.f32_to_bf16_bits(rng.standard_normal((B, H * g, 128)).astype(np.float32))
         mseq = -(-(bound + 1) // b)
-        n_cap = R.num_selected(mseq, 0.9, 2, n_local)
+        n_cap = R.num_selected(mseq, sp, 2, n_local)
         s1 = torch.full((B, H, mseq), float("nan"), device=dev())
         s2 = torch.full((B, H, mseq), float("nan"), device=dev())
         R.append_kv(c1, up(kn), up(vn), l1, bound)
-        i1, n1 = R.select_blocks(c1, up(q), l1, bound + 1, 0.9, 2, n_local, n_cap=n_cap,
+        i1, n1 = R.select_blocks(c1, up(q), l1, bound + 1, sp, 2, n_local, n_cap=n_cap,
                                  scores_out=s1, workspace=ws1)
-        i2, n2 = R.append_select(c2, up(kn), up(vn), up(q), l2, bound, 0.9, 2, n_local,
+        i2, n2 = R.append_select(c2, up(kn), up(vn), up(q), l2, bound, sp, 2, n_local,
                                  n_cap=n_cap, scores_out=s2, workspace=ws2)
-        i3, n3 = R.select_blocks(c2, up(q), l2, bound + 1, 0.9, 2, n_local, n_cap=n_cap)
+        i3, n3 = R.select_blocks(c2, up(q), l2, bound + 1, sp, 2, n_local, n_cap=n_cap)
         torch.cuda.synchronize()
         assert torch.equal(l1, l2)
         assert torch.equal(n1, n2) and torch.equal(i1, i2)
@@ -507,6 +521,9 @@ def test_append_select_matches_separate(b, n_local, M):
         assert torch.equal(torch.nan_to_num(s1), torch.nan_to_num(s2))
         bound += 1
     assert l2.cpu().tolist() == [x + 3 for x in lens0]
+    if M == 12500:
+        for ws in (ws1, ws2):
+            assert select_stats(ws, B, H).sum() > 0, "the in-window top-n path was not taken"
     for name in ("k", "v", "kmin", "kmax"):
         assert torch.equal(getattr(c1, name), getattr(c2, name)), name
 

@@ -11,7 +11,7 @@ import torch
 import oracle as O
 import paper_2506_04108_amd as R
 import workloads as W
-from gpu_util import down, i32, make_cache, make_paged_cache, up
+from gpu_util import down, i32, make_cache, make_paged_cache, select_stats, up
 from oracle.compare import check_selection, max_abs_err
 
 pytestmark = pytest.mark.gpu
@@ -32,13 +32,16 @@ def step_error_flag(ws: R.Workspace) -> int:
     return int(ws.buf[12:16].view(torch.int32).item())
 
 
-def run_pair(w, cache, lens, steps, num_splits=0, n_cap=None):
+def run_pair(w, cache, lens, steps, num_splits=0, n_cap=None, keep=None):
     """Runs `steps` decode tokens through resa_decode_step on `cache` and
     through append_select + sparse_decode on a copy; checks them against each
-    other every step and yields (step, q, idx, nsel, out) of the fused path."""
+    other every step and yields (step, q, idx, nsel, out) of the fused path.
+    `keep` (a dict) receives the step and selection workspaces."""
     ref_cache = clone(cache)
     lt, lr = i32(lens), i32(lens)
     ws_step, ws_sel, ws_dec = R.Workspace(), R.Workspace(), R.Workspace()
+    if keep is not None:
+        keep.update(step=ws_step, select=ws_sel)
     L = list(lens)
     for step in range(steps):
         kn, vn = W.decode_kv(w, step)
@@ -81,20 +84,27 @@ def test_step_matches_separate_calls(g, b):
 
 def test_step_window_lists():
     """16 groups of 8200 - 8750 blocks (32 keys per thread of the fused
-    step's 512-thread top-n, 31 score ranges of 288 blocks): from the second
-    step on, the window hint is set and the fused step's top-n takes the
-    in-window path (above-window bits and in-window lists written by its score
-    ranges), while append_select (12 keys per thread) reads every key; the
-    selections must be identical and the outputs equal up to summation order."""
-    w = W.LONG_64K.with_(batch=2, num_kv_heads=8, num_q_heads=32, seq_len=140000, seed_tag="steplists")
+    step's 512-thread top-n, 31 score ranges of 288 blocks) at sparsity 0.95
+    (n = 411 - 438, so the list entries the path needs fit the 512 threads):
+    from the second step on, the window hint is set and the fused step's top-n
+    takes the in-window path (above-window bits and in-window lists written by
+    its score ranges; the workspace counter of such calls must grow), while
+    append_select (12 keys per thread) reads every key; the selections must be
+    identical and the outputs equal up to summation order."""
+    w = W.LONG_64K.with_(batch=2, num_kv_heads=8, num_q_heads=32, seq_len=140000, sparsity=0.95,
+                         seed_tag="steplists")
     cap = 140064
     lens = [140000, 131500]
     K, V = W.kv_cache(w, capacity=cap)
     cache = make_cache(K, V, 16, sentinel=False)
     del K, V
     R.block_summarize(cache, i32(lens))
-    for _ in run_pair(w, cache, lens, steps=4):
+    keep = {}
+    for _ in run_pair(w, cache, lens, steps=4, keep=keep):
         pass
+    stats = select_stats(keep["step"], 2, 8, step=True)
+    print(f"in-window top-n calls per group: {stats.ravel().tolist()}", flush=True)
+    assert stats.sum() > 0, "the fused step never took the in-window path"
 
 
 def test_step_against_oracle_loop():
@@ -316,3 +326,47 @@ def test_step_fullsize(name):
         err = max_abs_err(go[bi, hi * g:(hi + 1) * g], o_ref)
         print(f"[step fullsize] {name} group ({bi},{hi}): |dO| {err:.2e}", flush=True)
         assert err <= TOL
+
+
+def test_step_guard_trip_does_not_leak():
+    """The fused step's bounded wait for a group's selection, forced to give
+    up at once (RESA_STEP_MAX_SPINS=0, read by the library at each call): the
+    call ends normally, a split that gave up decodes nothing and sets the
+    sticky status word, and the next call on the same workspace (normal bound)
+    finds every ready flag cleared and gives the results of the separate
+    calls."""
+    import os
+    w = W.LONG_64K.with_(batch=2, num_kv_heads=8, num_q_heads=32, seq_len=60000, seed_tag="guard")
+    cap = 60064
+    lens = [60000, 47000]
+    K, V = W.kv_cache(w, capacity=cap)
+    cache = make_cache(K, V, 16, sentinel=False)
+    ref = clone(cache)
+    del K, V
+    lt, lr = i32(lens), i32(lens)
+    R.block_summarize(cache, lt)
+    R.block_summarize(ref, lr)
+    ws, ws_sel, ws_dec = R.Workspace(), R.Workspace(), R.Workspace()
+    L = list(lens)
+    for step in range(2):
+        kn, vn = W.decode_kv(w, step)
+        q = W.decode_query(w, step)
+        os.environ["RESA_STEP_MAX_SPINS"] = "0" if step == 0 else str(1 << 20)
+        try:
+            idx, ns, out, lse = R.decode_step(cache, up(kn), up(vn), up(q), lt, max(L), w.sparsity,
+                                              w.min_blocks, w.n_local, workspace=ws)
+        finally:
+            os.environ.pop("RESA_STEP_MAX_SPINS", None)
+        ridx, rns = R.append_select(ref, up(kn), up(vn), up(q), lr, max(L), w.sparsity, w.min_blocks,
+                                    w.n_local, n_cap=idx.shape[-1], workspace=ws_sel)
+        rout, _ = R.sparse_decode(ref, up(q), lr, ridx, rns, workspace=ws_dec)
+        torch.cuda.synchronize()
+        groups = 16
+        ready = ws.buf[256:256 + 4 * groups].view(torch.int32).cpu().numpy()
+        assert np.all(ready == 0), "a ready flag leaked past the call"
+        assert torch.equal(lt, lr) and torch.equal(ns, rns) and torch.equal(idx, ridx)
+        if step == 0:
+            print(f"guard status after the forced call: {step_error_flag(ws)}", flush=True)
+        else:
+            assert max_abs_err(out.cpu().numpy(), rout.cpu().numpy()) <= REORDER
+        L = [x + 1 for x in L]
