@@ -9,10 +9,11 @@
 // Grid (num_splits, ceil(R / rows), batch * kv_heads) with 4 waves (rows =
 // 128, windows of up to 128 rows) or 8 waves (rows = 256, longer windows
 // such as prefill) per workgroup, each wave owning 32 query rows (two
-// 16-row tiles). A workgroup walks its key
-// range in tiles of 64 keys: K and V rows go from registers (loaded one tile
-// ahead) into one of two LDS buffers, row-major, so one barrier per tile
-// separates filling a buffer from reading it. Per tile and wave:
+// 16-row tiles). A workgroup walks its key range in tiles of 32 keys
+// through four LDS stages: K and V rows go from HBM straight into LDS
+// (buffer loads with the LDS destination, no registers), three tiles ahead
+// of the one being computed, and one barrier per tile publishes a tile and
+// frees the stage read before it. Per tile and wave:
 //   S^T = K . Q^T        (keys x queries; lane l holds query l % 16 and keys
 //                          16 kt + 4 (l / 16) + i)
 //   online softmax per query row in the log2 domain against a reference
@@ -22,15 +23,16 @@
 //                          ordered so that P^T is already in the B-operand
 //                          layout, and V^T comes from the row-major V tile
 //                          through the LDS transpose read)
-// V tiles are converted from bf16 to fp16 on their way into LDS, each head
-// dimension d multiplied by a power of two 2^-E_d first (E_d = 0 until a
-// value needs it). Every bf16 value of magnitude 2^-14 .. 65280 is an fp16
-// value (8 significant bits fit in 11), so in that range the conversion is
-// exact; smaller values keep fp16's subnormal spacing of 2^-24 (an error of at
-// most 2^-24 * P per key). A thread that finds a scaled value above 65504
-// flags the tile; on a flagged tile every wave reloads the tile's V, raises
-// E_d of the dimensions that need it (so that max |v| 2^-E_d < 2^16),
-// multiplies those accumulator rows by the change, and converts the tile
+// V tiles are converted from bf16 to fp16 in LDS, before the barrier, by
+// the threads that loaded them, each head dimension d multiplied by a power
+// of two 2^-E_d first (E_d = 0 until a value needs it). Every bf16 value of
+// magnitude 2^-14 .. 65280 is an fp16 value (8 significant bits fit in 11),
+// so in that range the conversion is exact; smaller values keep fp16's
+// subnormal spacing of 2^-24 (an error of at most 2^-24 * P per key). A
+// thread that finds a scaled value above 65504 flags the tile; on a flagged
+// tile every thread reloads its V pieces from HBM, E_d rises for the
+// dimensions that need it (so that max |v| 2^-E_d < 2^16), those
+// accumulator rows are multiplied by the change, and the tile is converted
 // again. Rows are multiplied back by 2^E_d after the normalisation by the
 // softmax sum, so every finite bf16 V gives a finite result (products
 // P V 2^-E_d stay below 2^24 and their sums far below the fp32 range).
@@ -59,9 +61,61 @@ constexpr int kRowsPerWave = 32;
 template <int kWaves>
 constexpr int rows_per_wg() { return kWaves * kRowsPerWave; }
 __host__ __device__ constexpr int waves_for_rows(int rows) { return rows > 128 ? 8 : 4; }
-constexpr int kKeyTile = 64;
-constexpr int kStride = kHeadDim + 8;    // bf16 per K or V row in LDS (272 B, 16-B aligned)
-constexpr int kTileElems = kKeyTile * kStride;
+constexpr int kKeyTile = 32;                      // keys per tile
+constexpr int kStages = 4;                        // LDS stages: the tile computed, three in flight
+constexpr int kRowBytes = kHeadDim * 2;           // one K or V row (16-bit values)
+constexpr int kTileBytes = kKeyTile * kRowBytes;  // 8 KB of K and 8 KB of V per tile
+constexpr int kPageRing = 8;                      // page ids per wave held in LDS
+typedef int32_t i32x4_t __attribute__((ext_vector_type(4)));
+
+// Tile rows are stored unpadded (256 B); 16-byte piece p of row r sits in
+// slot p ^ swz(r). swz is a bijection on r % 16, so the K operand reads (16
+// rows, one piece) hit 16 distinct slots; its bits 1..3 follow r % 8 and
+// its low bit r / 8, so the V transpose reads (4 aligned rows, two
+// neighbouring pieces) hit 8 distinct slots: no LDS bank conflicts.
+__host__ __device__ constexpr int swz(int r) { return ((r & 7) << 1) | ((r >> 3) & 1); }
+
+// s_waitcnt immediates (vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+constexpr int wait_vm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0F70; }
+constexpr int kWaitLgkm0 = 0xC07F;
+// Buffer resource over `bytes` bytes at p (stride 0, 32-bit format), for
+// values the caller knows are uniform across the wave: read from the first
+// lane, so the resource sits in scalar registers. Offsets at or past
+// `bytes` read as zero.
+__device__ __forceinline__ i32x4_t rsrc_words(const void* p, int bytes) {
+  const uint64_t u = reinterpret_cast<uint64_t>(p);
+  return i32x4_t{(int32_t)__builtin_amdgcn_readfirstlane((uint32_t)u),
+                 (int32_t)(__builtin_amdgcn_readfirstlane((uint32_t)(u >> 32)) & 0xffffu),
+                 __builtin_amdgcn_readfirstlane(bytes), kBufWord3};
+}
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void* p, int bytes) {
+  const uint64_t u = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+  void* q = reinterpret_cast<void*>(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(q, (short)0, __builtin_amdgcn_readfirstlane(bytes), kBufWord3);
+}
+// LDS byte address of an LDS object.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+// Buffer loads straight into LDS (no registers): lane i's 16 (4) bytes at
+// offset voff land at LDS byte address lds + 16 i (lds + 4 i); M0 carries
+// lds. Written as assembly so that the compiler does not track them: it
+// would otherwise make every V transpose read wait for all of them. Their
+// completion is ordered by hand (vmcnt waits, then a barrier). The kernels
+// that use them give M0 no other use.
+__device__ __forceinline__ void lds_load16(uint32_t lds, uint32_t voff, i32x4_t rs) {
+  __asm__ volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen nt lds"
+                   :: "s"(lds), "v"(voff), "s"(rs) : "memory");
+}
+__device__ __forceinline__ void lds_load4(uint32_t lds, uint32_t voff, i32x4_t rs) {
+  __asm__ volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+                   :: "s"(lds), "v"(voff), "s"(rs) : "memory");
+}
+// Keeps the compiler from moving memory accesses across this point; the
+// hardware ordering comes from the explicit waits and barriers around it.
+__device__ __forceinline__ void compiler_fence() { __asm__ volatile("" ::: "memory"); }
 constexpr int kMaxRectSplits = 1024;     // splits per group (bounded by the host)
 constexpr float kRefSlack = 8.f;         // log2-domain headroom of the softmax reference
 
@@ -76,10 +130,10 @@ __device__ __forceinline__ f32x4_t mfma16(f16x8_t a, f16x8_t b, f32x4_t c) {
 // 16-lane group: lane c of the group passes the address of key
 // kbase + c / 4, dims dbase + 4 (c % 4) .. + 4; lane i of the group receives
 // dim dbase + i of keys kbase .. kbase + 3.
-__device__ __forceinline__ f16x4_t lds_read_tr(const uint16_t* p) {
+__device__ __forceinline__ f16x4_t lds_read_tr(const uint8_t* p) {
   typedef __attribute__((address_space(3))) i16x4_t lds_i16x4;
   const i16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (lds_i16x4*)(const_cast<uint16_t*>(p)));
+      (lds_i16x4*)(const_cast<uint8_t*>(p)));
   return __builtin_bit_cast(f16x4_t, v);
 }
 
@@ -106,22 +160,42 @@ __global__ __launch_bounds__(256) void k_rectify_rows(RectifyArgs a) {
   }
 }
 
-template <int kWaves>
+template <int kWaves, bool kPaged>
 __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_rectify_attn(RectifyArgs a) {
   constexpr int kRowsPerWg = rows_per_wg<kWaves>();
-  constexpr int kThreads = 64 * kWaves;
-  constexpr int kPieces = kKeyTile * 16 / kThreads;  // 16-byte pieces of K (and of V) per thread per tile
-  constexpr int kRowStep = kThreads / 16;           // tile rows covered by one pass of the threads
-  __shared__ __attribute__((aligned(16))) uint16_t sK[2][kTileElems];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[2][kTileElems];
-  // V range handling: s_flag[buf] = first key of the tile in buffer buf when
-  // one of its scaled values is above the fp16 range (else an older tile's
-  // key, or -1); s_vscale[cur][d] = 2^-E_d; s_vmax[d] = max |v| of dimension
-  // d over a flagged tile (fp32 bits: non-negative values order as integers).
-  __shared__ int s_flag[2];
-  __shared__ __attribute__((aligned(16))) float s_vscale[2][kHeadDim];
-  __shared__ uint32_t s_vmax[kHeadDim];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int kLoadRows = kKeyTile / kWaves;   // tile rows whose K and V each wave loads
+  constexpr int kLoads = kLoadRows / 4;          // 1 KB load instructions per wave, tensor and tile
+  // Loads a wave issues per tile (K, V and, paged, one page id). When tile t
+  // is waited for, those of tiles t + 1 and t + 2 may still be in flight
+  // (page ids run three tiles ahead of the data they locate).
+  constexpr int kOpsPerTile = 2 * kLoads + (kPaged ? 1 : 0);
+  constexpr int kWaitTile = wait_vm(2 * kOpsPerTile);
+  // All of the workgroup's LDS is one object. With several, the compiler
+  // tags each access with the object it touches and then makes every LDS
+  // read of the tile buffers wait for all loads into them (the newest
+  // included), which would drain the pipeline; here the explicit waits and
+  // barriers below order the loads into LDS against the reads.
+  struct Lds {
+    uint8_t kv[kStages][2][kTileBytes];  // [stage][K, V] tile rows
+    int page[kWaves][kPageRing];         // page ids of each wave's rows
+    // V range handling: flag[st] = first key of the tile in stage st when
+    // one of its scaled values is above the fp16 range (else an older
+    // tile's key, or -1); vscale[cur][d] = 2^-E_d; vmax[d] = max |v| of
+    // dimension d over a flagged tile (fp32 bits: non-negative values order
+    // as integers).
+    int flag[kStages];
+    float vscale[2][kHeadDim];
+    uint32_t vmax[kHeadDim];
+  };
+  __shared__ __attribute__((aligned(1024))) Lds lds;
+  auto& s_kv = lds.kv;
+  auto& s_page = lds.page;
+  auto& s_flag = lds.flag;
+  auto& s_vscale = lds.vscale;
+  auto& s_vmax = lds.vmax;
+  // The wave index is uniform per wave (readfirstlane tells the compiler), so
+  // the load addressing below stays in scalar registers.
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int split = blockIdx.x, qblk = blockIdx.y, grp = blockIdx.z;
   const int bb = grp / a.c.kv_heads, hk = grp % a.c.kv_heads;
   // A sequence left out of this call: nothing is read or written (uniform
@@ -137,6 +211,7 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
   // skip them instead of masking them.
   const int last_row = min(R - 1, (qblk + 1) * kRowsPerWg - 1);
   const int k1 = seq_ok ? min(min(k0 + a.chunk, L), L - f + last_row / G + 1) : k0;
+  const int ntiles = k1 > k0 ? (k1 - k0 + kKeyTile - 1) / kKeyTile : 0;
   const int j = lane >> 4, lq = lane & 15;
   const int row_base = qblk * kRowsPerWg + wave * kRowsPerWave;
   const float ninf = -__builtin_inff();
@@ -172,41 +247,63 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
     for (int qt = 0; qt < 2; ++qt) o[dt][qt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m[2] = {ninf, ninf}, l[2] = {0.f, 0.f};
 
-  // Thread tid moves 16-byte pieces tid + kThreads e (e < kPieces) of a
-  // tile's K and V: key (tid + kThreads e) / 16, dims 8 (tid % 16) .. + 8.
-  const int part = tid & 15;
-  U4 rk[kPieces], rv[kPieces];
-  // Cache rows of the next tile to load. With a block table they are looked
-  // up one load ahead (gload(t0) loads tile t0 and looks up tile t0 + 64, the
-  // next one loaded), so the table read is not on the path of the data loads.
-  int64_t nrow[kPieces];
-  auto lookup = [&](int t0) {
+  // Wave w loads tile rows kLoadRows w .. + kLoadRows; load instruction e
+  // covers four of them: lane i fills LDS slot i % 16 of row
+  // kLoadRows w + 4 e + i / 16, fetching the row's piece (i % 16) ^ swz(row).
+  const int wrow = kLoadRows * wave;
+  const int lrow = lane >> 4, lslot = lane & 15;
+  // Buffer resources over this wave's rows of tile ti: rows at or past k1
+  // and rows of a page outside the pool fall outside them and read as zero.
+  auto tile_src = [&](int ti, const uint16_t*& pk, const uint16_t*& pv, int& nrec) __attribute__((always_inline)) {
+    const int key = k0 + ti * kKeyTile + wrow;
+    nrec = min(max(k1 - key, 0), kLoadRows) * kRowBytes;
+    size_t row;
+    if constexpr (kPaged) {
+      const int page = __builtin_amdgcn_readfirstlane(s_page[wave][ti & (kPageRing - 1)]);
+      if ((unsigned)page >= (unsigned)a.c.num_pages) nrec = 0;
+      row = ((size_t)page * a.c.kv_heads + hk) * a.c.block_size + (key & (a.c.block_size - 1));
+    } else {
+      row = ((size_t)bb * a.c.kv_heads + hk) * a.c.capacity + key;
+    }
+    pk = a.c.k + row * kHeadDim;
+    pv = a.c.v + row * kHeadDim;
+  };
+  auto src_off = [&](int e) __attribute__((always_inline)) {
+    return (uint32_t)((4 * e + lrow) * kRowBytes + 16 * (lslot ^ swz(wrow + 4 * e + lrow)));
+  };
+  const uint32_t lds_kv = __builtin_amdgcn_readfirstlane(lds_addr(&s_kv[0][0][0]));
+  // Tile ti's K and V rows of this wave, straight into stage ti % kStages.
+  auto issue = [&](int ti) __attribute__((always_inline)) {
+    const uint16_t *pk, *pv;
+    int nrec;
+    tile_src(ti, pk, pv, nrec);
+    const i32x4_t rk = rsrc_words(pk, nrec), rv = rsrc_words(pv, nrec);
+    const uint32_t dk = lds_kv + (uint32_t)((ti & (kStages - 1)) * 2 * kTileBytes + wrow * kRowBytes);
 #pragma unroll
-    for (int e = 0; e < kPieces; ++e) {
-      const int kk = t0 + (tid >> 4) + kRowStep * e;
-      nrow[e] = kk < k1 ? kv_row(a.c, bb, hk, kk) : -1;
+    for (int e = 0; e < kLoads; ++e) {
+      const uint32_t off = src_off(e);
+      lds_load16(dk + 4 * e * kRowBytes, off, rk);
+      lds_load16(dk + kTileBytes + 4 * e * kRowBytes, off, rv);
     }
   };
-  auto gload = [&](int t0) {
-#pragma unroll
-    for (int e = 0; e < kPieces; ++e) {
-      if (nrow[e] >= 0) {
-        rk[e] = ld16_stream(a.c.k + (size_t)nrow[e] * kHeadDim + part * 8);
-        rv[e] = ld16_stream(a.c.v + (size_t)nrow[e] * kHeadDim + part * 8);
-      } else {
-        rk[e] = U4{0, 0, 0, 0};
-        rv[e] = U4{0, 0, 0, 0};
-      }
+  // Page id of this wave's rows of tile ti (its rows lie in one block), into
+  // the ring; blocks past the table read as page 0 (only tiles past k1 ask).
+  auto issue_page = [&](int ti) __attribute__((always_inline)) {
+    if constexpr (kPaged) {
+      const int mb = (k0 + ti * kKeyTile + wrow) >> a.c.log2_block;
+      const i32x4_t rt = rsrc_words(a.c.table + (size_t)bb * a.c.max_blocks, a.c.max_blocks * 4);
+      const uint32_t dst = __builtin_amdgcn_readfirstlane(lds_addr(&s_page[wave][ti & (kPageRing - 1)]));
+      if (lane == 0) lds_load4(dst, (uint32_t)mb * 4, rt);
     }
-    lookup(t0 + kKeyTile);
   };
+
   // V scale state, uniform across the workgroup: `scaled` once any E_d > 0,
   // `cur` the current half of s_vscale.
   bool scaled = false;
   int cur = 0;
-  // Converts a 16-byte piece of V (8 bf16 values of dims part*8 ..) to fp16,
-  // times the per-dimension factors when `scaled`; vmax collects the largest
-  // scaled magnitude.
+  // Converts a 16-byte piece of V (8 bf16 values) to fp16, times the
+  // per-dimension factors when `use_sc`; vmax collects the largest scaled
+  // magnitude.
   auto to_h8 = [&](const U4& w, const float (&sc)[8], bool use_sc, float& vmax) __attribute__((always_inline)) {
     float x[8] = {bf_lo(w.x), bf_hi(w.x), bf_lo(w.y), bf_hi(w.y),
                   bf_lo(w.z), bf_hi(w.z), bf_lo(w.w), bf_hi(w.w)};
@@ -223,64 +320,65 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
     }
     return U4{h[0], h[1], h[2], h[3]};
   };
-  // Stores the loaded tile (first key `tag`) into buffer buf; a thread with a
-  // scaled V value outside the fp16 range flags the tile.
-  auto lstore = [&](int buf, int tag) __attribute__((always_inline)) {
-    float sc[8];
-    if (scaled) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) sc[i] = s_vscale[cur][part * 8 + i];
-    }
+  // Converts the V pieces this thread loaded for the tile in stage st
+  // (first key t0) in place; a thread with a scaled value outside the fp16
+  // range flags the tile.
+  auto convert = [&](int st, int t0) __attribute__((always_inline)) {
     float vmax = 0.f;
 #pragma unroll
-    for (int e = 0; e < kPieces; ++e) {
-      const int off = ((tid >> 4) + kRowStep * e) * kStride + part * 8;
-      st16(&sK[buf][off], rk[e]);
-      st16(&sV[buf][off], scaled ? to_h8(rv[e], sc, true, vmax) : to_h8(rv[e], sc, false, vmax));
+    for (int e = 0; e < kLoads; ++e) {
+      uint8_t* p = s_kv[st][1] + (wrow + 4 * e) * kRowBytes + 16 * lane;
+      const U4 w = ld16(p);
+      float sc[8];
+      if (scaled) {
+        const int piece = lslot ^ swz(wrow + 4 * e + lrow);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) sc[i] = s_vscale[cur][8 * piece + i];
+        st16(p, to_h8(w, sc, true, vmax));
+      } else {
+        st16(p, to_h8(w, sc, false, vmax));
+      }
     }
-    if (!(vmax <= 65504.f)) s_flag[buf] = tag;
+    if (!(vmax <= 65504.f)) s_flag[st] = t0;
   };
-  // A flagged tile (uniform: every wave reads the same flag). The tile's V is
-  // reloaded, the per-dimension maxima are gathered, E_d rises where
-  // max |v| 2^-E_d would reach 2^16, the accumulator rows of those dimensions
-  // follow, and the tile is converted again into its buffer.
-  auto fix_tile = [&](int t0, int buf) __attribute__((always_inline)) {
-    U4 vv[kPieces];
+  // A flagged tile (uniform: every wave reads the same flag). This thread's
+  // raw V pieces are reloaded, the per-dimension maxima are gathered, E_d
+  // rises where max |v| 2^-E_d would reach 2^16, the accumulator rows of
+  // those dimensions follow, and the pieces are converted again in place.
+  auto fix_tile = [&](int ti, int st) __attribute__((always_inline)) {
+    const uint16_t *pk, *pv;
+    int nrec;
+    tile_src(ti, pk, pv, nrec);
+    const __amdgpu_buffer_rsrc_t rv = uniform_rsrc(pv, nrec);
+    U4 vv[kLoads];
 #pragma unroll
-    for (int e = 0; e < kPieces; ++e) {
-      const int kk = t0 + (tid >> 4) + kRowStep * e;
-      const int64_t row = kk < k1 ? kv_row(a.c, bb, hk, kk) : -1;
-      vv[e] = row >= 0 ? ld16(a.c.v + (size_t)row * kHeadDim + part * 8) : U4{0, 0, 0, 0};
-    }
-    float dm[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int e = 0; e < kLoads; ++e)
+      vv[e] = __builtin_bit_cast(U4, __builtin_amdgcn_raw_buffer_load_b128(rv, src_off(e), 0, 0));
 #pragma unroll
-    for (int e = 0; e < kPieces; ++e) {
+    for (int e = 0; e < kLoads; ++e) {
+      const int piece = lslot ^ swz(wrow + 4 * e + lrow);
       const float x[8] = {bf_lo(vv[e].x), bf_hi(vv[e].x), bf_lo(vv[e].y), bf_hi(vv[e].y),
                           bf_lo(vv[e].z), bf_hi(vv[e].z), bf_lo(vv[e].w), bf_hi(vv[e].w)};
 #pragma unroll
-      for (int i = 0; i < 8; ++i) dm[i] = fmaxf(dm[i], fabsf(x[i]));
+      for (int i = 0; i < 8; ++i) atomicMax(&s_vmax[8 * piece + i], __float_as_uint(fabsf(x[i])));
     }
-#pragma unroll
-    for (int i = 0; i < 8; ++i) atomicMax(&s_vmax[part * 8 + i], __float_as_uint(dm[i]));
     lds_sync();
-    float ns[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const uint32_t mb = s_vmax[part * 8 + i];
+    if (tid < kHeadDim) {
+      const uint32_t mb = s_vmax[tid];
       // max |v| < 2^(ex + 1); E = ex - 15 keeps the scaled maximum below 2^16.
       const int ex = (int)((mb >> 23) & 0xff) - 127;
       const int E = ex > 15 ? ex - 15 : 0;
-      ns[i] = fminf(s_vscale[cur][part * 8 + i], __uint_as_float((uint32_t)(127 - E) << 23));
+      s_vscale[cur ^ 1][tid] = fminf(s_vscale[cur][tid], __uint_as_float((uint32_t)(127 - E) << 23));
     }
-    if (tid < 16) {  // part == tid: one thread per 8 dimensions publishes them
-#pragma unroll
-      for (int i = 0; i < 8; ++i) s_vscale[cur ^ 1][part * 8 + i] = ns[i];
-    }
+    lds_sync();
     float unused = 0.f;
 #pragma unroll
-    for (int e = 0; e < kPieces; ++e) {
-      const int off = ((tid >> 4) + kRowStep * e) * kStride + part * 8;
-      st16(&sV[buf][off], to_h8(vv[e], ns, true, unused));
+    for (int e = 0; e < kLoads; ++e) {
+      const int piece = lslot ^ swz(wrow + 4 * e + lrow);
+      float ns[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) ns[i] = s_vscale[cur ^ 1][8 * piece + i];
+      st16(s_kv[st][1] + (wrow + 4 * e) * kRowBytes + 16 * lane, to_h8(vv[e], ns, true, unused));
     }
     lds_sync();
     if (tid < kHeadDim) s_vmax[tid] = 0u;
@@ -299,35 +397,44 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
     scaled = true;
   };
 
+  // LDS byte offsets of this lane's operand reads within a stage. K (A of
+  // S^T): row 16 kt + lq, piece 4 s + j. V^T (A of O^T, transpose read):
+  // rows 4 j + lq / 4 and 16 + 4 j + lq / 4 (the same swizzle), dims
+  // 16 dt + 4 (lq % 4) .. + 4, i.e. piece 2 dt + (lq % 4) / 2, byte
+  // 8 (lq % 2) within it.
+  const int swq = swz(lq);
+  const int vrow = 4 * j + (lq >> 2), swv = swz(vrow);
   // One tile: scores, softmax update, P.V. kMasked evaluates the causal cut
   // and the split end per key.
-  auto tile = [&](int t0, int buf, auto masked) {
+  auto tile = [&](int ti, int st, auto masked) __attribute__((always_inline)) {
     constexpr bool kMasked = decltype(masked)::value;
-    const uint16_t* tk = sK[buf];
-    const uint16_t* tv = sV[buf];
-    const int flag = s_flag[buf];  // read now, used after the scores
-    f32x4_t sacc[4][2];
+    const int t0 = k0 + ti * kKeyTile;
+    const uint8_t* tk = s_kv[st][0];
+    const uint8_t* tv = s_kv[st][1];
+    const int flag = s_flag[st];  // read now, used after the scores
+    f32x4_t sacc[2][2];
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
+    for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) sacc[kt][qt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt) {
-        const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(&tk[(16 * kt + lq) * kStride + 32 * s + 8 * j]);
+      for (int kt = 0; kt < 2; ++kt) {
+        const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(
+            tk + (16 * kt + lq) * kRowBytes + 16 * ((4 * s + j) ^ swq));
 #pragma unroll
         for (int qt = 0; qt < 2; ++qt) sacc[kt][qt] = mfma16(ka, qb[qt][s], sacc[kt][qt]);
       }
     }
 
-    f16x8_t ph[2][2];  // [qt][32-key step]
+    f16x8_t ph[2];  // [qt]: keys 4 j + (0..3), then 16 + 4 j + (0..3)
 #pragma unroll
     for (int qt = 0; qt < 2; ++qt) {
-      float x[16];
+      float x[8];
       float tmax = ninf;
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
+      for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           float y = sacc[kt][qt][i];
@@ -342,7 +449,7 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
       // The reference m moves only when the tile's maximum exceeds it by
       // more than kRefSlack, so the accumulator rescale is rare; every
       // weight stays <= 2^kRefSlack, well inside fp16 and fp32 range, and
-      // the normalisation by l uses the same reference. A query's 64 keys
+      // the normalisation by l uses the same reference. A query's 32 keys
       // sit in four lanes (lq + 16 j): the row maximum across them is only
       // needed when one of them exceeds the reference, so the cross-lane
       // reduction runs on those (rare) tiles only.
@@ -359,10 +466,10 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
       const float mref = m[qt] == ninf ? 0.f : m[qt];
       float ps = 0.f;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
+      for (int e = 0; e < 8; ++e) {
         const float pe = fast_exp2(fmaf(x[e], c, -mref));
         ps += pe;
-        ph[qt][e >> 3][e & 7] = (_Float16)pe;
+        ph[qt][e] = (_Float16)pe;
       }
       l[qt] = fmaf(l[qt], alpha, ps);
       if (__any(alpha != 1.f)) {
@@ -371,54 +478,71 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
       }
     }
 
-    if (__builtin_amdgcn_readfirstlane(flag) == t0) fix_tile(t0, buf);
+    if (__builtin_amdgcn_readfirstlane(flag) == t0) fix_tile(ti, st);
 
-    // P^T for 32-key step ks: lane keys 32 ks + 4 j + (0..3) then
-    // 32 ks + 16 + 4 j + (0..3) (S^T tiles kt = 2 ks, 2 ks + 1); V^T rows of
-    // the same keys come from two transpose reads.
-    const int tr_key = 4 * j + (lq >> 2), tr_dim = 4 * (lq & 3);
+    // P^T: lane keys 4 j + (0..3) then 16 + 4 j + (0..3) (S^T tiles kt = 0,
+    // 1); V^T rows of the same keys come from two transpose reads.
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
+      const int off = 16 * ((2 * dt + ((lq & 3) >> 1)) ^ swv) + 8 * (lq & 1);
+      const f16x4_t v0 = lds_read_tr(tv + vrow * kRowBytes + off);
+      const f16x4_t v1 = lds_read_tr(tv + (vrow + 16) * kRowBytes + off);
+      const f16x8_t va = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const f16x4_t v0 = lds_read_tr(&tv[(32 * ks + tr_key) * kStride + 16 * dt + tr_dim]);
-        const f16x4_t v1 = lds_read_tr(&tv[(32 * ks + 16 + tr_key) * kStride + 16 * dt + tr_dim]);
-        const f16x8_t va = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt) o[dt][qt] = mfma16(va, ph[qt][ks], o[dt][qt]);
-      }
+      for (int qt = 0; qt < 2; ++qt) o[dt][qt] = mfma16(va, ph[qt], o[dt][qt]);
     }
   };
 
-  if (k0 < k1) {
-    lookup(k0);
-    gload(k0);
-  }
   if (tid < kHeadDim) {
     s_vscale[0][tid] = 1.f;
     s_vmax[tid] = 0u;
   }
-  if (tid < 2) s_flag[tid] = -1;
+  if (tid < kStages) s_flag[tid] = -1;
   lds_sync();
-  if (k0 < k1) {
-    lstore(0, k0);
-    if (k0 + kKeyTile < k1) gload(k0 + kKeyTile);
-    lds_sync();
+  // The Q operand has landed before the pipeline starts: no load that
+  // writes registers is pending inside the loop, whose waits then only
+  // follow the tile loads.
+  __builtin_amdgcn_s_waitcnt(wait_vm(0));
+  if (ntiles > 0) {
+    // Pipeline start: page ids of tiles 0 .. 2 (waited for), then for tiles
+    // i = 0 .. kStages - 2 the page id of tile i + 3 and the rows of tile i.
+    if constexpr (kPaged) {
+      issue_page(0);
+      issue_page(1);
+      issue_page(2);
+      __builtin_amdgcn_s_waitcnt(wait_vm(0));
+      compiler_fence();
+    }
+#pragma unroll
+    for (int i = 0; i < kStages - 1; ++i) {
+      issue_page(i + 3);
+      issue(i);
+    }
   }
-  int buf = 0;
-  for (int t0 = k0; t0 < k1; t0 += kKeyTile) {
-    if (t0 + kKeyTile > cut)
-      tile(t0, buf, std::true_type{});
+  for (int ti = 0; ti < ntiles; ++ti) {
+    const int st = ti & (kStages - 1);
+    // This wave's rows of tile ti (and the page id of tile ti + 3) have
+    // landed: convert its V pieces, then one barrier publishes the whole
+    // tile. Every wave finished reading stage (ti - 1) % kStages before it,
+    // so that stage takes tile ti + kStages - 1; phantom tiles past the end
+    // read nothing (empty resources) and keep the load count per tile fixed.
+    __builtin_amdgcn_s_waitcnt(kWaitTile);
+    compiler_fence();
+    convert(st, k0 + ti * kKeyTile);
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    compiler_fence();
+    __builtin_amdgcn_s_barrier();
+    compiler_fence();
+    issue_page(ti + kStages + 2);
+    issue(ti + kStages - 1);
+    if (k0 + ti * kKeyTile + kKeyTile > cut)
+      tile(ti, st, std::true_type{});
     else
-      tile(t0, buf, std::false_type{});
-    // The other buffer was last read in the previous tile, before the
-    // barrier that ended it: fill it with the next tile, start the loads of
-    // the one after, and publish.
-    if (t0 + kKeyTile < k1) lstore(buf ^ 1, t0 + kKeyTile);
-    if (t0 + 2 * kKeyTile < k1) gload(t0 + 2 * kKeyTile);
-    lds_sync();
-    buf ^= 1;
+      tile(ti, st, std::false_type{});
   }
+  // No load may still be writing LDS when the workgroup ends.
+  __builtin_amdgcn_s_waitcnt(wait_vm(0));
+  compiler_fence();
 
   // This split's normalised partial rows and their lse (log2 domain).
 #pragma unroll
@@ -511,10 +635,18 @@ hipError_t launch_rectify(const RectifyArgs& a, hipStream_t stream) {
   }
   const int32_t nq = rectify_num_qblocks(a.group, a.f);
   const dim3 grid(a.num_splits, nq, a.c.batch * a.c.kv_heads);
-  if (waves_for_rows(a.group * a.f) == 8)
-    hipLaunchKernelGGL(k_rectify_attn<8>, grid, dim3(512), 0, stream, a);
-  else
-    hipLaunchKernelGGL(k_rectify_attn<4>, grid, dim3(256), 0, stream, a);
+  const bool paged = a.c.table != nullptr;
+  if (waves_for_rows(a.group * a.f) == 8) {
+    if (paged)
+      hipLaunchKernelGGL((k_rectify_attn<8, true>), grid, dim3(512), 0, stream, a);
+    else
+      hipLaunchKernelGGL((k_rectify_attn<8, false>), grid, dim3(512), 0, stream, a);
+  } else {
+    if (paged)
+      hipLaunchKernelGGL((k_rectify_attn<4, true>), grid, dim3(256), 0, stream, a);
+    else
+      hipLaunchKernelGGL((k_rectify_attn<4, false>), grid, dim3(256), 0, stream, a);
+  }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (a.num_splits == 1) return hipSuccess;  // the attention kernel wrote out / lse
