@@ -417,6 +417,10 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) sacc[kt][qt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    // The matrix-core sections run at wave priority 1 (the softmax and the
+    // conversion at 0): a SIMD's other wave, at another point of its tile,
+    // then fills the gaps with vector work instead of delaying the MFMAs.
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
 #pragma unroll
@@ -428,6 +432,7 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
       }
     }
 
+    __builtin_amdgcn_s_setprio(0);
     f16x8_t ph[2];  // [qt]: keys 4 j + (0..3), then 16 + 4 j + (0..3)
 #pragma unroll
     for (int qt = 0; qt < 2; ++qt) {
@@ -479,6 +484,7 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
     }
 
     if (__builtin_amdgcn_readfirstlane(flag) == t0) fix_tile(ti, st);
+    __builtin_amdgcn_s_setprio(1);
 
     // P^T: lane keys 4 j + (0..3) then 16 + 4 j + (0..3) (S^T tiles kt = 0,
     // 1); V^T rows of the same keys come from two transpose reads.
@@ -491,6 +497,7 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) o[dt][qt] = mfma16(va, ph[qt], o[dt][qt]);
     }
+    __builtin_amdgcn_s_setprio(0);
   };
 
   if (tid < kHeadDim) {
