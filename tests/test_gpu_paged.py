@@ -201,3 +201,87 @@ def test_rectify_per_request_phases(paged):
                 assert np.array_equal(O.bf16_to_f64(down(cache.kmax)[bi, hi, :M]), st.kmax[bi, hi, :M])
     assert rect_done == [2, 2, 3], rect_done   # every request rectified at its own steps
     assert swaps <= 6
+
+
+# ------------------------------------------------- table entries outside the pool
+
+def test_out_of_pool_entries_are_isolated():
+    """A sequence whose block table names pages outside the pool (negative or
+    past num_pages) gets unspecified results, but those entries are never
+    dereferenced: every call completes, and the other sequences' cache rows,
+    summaries, selections, decode outputs and rectified rows are
+    bit-identical to a run whose table is intact."""
+    b, g = 16, 4
+    w = W.LONG_64K.with_(batch=3, num_q_heads=2 * g, num_kv_heads=2, seq_len=600, min_tokens=4 * b,
+                         block_size=b, seed_tag="oob")
+    cap = 768
+    lens = [600, 530, 480]
+    steps, f = 6, 3
+    final = [x + steps for x in lens]
+    K, V = W.kv_cache(w, capacity=cap)
+    ok = make_paged_cache(K, V, b, final, seed=11)
+    bad = make_paged_cache(K, V, b, final, seed=11)
+    tab = bad.block_table.cpu().numpy().copy()
+    P = bad.k.shape[0]
+    # blocks inside sequence 1's history, its open block and the block the
+    # appends move into
+    tab[1, 3], tab[1, 20], tab[1, 33], tab[1, 34] = P + 3, -7, P, 1 << 30
+    bad.block_table.copy_(torch.from_numpy(tab))
+    keep = [0, 2]
+    l_ok, l_bad = i32(lens), i32(lens)
+    R.block_summarize(ok, l_ok)
+    R.block_summarize(bad, l_bad)
+    ws = [R.Workspace() for _ in range(4)]
+    bound = max(lens)
+    for step in range(steps):
+        kn, vn = W.decode_kv(w, step)
+        q = W.decode_query(w, step)
+        i1, n1 = R.append_select(ok, up(kn), up(vn), up(q), l_ok, bound, w.sparsity, w.min_blocks, 1,
+                                 workspace=ws[0])
+        i2, n2 = R.append_select(bad, up(kn), up(vn), up(q), l_bad, bound, w.sparsity, w.min_blocks, 1,
+                                 workspace=ws[1])
+        bound += 1
+        o1, s1 = R.sparse_decode(ok, up(q), l_ok, i1, n1, workspace=ws[2])
+        o2, s2 = R.sparse_decode(bad, up(q), l_bad, i2, n2, workspace=ws[3])
+        torch.cuda.synchronize()
+        assert torch.equal(l_ok, l_bad), step
+        for bi in keep:
+            assert torch.equal(n1[bi], n2[bi]) and torch.equal(i1[bi], i2[bi]), (step, bi)
+            assert torch.equal(o1[bi], o2[bi]) and torch.equal(s1[bi], s2[bi]), (step, bi)
+        if (step + 1) % f == 0:
+            cur = l_ok.cpu().tolist()
+            kc, vc = unpage(ok, cur)
+            last_k = np.stack([np.stack([kc[bi, hi, cur[bi] - f:cur[bi]] for hi in range(2)]) for bi in range(3)])
+            last_v = np.stack([np.stack([vc[bi, hi, cur[bi] - f:cur[bi]] for hi in range(2)]) for bi in range(3)])
+            qf, kf, vf = W.rectify_inputs(w, step, last_k, last_v, f)
+            r1, t1 = R.dense_rectify(ok, up(qf), up(kf), up(vf), l_ok, bound)
+            r2, t2 = R.dense_rectify(bad, up(qf), up(kf), up(vf), l_bad, bound)
+            torch.cuda.synchronize()
+            for bi in keep:
+                assert torch.equal(r1[bi], r2[bi]) and torch.equal(t1[bi], t2[bi]), (step, bi)
+    cur = l_ok.cpu().tolist()
+    k1, v1 = unpage(ok, cur)
+    # sequence 1's valid pages and every other sequence's rows
+    k2, v2 = unpage_valid(bad, cur)
+    for bi in keep:
+        assert np.array_equal(k1[bi, :, :cur[bi]], k2[bi, :, :cur[bi]])
+        assert np.array_equal(v1[bi, :, :cur[bi]], v2[bi, :, :cur[bi]])
+        assert torch.equal(ok.kmin[bi], bad.kmin[bi]) and torch.equal(ok.kmax[bi], bad.kmax[bi])
+
+
+def unpage_valid(cache, lens):
+    """unpage() that leaves the rows of blocks whose table entry lies
+    outside the pool at zero."""
+    table = cache.block_table.cpu().numpy()
+    Kp, Vp = down(cache.k), down(cache.v)
+    B, mb = table.shape
+    b = cache.block_size
+    K = np.zeros((B, Kp.shape[1], mb * b, Kp.shape[3]), dtype=np.uint16)
+    V = np.zeros_like(K)
+    for bi in range(B):
+        for m in range(-(-int(lens[bi]) // b)):
+            p = table[bi, m]
+            if 0 <= p < Kp.shape[0]:
+                K[bi, :, m * b:(m + 1) * b] = Kp[p]
+                V[bi, :, m * b:(m + 1) * b] = Vp[p]
+    return K, V
