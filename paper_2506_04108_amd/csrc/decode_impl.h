@@ -579,10 +579,13 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
   }
   lds_sync();
 
-  // Merge the NE row-group states: this split's normalised partial and its
-  // lse (log2 domain) for items it = tid + k NT of two dims each (head
-  // it / 64, dims 2 (it % 64) ..). A wave's items share one head, so the
-  // per-head references and sums are broadcast vector reads.
+  // Merge the NE = 16 row-group states: this split's normalised partial and
+  // its lse (log2 domain) for items it = tid + k NT of two dims each (head
+  // it / 64, dims 2 (it % 64) ..). A wave's items share one head: each
+  // 16-lane row holds the head's 16 states (lane e: state e), takes their
+  // maximum and the weighted sum of l with DPP, and the 16 weights reach
+  // every lane as wave-uniform values (one exp per lane, not 16).
+  static_assert(NE == 16, "one row-group state per lane of a 16-lane row");
   constexpr int NT2 = 64 * NW;
   constexpr int kItems = (G * 64 + NT2 - 1) / NT2;
   f2_t val[kItems];
@@ -592,25 +595,20 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
     const int it = tid + k * NT2;
     val[k] = f2_t{0.f, 0.f};
     lg[k] = ninf;
-    if (it < G * 64) {
-      const int h = it / 64, d = 2 * (it % 64);
-      float mv[NE], lv[NE];
-#pragma unroll
-      for (int e = 0; e < NE; e += 4) {
-        const f4_t m4 = *reinterpret_cast<const f4_t*>(&lds.rm[h][e]);
-        const f4_t l4 = *reinterpret_cast<const f4_t*>(&lds.rl[h][e]);
-        mv[e] = m4.x; mv[e + 1] = m4.y; mv[e + 2] = m4.z; mv[e + 3] = m4.w;
-        lv[e] = l4.x; lv[e + 1] = l4.y; lv[e + 2] = l4.z; lv[e + 3] = l4.w;
-      }
-      float mx = ninf;
-#pragma unroll
-      for (int e = 0; e < NE; ++e) mx = fmaxf(mx, mv[e]);
-      float lsum = 0.f;
+    if (k * NT2 + wave * 64 < G * 64) {  // uniform across the wave
+      const int h = it / 64, d = 2 * (it % 64), e0 = lane & 15;
+      const float me = lds.rm[h][e0], le = lds.rl[h][e0];
+      float mx = me;
+      mx = fmaxf(mx, dpp<kDppXor1>(mx));
+      mx = fmaxf(mx, dpp<kDppXor2>(mx));
+      mx = fmaxf(mx, dpp<kDppHalfMirror>(mx));
+      mx = fmaxf(mx, dpp<kDppMirror>(mx));
+      const float fe = me == ninf ? 0.f : fast_exp2(me - mx);
+      const float lsum = row16_sum(le * fe);
       f2_t x = {0.f, 0.f};
 #pragma unroll
       for (int e = 0; e < NE; ++e) {
-        const float f = mv[e] == ninf ? 0.f : fast_exp2(mv[e] - mx);
-        lsum = fmaf(lv[e], f, lsum);
+        const float f = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, fe), e));
         x += f * *reinterpret_cast<const f2_t*>(&lds.racc[e / RG][e % RG][h][d]);
       }
       if (lsum > 0.f) {
