@@ -61,10 +61,14 @@ constexpr int kRowsPerWave = 32;
 template <int kWaves>
 constexpr int rows_per_wg() { return kWaves * kRowsPerWave; }
 __host__ __device__ constexpr int waves_for_rows(int rows) { return rows > 128 ? 8 : 4; }
-constexpr int kKeyTile = 32;                      // keys per tile
+// Keys per tile: 32 for 4-wave workgroups (two per CU share the LDS), 64 for
+// 8-wave ones (one per CU: fewer barriers, load issues and softmax
+// bookkeeping per key where the matrix work dominates).
+template <int kWaves>
+constexpr int key_tile() { return kWaves == 8 ? 64 : 32; }
+constexpr int kMaxKeyTile = 64;
 constexpr int kStages = 4;                        // LDS stages: the tile computed, three in flight
 constexpr int kRowBytes = kHeadDim * 2;           // one K or V row (16-bit values)
-constexpr int kTileBytes = kKeyTile * kRowBytes;  // 8 KB of K and 8 KB of V per tile
 constexpr int kPageRing = 8;                      // page ids per wave held in LDS
 typedef int32_t i32x4_t __attribute__((ext_vector_type(4)));
 
@@ -163,7 +167,9 @@ __global__ __launch_bounds__(256) void k_rectify_rows(RectifyArgs a) {
 template <int kWaves, bool kPaged>
 __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_rectify_attn(RectifyArgs a) {
   constexpr int kRowsPerWg = rows_per_wg<kWaves>();
-  constexpr int kLoadRows = kKeyTile / kWaves;   // tile rows whose K and V each wave loads
+  constexpr int kKT = key_tile<kWaves>();
+  constexpr int kTileBytes = kKT * kRowBytes;    // K (and V) bytes of a tile
+  constexpr int kLoadRows = kKT / kWaves;        // tile rows whose K and V each wave loads
   constexpr int kLoads = kLoadRows / 4;          // 1 KB load instructions per wave, tensor and tile
   // Loads a wave issues per tile (K, V and, paged, one page id). When tile t
   // is waited for, those of tiles t + 1 and t + 2 may still be in flight
@@ -211,7 +217,7 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
   // skip them instead of masking them.
   const int last_row = min(R - 1, (qblk + 1) * kRowsPerWg - 1);
   const int k1 = seq_ok ? min(min(k0 + a.chunk, L), L - f + last_row / G + 1) : k0;
-  const int ntiles = k1 > k0 ? (k1 - k0 + kKeyTile - 1) / kKeyTile : 0;
+  const int ntiles = k1 > k0 ? (k1 - k0 + kKT - 1) / kKT : 0;
   const int j = lane >> 4, lq = lane & 15;
   const int row_base = qblk * kRowsPerWg + wave * kRowsPerWave;
   const float ninf = -__builtin_inff();
@@ -255,7 +261,7 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
   // Buffer resources over this wave's rows of tile ti: rows at or past k1
   // and rows of a page outside the pool fall outside them and read as zero.
   auto tile_src = [&](int ti, const uint16_t*& pk, const uint16_t*& pv, int& nrec) __attribute__((always_inline)) {
-    const int key = k0 + ti * kKeyTile + wrow;
+    const int key = k0 + ti * kKT + wrow;
     nrec = min(max(k1 - key, 0), kLoadRows) * kRowBytes;
     size_t row;
     if constexpr (kPaged) {
@@ -290,7 +296,7 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
   // the ring; blocks past the table read as page 0 (only tiles past k1 ask).
   auto issue_page = [&](int ti) __attribute__((always_inline)) {
     if constexpr (kPaged) {
-      const int mb = (k0 + ti * kKeyTile + wrow) >> a.c.log2_block;
+      const int mb = (k0 + ti * kKT + wrow) >> a.c.log2_block;
       const i32x4_t rt = rsrc_words(a.c.table + (size_t)bb * a.c.max_blocks, a.c.max_blocks * 4);
       const uint32_t dst = __builtin_amdgcn_readfirstlane(lds_addr(&s_page[wave][ti & (kPageRing - 1)]));
       if (lane == 0) lds_load4(dst, (uint32_t)mb * 4, rt);
@@ -408,13 +414,14 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
   // and the split end per key.
   auto tile = [&](int ti, int st, auto masked) __attribute__((always_inline)) {
     constexpr bool kMasked = decltype(masked)::value;
-    const int t0 = k0 + ti * kKeyTile;
+    constexpr int KT16 = kKT / 16, KT32 = kKT / 32;
+    const int t0 = k0 + ti * kKT;
     const uint8_t* tk = s_kv[st][0];
     const uint8_t* tv = s_kv[st][1];
     const int flag = s_flag[st];  // read now, used after the scores
-    f32x4_t sacc[2][2];
+    f32x4_t sacc[KT16][2];
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < KT16; ++kt)
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) sacc[kt][qt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     // The matrix-core sections run at wave priority 1 (the softmax and the
@@ -424,7 +431,7 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
+      for (int kt = 0; kt < KT16; ++kt) {
         const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(
             tk + (16 * kt + lq) * kRowBytes + 16 * ((4 * s + j) ^ swq));
 #pragma unroll
@@ -433,13 +440,13 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
     }
 
     __builtin_amdgcn_s_setprio(0);
-    f16x8_t ph[2];  // [qt]: keys 4 j + (0..3), then 16 + 4 j + (0..3)
+    f16x8_t ph[2][KT32];  // [qt][32-key step ks]: keys 32 ks + 4 j + (0..3), then + 16
 #pragma unroll
     for (int qt = 0; qt < 2; ++qt) {
-      float x[8];
+      float x[4 * KT16];
       float tmax = ninf;
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < KT16; ++kt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           float y = sacc[kt][qt][i];
@@ -454,8 +461,8 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
       // The reference m moves only when the tile's maximum exceeds it by
       // more than kRefSlack, so the accumulator rescale is rare; every
       // weight stays <= 2^kRefSlack, well inside fp16 and fp32 range, and
-      // the normalisation by l uses the same reference. A query's 32 keys
-      // sit in four lanes (lq + 16 j): the row maximum across them is only
+      // the normalisation by l uses the same reference. A query's keys of
+      // the tile sit in four lanes (lq + 16 j): the row maximum across them is only
       // needed when one of them exceeds the reference, so the cross-lane
       // reduction runs on those (rare) tiles only.
       float alpha = 1.f;
@@ -471,10 +478,10 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
       const float mref = m[qt] == ninf ? 0.f : m[qt];
       float ps = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
+      for (int e = 0; e < 4 * KT16; ++e) {
         const float pe = fast_exp2(fmaf(x[e], c, -mref));
         ps += pe;
-        ph[qt][e] = (_Float16)pe;
+        ph[qt][e >> 3][e & 7] = (_Float16)pe;
       }
       l[qt] = fmaf(l[qt], alpha, ps);
       if (__any(alpha != 1.f)) {
@@ -486,16 +493,21 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
     if (__builtin_amdgcn_readfirstlane(flag) == t0) fix_tile(ti, st);
     __builtin_amdgcn_s_setprio(1);
 
-    // P^T: lane keys 4 j + (0..3) then 16 + 4 j + (0..3) (S^T tiles kt = 0,
-    // 1); V^T rows of the same keys come from two transpose reads.
+    // P^T for 32-key step ks: lane keys 32 ks + 4 j + (0..3) then
+    // 32 ks + 16 + 4 j + (0..3) (S^T tiles kt = 2 ks, 2 ks + 1); V^T rows of
+    // the same keys come from two transpose reads (rows 32 ks + r keep the
+    // swizzle of row r).
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
       const int off = 16 * ((2 * dt + ((lq & 3) >> 1)) ^ swv) + 8 * (lq & 1);
-      const f16x4_t v0 = lds_read_tr(tv + vrow * kRowBytes + off);
-      const f16x4_t v1 = lds_read_tr(tv + (vrow + 16) * kRowBytes + off);
-      const f16x8_t va = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt) o[dt][qt] = mfma16(va, ph[qt], o[dt][qt]);
+      for (int ks = 0; ks < KT32; ++ks) {
+        const f16x4_t v0 = lds_read_tr(tv + (32 * ks + vrow) * kRowBytes + off);
+        const f16x4_t v1 = lds_read_tr(tv + (32 * ks + vrow + 16) * kRowBytes + off);
+        const f16x8_t va = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) o[dt][qt] = mfma16(va, ph[qt][ks], o[dt][qt]);
+      }
     }
     __builtin_amdgcn_s_setprio(0);
   };
@@ -535,14 +547,14 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
     // read nothing (empty resources) and keep the load count per tile fixed.
     __builtin_amdgcn_s_waitcnt(kWaitTile);
     compiler_fence();
-    convert(st, k0 + ti * kKeyTile);
+    convert(st, k0 + ti * kKT);
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     compiler_fence();
     __builtin_amdgcn_s_barrier();
     compiler_fence();
     issue_page(ti + kStages + 2);
     issue(ti + kStages - 1);
-    if (k0 + ti * kKeyTile + kKeyTile > cut)
+    if (k0 + ti * kKT + kKT > cut)
       tile(ti, st, std::true_type{});
     else
       tile(ti, st, std::false_type{});
@@ -623,11 +635,11 @@ int32_t rectify_chunk(int32_t batch, int32_t kv_heads, int32_t nqblk, int32_t ma
   int64_t target = (512 + wgs - 1) / wgs;
   if (target < 1) target = 1;
   int64_t chunk = (max_seq_len + target - 1) / target;
-  chunk = (chunk + kKeyTile - 1) / kKeyTile * kKeyTile;
+  chunk = (chunk + kMaxKeyTile - 1) / kMaxKeyTile * kMaxKeyTile;
   if (chunk < 512) chunk = 512;
   // At most kMaxRectSplits splits, so the combine's weights fit in LDS.
   const int64_t least = ((int64_t)max_seq_len + kMaxRectSplits - 1) / kMaxRectSplits;
-  if (chunk < least) chunk = (least + kKeyTile - 1) / kKeyTile * kKeyTile;
+  if (chunk < least) chunk = (least + kMaxKeyTile - 1) / kMaxKeyTile * kMaxKeyTile;
   return (int32_t)chunk;
 }
 
