@@ -9,8 +9,8 @@
 // Grid (num_splits, ceil(R / rows), batch * kv_heads) with 4 waves (rows =
 // 128, windows of up to 128 rows) or 8 waves (rows = 256, longer windows
 // such as prefill) per workgroup, each wave owning 32 query rows (two
-// 16-row tiles). A workgroup walks its key range in tiles of 32 keys
-// through four LDS stages: K and V rows go from HBM straight into LDS
+// 16-row tiles). A workgroup walks its key range in tiles of 32 keys (4
+// waves) or 64 keys (8 waves) through four LDS stages: K and V rows go from HBM straight into LDS
 // (buffer loads with the LDS destination, no registers), three tiles ahead
 // of the one being computed, and one barrier per tile publishes a tile and
 // frees the stage read before it. Per tile and wave:
