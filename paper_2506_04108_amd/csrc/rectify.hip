@@ -600,7 +600,7 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
 
 // Log-sum-exp merge of the splits (Alg. 2, "Combine") spread over many
 // workgroups: each takes kCombineRows query rows of one group.
-constexpr int kCombineRows = 2;
+constexpr int kCombineRows = 8;
 
 __global__ __launch_bounds__(256) void k_rectify_combine(RectifyArgs a) {
   __shared__ float s_w[kMaxRectSplits * kCombineRows];
