@@ -105,17 +105,37 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 }
 // Buffer loads straight into LDS (no registers): lane i's 16 (4) bytes at
 // offset voff land at LDS byte address lds + 16 i (lds + 4 i); M0 carries
-// lds. Written as assembly so that the compiler does not track them: it
-// would otherwise make every V transpose read wait for all of them. Their
-// completion is ordered by hand (vmcnt waits, then a barrier). The kernels
-// that use them give M0 no other use.
-__device__ __forceinline__ void lds_load16(uint32_t lds, uint32_t voff, i32x4_t rs) {
-  __asm__ volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen nt lds"
-                   :: "s"(lds), "v"(voff), "s"(rs) : "memory");
+// the LDS address. Written as assembly so that the compiler does not track
+// them: it would otherwise make every V transpose read wait for all of them.
+// Their completion is ordered by hand (vmcnt waits, then a barrier). M0 is
+// saved and restored around each group of loads, so whatever the compiler
+// keeps in it survives; one wait state follows each write of M0 that a load
+// reads.
+//
+// A wave's rows of one tile: two 1 KB loads of K (rows +0 and +4 of its
+// LDS rows, global offsets voff0 / voff1 in rk) and the same two of V (LDS
+// address + kTile, rv).
+template <int kTile>
+__device__ __forceinline__ void lds_load_rows8(uint32_t lds, uint32_t voff0, uint32_t voff1, i32x4_t rk,
+                                               i32x4_t rv) {
+  uint32_t saved;
+  __asm__ volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\ts_nop 0\n\tbuffer_load_dwordx4 %2, %4, 0 offen nt lds\n\t"
+      "s_add_i32 m0, %1, %6\n\ts_nop 0\n\tbuffer_load_dwordx4 %2, %5, 0 offen nt lds\n\t"
+      "s_add_i32 m0, %1, 1024\n\ts_nop 0\n\tbuffer_load_dwordx4 %3, %4, 0 offen nt lds\n\t"
+      "s_add_i32 m0, %1, %7\n\ts_nop 0\n\tbuffer_load_dwordx4 %3, %5, 0 offen nt lds\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds), "v"(voff0), "v"(voff1), "s"(rk), "s"(rv), "n"(kTile), "n"(kTile + 1024)
+      : "memory", "scc");
 }
 __device__ __forceinline__ void lds_load4(uint32_t lds, uint32_t voff, i32x4_t rs) {
-  __asm__ volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
-                   :: "s"(lds), "v"(voff), "s"(rs) : "memory");
+  uint32_t saved;
+  __asm__ volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+      "buffer_load_dword %2, %3, 0 offen lds\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved) : "s"(lds), "v"(voff), "s"(rs) : "memory");
 }
 // Keeps the compiler from moving memory accesses across this point; the
 // hardware ordering comes from the explicit waits and barriers around it.
@@ -285,12 +305,8 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
     tile_src(ti, pk, pv, nrec);
     const i32x4_t rk = rsrc_words(pk, nrec), rv = rsrc_words(pv, nrec);
     const uint32_t dk = lds_kv + (uint32_t)((ti & (kStages - 1)) * 2 * kTileBytes + wrow * kRowBytes);
-#pragma unroll
-    for (int e = 0; e < kLoads; ++e) {
-      const uint32_t off = src_off(e);
-      lds_load16(dk + 4 * e * kRowBytes, off, rk);
-      lds_load16(dk + kTileBytes + 4 * e * kRowBytes, off, rv);
-    }
+    static_assert(kLoads == 2, "eight rows per wave and tile");
+    lds_load_rows8<kTileBytes>(dk, src_off(0), src_off(1), rk, rv);
   };
   // Page id of this wave's rows of tile ti (its rows lie in one block), into
   // the ring; blocks past the table read as page 0 (only tiles past k1 ask).
