@@ -344,7 +344,7 @@ __device__ __forceinline__ int ld_i32(const int32_t* p) {
 // are all requested before anything waits for one of them (vector loads, so
 // one wait covers them), which leaves one memory round trip between the
 // kernel arguments and the first K / V loads.
-template <int G, int BS, int NW, bool kCoherent, int kDepth = 2>
+template <int G, int BS, int NW, bool kCoherent, int kDepth>
 __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk, int split,
                                              const int32_t* lens, bool append, DecodeLds<G, NW>& lds,
                                              bool empty = false) {

@@ -130,7 +130,7 @@ __global__ __launch_bounds__(kTopnThreads) void k_topn(SelectArgs a) {
 // (Eq. 5) in one kernel. Grid (ceil(max_blocks_seq / blocks_per_wg), kv
 // heads, batch), about one 16-wave workgroup per CU. Each workgroup streams
 // the summaries of its block range (score_range): lane (r, c) handles dims [8c, 8c + 8) of
-// 16-block tiles, so each wave-wide load is four whole 256-byte summary rows,
+// 8-block tiles, so each wave-wide load is four whole 256-byte summary rows,
 // and the next tile's loads are in flight while one is scored. Per dimension
 // the larger of q*kmax and q*kmin is the product with kmax when q >= 0 and
 // with kmin otherwise (exactly, as fp32 rounding is monotone), so the
@@ -141,14 +141,7 @@ __global__ __launch_bounds__(kTopnThreads) void k_topn(SelectArgs a) {
 // ticket use agent scope (write-through stores, coherent loads, a relaxed
 // atomic after the stores are acknowledged), so no cache writeback is needed
 // between workgroups.
-//
-// PF: tiles in flight per wave beyond the one being scored. One keeps the
-// next tile's loads going while a tile is scored; where a range holds at
-// most three tiles per wave (long groups cut into many short ranges, e.g.
-// 256K at batch 1) that would request two thirds of the data set at once,
-// which was measured slower than one tile at a time (selection 25.2 against
-// 24.2 us at 256K; the same at 64K, four tiles per wave).
-template <int NJ, int PF>
+template <int NJ>
 __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t s_hist[kBins2];
   __shared__ __attribute__((aligned(16))) float s_score[kMaxBlocksPerWg];
@@ -157,7 +150,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
   const int tid = threadIdx.x;
   const int hk = blockIdx.y, bb = blockIdx.z;
   const size_t grp = (size_t)bb * a.c.kv_heads + hk;
-  const RangeInfo ri = score_range<kSelWaves, PF, false, window_lists(NJ, kSelThreads)>(a, bb, hk, blockIdx.x, gridDim.x, s_hist, s_score);
+  const RangeInfo ri = score_range<kSelWaves, 1, false, window_lists(NJ, kSelThreads)>(a, bb, hk, blockIdx.x, gridDim.x, s_hist, s_score);
   if (!a.fused) return;
   __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
@@ -177,29 +170,22 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
     // Keys per thread of the fused top-n: the smallest instantiation that
     // holds the longest group (every group's M <= max_blocks_seq).
     const int per = (a.max_blocks_seq + kSelThreads - 1) / kSelThreads;
-    const bool short_ranges = ((a.blocks_per_wg + 15) / 16 + kSelWaves - 1) / kSelWaves <= 3;
     if (per <= 4)
-      hipLaunchKernelGGL((k_select<4, 1>), grid, dim3(kSelThreads), 0, stream, a);
+      hipLaunchKernelGGL((k_select<4>), grid, dim3(kSelThreads), 0, stream, a);
     else if (per <= 5)
-      hipLaunchKernelGGL((k_select<5, 1>), grid, dim3(kSelThreads), 0, stream, a);
+      hipLaunchKernelGGL((k_select<5>), grid, dim3(kSelThreads), 0, stream, a);
     else if (per <= 6)
-      hipLaunchKernelGGL((k_select<6, 1>), grid, dim3(kSelThreads), 0, stream, a);
+      hipLaunchKernelGGL((k_select<6>), grid, dim3(kSelThreads), 0, stream, a);
     else if (per <= 8)
-      hipLaunchKernelGGL((k_select<8, 1>), grid, dim3(kSelThreads), 0, stream, a);
+      hipLaunchKernelGGL((k_select<8>), grid, dim3(kSelThreads), 0, stream, a);
     else if (per <= 12)
-      hipLaunchKernelGGL((k_select<12, 1>), grid, dim3(kSelThreads), 0, stream, a);
-    else if (per <= 16 && short_ranges)
-      hipLaunchKernelGGL((k_select<16, 0>), grid, dim3(kSelThreads), 0, stream, a);
+      hipLaunchKernelGGL((k_select<12>), grid, dim3(kSelThreads), 0, stream, a);
     else if (per <= 16)
-      hipLaunchKernelGGL((k_select<16, 1>), grid, dim3(kSelThreads), 0, stream, a);
-    else if (per <= 24 && short_ranges)
-      hipLaunchKernelGGL((k_select<24, 0>), grid, dim3(kSelThreads), 0, stream, a);
+      hipLaunchKernelGGL((k_select<16>), grid, dim3(kSelThreads), 0, stream, a);
     else if (per <= 24)
-      hipLaunchKernelGGL((k_select<24, 1>), grid, dim3(kSelThreads), 0, stream, a);
-    else if (short_ranges)
-      hipLaunchKernelGGL((k_select<32, 0>), grid, dim3(kSelThreads), 0, stream, a);
+      hipLaunchKernelGGL((k_select<24>), grid, dim3(kSelThreads), 0, stream, a);
     else
-      hipLaunchKernelGGL((k_select<32, 1>), grid, dim3(kSelThreads), 0, stream, a);
+      hipLaunchKernelGGL((k_select<32>), grid, dim3(kSelThreads), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (a.fused) return hipSuccess;
@@ -213,8 +199,8 @@ int32_t select_fused_max_blocks() { return kMaxSelectBlocks; }
 int32_t select_blocks_per_wg(int32_t batch, int32_t kv_heads, int32_t max_blocks_seq) {
   // About one 16-wave workgroup per CU (256 CUs) in all: a group's blocks are
   // cut into equal ranges of whole 32-block words (so a word of the
-  // above-window bits belongs to one range), at least one 16-block tile per
-  // wave (256 blocks) and at most the LDS staging area.
+  // above-window bits belongs to one range), at least 16 blocks per wave
+  // (256 blocks) and at most the LDS staging area.
   const int64_t groups = (int64_t)batch * kv_heads;
   const int64_t per_group = (256 + groups - 1) / groups;
   int64_t bpw = ((int64_t)max_blocks_seq + per_group - 1) / per_group;

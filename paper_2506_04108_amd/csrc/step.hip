@@ -167,7 +167,7 @@ int32_t step_blocks_per_range(int32_t batch, int32_t kv_heads, int32_t max_block
   // About two score ranges per CU in all (256 CUs), so that groups finish
   // scoring in two rounds and the first round's top-n overlaps the second;
   // whole 32-block words (one word of the above-window bits per range), at
-  // least two 16-block tiles per wave, at most the LDS staging area.
+  // least 32 blocks per wave, at most the LDS staging area.
   const int64_t groups = (int64_t)batch * kv_heads;
   const int64_t per_group = (512 + groups - 1) / groups;
   int64_t bpr = ((int64_t)max_blocks_seq + per_group - 1) / per_group;
