@@ -30,10 +30,11 @@ namespace {
 
 constexpr int kStepWaves = 8;
 constexpr int kStepThreads = 64 * kStepWaves;
-// Chunks in flight per wave in the decode splits: the selection code shares
-// the register budget, so wide groups keep one chunk fewer in flight.
+// Chunks in flight per wave in the decode splits: one, as in the decode
+// kernel (measured against two: 94.3 – 94.6 against 95.5 – 95.8 us per step
+// at 64K, 65.8 – 66.1 against 66.6 us at 256K).
 template <int G>
-constexpr int kStepDepth = G <= 4 ? 2 : 1;
+constexpr int kStepDepth = 1;
 
 // The kernel arguments through a pointer the compiler cannot follow from
 // one call to the next: each phase loads the fields it uses where it uses
