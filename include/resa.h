@@ -241,9 +241,12 @@ size_t resa_decode_workspace_size(int32_t batch, int32_t num_kv_heads,
  * for |v| <= 2^100. num_splits = 0 picks resa_decode_num_splits();
  * explicit counts must lie in [1, 256].
  * One kernel: each split writes a partial into the workspace and the last
- * split of a group to finish merges them. The workspace starts with one merge
- * counter per group: zero-fill it before its first use (resa_workspace_clear
- * or any zeroing allocator); every call leaves the counters at zero again.
+ * split of a group to finish merges them (with 16 or more splits, the last g
+ * splits to finish merge one query head each). The workspace starts with one
+ * merge counter and one count of merged calls per group, which tags the
+ * splits' ready flags of each call: zero-fill it before its first use
+ * (resa_workspace_clear or any zeroing allocator); every call leaves the
+ * counters at zero again and advances the counts.
  * Calls sharing a workspace must be ordered on one stream.
  */
 int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
@@ -260,8 +263,8 @@ int resa_sparse_decode(const resa_kv_cache_t* c, const void* q, int32_t num_q_he
  * workspace: the split partials and merge counters live in a static device
  * array of resa_sparse_decode_noalloc_max_bytes() bytes (4 MiB) that each GPU
  * the library runs on holds until the process ends. The call allocates and
- * frees nothing; it zero-fills the merge counters with a kernel before the
- * decode. The first call on a device looks up that device's array address
+ * frees nothing; it zero-fills the merge counters, call counts and ready
+ * flags with a kernel before the decode. The first call on a device looks up that device's array address
  * (hipGetSymbolAddress). Every call on one GPU shares that GPU's array and
  * the array keeps the last call's contents, so calls that may overlap on one
  * GPU (different streams without ordering, concurrent host threads) race:
@@ -307,7 +310,8 @@ size_t resa_step_workspace_size(int32_t batch, int32_t num_kv_heads, int32_t num
  * overlaps the selection of later groups). The workspace
  * (resa_step_workspace_size) holds claim counters, per-group flags and
  * tickets and the selection hint: zero-fill it before its first use
- * (resa_workspace_clear); every call leaves the counters and flags at zero.
+ * (resa_workspace_clear); every call leaves the counters and the ready flags
+ * at zero (the decode's split flags carry a per-call tag instead).
  * Calls sharing a workspace must be ordered on one stream.
  * Status: the uint32 at byte offset 12 of the workspace becomes 1 if a decode
  * split gave up waiting for its group's selection (a bounded wait, a guard

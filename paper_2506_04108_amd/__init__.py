@@ -135,7 +135,8 @@ class Workspace:
 
     Use one per operation kind. The decode kernel keeps one merge counter per
     group at the start of its workspace and leaves it at zero after every
-    call, so the buffer is cleared only when it is (re)allocated. Calls that
+    call (and a count of merged calls that tags its ready flags), so the
+    buffer is cleared only when it is (re)allocated. Calls that
     share a workspace must be ordered on one stream.
     """
 

@@ -146,18 +146,21 @@ SelectLayout select_layout(int32_t batch, int32_t kv_heads, int32_t max_seq_len,
                              (size_t)resa::select_hist_words(batch, kv_heads, (int32_t)mseq));
 }
 
-// Workspace of resa_sparse_decode: per group a ticket counter and one ready
-// flag per split (zero between calls), then the split partials.
+// Workspace of resa_sparse_decode: per group a ticket counter (zero between
+// calls) and a count of the calls merged so far, one ready flag per split
+// (tagged with that count and the split count, so flags of earlier calls
+// never match and need no reset), then the split partials.
 struct DecodeLayout {
-  size_t counters, flags, lse, o, total;
+  size_t counters, epochs, flags, lse, o, total;
 };
 
 DecodeLayout decode_layout(int32_t batch, int32_t kv_heads, int32_t group, int32_t splits) {
   DecodeLayout d;
   const size_t groups = (size_t)batch * kv_heads;
   d.counters = 0;
-  d.flags = groups * 4;
-  d.lse = round256(groups * 4 + groups * splits * 4);
+  d.epochs = groups * 4;
+  d.flags = (groups * 8 + 7) & ~size_t(7);
+  d.lse = round256(d.flags + groups * splits * 8);
   d.o = d.lse + round256(groups * splits * group * 4);
   d.total = d.o + groups * splits * group * RESA_HEAD_DIM * 4;
   return d;
@@ -442,7 +445,8 @@ int decode_launch(const resa_kv_cache_t* c, const void* q, int32_t num_q_heads,
   a.out = out;
   a.lse = lse;
   a.counters = reinterpret_cast<uint32_t*>(ws + lay.counters);
-  a.flags = reinterpret_cast<uint32_t*>(ws + lay.flags);
+  a.epochs = reinterpret_cast<uint32_t*>(ws + lay.epochs);
+  a.flags = reinterpret_cast<uint64_t*>(ws + lay.flags);
   a.part_lse = reinterpret_cast<float*>(ws + lay.lse);
   a.part_o = reinterpret_cast<float*>(ws + lay.o);
   a.k_new = nullptr;
@@ -649,7 +653,8 @@ int resa_decode_step(const resa_kv_cache_t* c, const void* k_new, const void* v_
   d.out = out;
   d.lse = lse;
   d.counters = reinterpret_cast<uint32_t*>(wdec + lay.d.counters);
-  d.flags = reinterpret_cast<uint32_t*>(wdec + lay.d.flags);
+  d.epochs = reinterpret_cast<uint32_t*>(wdec + lay.d.epochs);
+  d.flags = reinterpret_cast<uint64_t*>(wdec + lay.d.flags);
   d.part_lse = reinterpret_cast<float*>(wdec + lay.d.lse);
   d.part_o = reinterpret_cast<float*>(wdec + lay.d.o);
   d.k_new = sa.k_new;

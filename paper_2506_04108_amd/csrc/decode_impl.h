@@ -284,11 +284,94 @@ __device__ void merge_tail(const DecodeArgs& a, size_t grp, int S, int own, size
     *reinterpret_cast<f4_t*>(a.out + (ob + r) * kHeadDim + 4 * c4) = acc;
     if (c4 == 0 && a.lse) a.lse[ob + r] = wsum > 0.f ? (mx + fast_log2(wsum)) * kLn2 : ninf;
   }
-  // Every other split has published (its flag was seen): the flags and the
-  // ticket counter return to zero for the next call.
-  if (tid < S && tid != own)
-    __hip_atomic_store(a.flags + grp * S + tid, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if (tid == 0) __hip_atomic_store(a.counters + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Wave-wide maximum and sum (every lane active; every lane gets the result):
+// the 16 lanes of each row by DPP, then the rows by lane swaps.
+__device__ __forceinline__ float wave_max_f(float x) {
+  x = fmaxf(x, dpp<kDppXor1>(x));
+  x = fmaxf(x, dpp<kDppXor2>(x));
+  x = fmaxf(x, dpp<kDppHalfMirror>(x));
+  x = fmaxf(x, dpp<kDppMirror>(x));
+  return max_xor32(max_xor16(x));
+}
+__device__ __forceinline__ float wave_sum_f(float x) { return sum_xor32(sum_xor16(row16_sum(x))); }
+
+// Alg. 2, "Combine", for one query head h of the group, by one of the G
+// merging workgroups of a group with many splits (each takes one head, so
+// each loads 1 / G of the partials). Thread i < S forms split i's weight
+// 2^(lse_i - max) once (wave maxima and sums through LDS: two barriers);
+// float4 column u of the head gets T = NT / 32 threads, each summing splits
+// ph, ph + T, ...; the T sums are added through LDS. The merging split's
+// own partial and lse are read from LDS. s_w holds kMaxSplits + 2 NT / 64
+// floats.
+template <int G, int NT>
+__device__ void merge_head(const DecodeArgs& a, size_t grp, int S, int own, int h, size_t ob,
+                           const float* own_o, const float* own_l, float* s_w, f4_t* s_red) {
+  constexpr int U = kHeadDim / 4;
+  constexpr int T = NT / U;
+  constexpr int NWv = NT / 64;
+  static_assert(NT % U == 0 && NT >= kMaxSplits, "merge_head shape");
+  constexpr int kOut = 0x7fffffff;  // an offset past every buffer
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const float ninf = -__builtin_inff();
+  const float* pl = a.part_lse + grp * S * (size_t)G;
+  const float* po = a.part_o + grp * S * (size_t)(G * kHeadDim);
+  const __amdgpu_buffer_rsrc_t rl = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(pl), (short)0, S * G * 4, kBufWord3);
+  const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(po), (short)0, S * G * kHeadDim * 4, kBufWord3);
+  // Every load is unconditional (offsets past the buffer read 0), and the
+  // own split's slot is replaced by its LDS copy when used.
+  const uint32_t lraw = __builtin_amdgcn_raw_buffer_load_b32(rl, tid < S ? (tid * G + h) * 4 : kOut, 0, kSc1);
+  const int u = tid % U, ph = tid / U;
+  const int nb = (S + T * kTailBatch - 1) / (T * kTailBatch);
+  const f4_t own_v = *reinterpret_cast<const f4_t*>(own_o + h * kHeadDim + 4 * u);
+  f4_t part[kTailBatch];
+  auto issue = [&](int b) {
+#pragma unroll
+    for (int k = 0; k < kTailBatch; ++k) {
+      const int sp = b * T * kTailBatch + k * T + ph;
+      part[k] = __builtin_bit_cast(f4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                    ro, sp < S ? ((sp * G + h) * kHeadDim + 4 * u) * 4 : kOut, 0, kSc1));
+    }
+  };
+  issue(0);
+  const float l = tid >= S ? ninf : tid == own ? own_l[h] : __builtin_bit_cast(float, lraw);
+  float* s_max = s_w + kMaxSplits;
+  float* s_sum = s_max + NWv;
+  const float wm = wave_max_f(l);
+  if (lane == 0) s_max[wave] = wm;
+  lds_sync();
+  float mx = s_max[0];
+#pragma unroll
+  for (int w = 1; w < NWv; ++w) mx = fmaxf(mx, s_max[w]);
+  const float wt = l == ninf ? 0.f : fast_exp2(l - mx);
+  if (tid < kMaxSplits) s_w[tid] = wt;
+  const float ws = wave_sum_f(wt);
+  if (lane == 0) s_sum[wave] = ws;
+  lds_sync();
+  float wsum = s_sum[0];
+#pragma unroll
+  for (int w = 1; w < NWv; ++w) wsum += s_sum[w];
+  f4_t acc = {0.f, 0.f, 0.f, 0.f};
+  for (int b = 0; b < nb; ++b) {
+    if (b > 0) issue(b);
+#pragma unroll
+    for (int k = 0; k < kTailBatch; ++k) {
+      const int sp = b * T * kTailBatch + k * T + ph;
+      if (sp < S) acc += s_w[sp] * (sp == own ? own_v : part[k]);
+    }
+  }
+  acc *= wsum > 0.f ? 1.f / wsum : 0.f;
+  s_red[tid] = acc;
+  lds_sync();
+  if (ph == 0) {
+#pragma unroll
+    for (int k = 1; k < T; ++k) acc += s_red[tid + k * U];
+    *reinterpret_cast<f4_t*>(a.out + (ob + h) * kHeadDim + 4 * u) = acc;
+    if (u == 0 && a.lse) a.lse[ob + h] = wsum > 0.f ? (mx + fast_log2(wsum)) * kLn2 : ninf;
+  }
 }
 
 // LDS of one split: per-wave softmax states for the wave merge, the staged
@@ -316,10 +399,13 @@ struct DecodeLds {
   uint32_t ticket;
 };
 
-// Bound of the last split's wait for the other splits' flags (each poll
+// Bound of a merging split's wait for the other splits' flags (each poll
 // sleeps about 64 cycles): the splits it waits for have taken their tickets
 // and are finishing, so the bound is only a guard.
 constexpr uint32_t kFlagSpins = 1u << 22;
+// Splits from which the combine is spread over G merging workgroups, one
+// query head each (merge_head), instead of done by the last one alone.
+constexpr int kSpreadSplits = 16;
 
 template <bool kCoherent>
 __device__ __forceinline__ int ld_i32(const int32_t* p) {
@@ -410,6 +496,9 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
   // (a move into scalar registers) then waits for everything above at once.
   const int n_raw = ld_i32<true>(a.num_sel + grp);
   const int L0 = ld_i32<true>(lens + bb);
+  // Calls of this group merged so far (several splits): tags this call's
+  // ready flags.
+  const uint32_t epoch = S > 1 ? __hip_atomic_load(a.epochs + grp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
   const bool app = append && L0 >= 0 && L0 < a.c.capacity;
   const int L = app ? L0 + 1 : L0;
   const int pos = app ? L0 : -1;
@@ -529,8 +618,8 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
 
   // Tail. With several splits, one thread takes the split's ticket first:
   // its round trip overlaps the merge of the waves below. The ticket only
-  // orders the splits' ends; the split holding the last one waits for the
-  // others' ready flags (their partials are in memory then) and merges.
+  // orders the splits' ends; the merging split(s) (below) wait for the
+  // others' ready flags (their partials are in memory then) and merge.
   // Every K / V load of the loop has been consumed here; the compiler cannot
   // see that (refills are conditional), so without this explicit wait it
   // would place waits in the merge below that also cover the ticket.
@@ -631,7 +720,17 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
   }
   if (tid == 0) lds.ticket = ticket;
   lds_sync();
-  if (lds.ticket != (uint32_t)(S - 1)) {
+  // Merging splits: the one holding the last ticket, or with many splits
+  // those holding the last G tickets, one query head each. A ready flag
+  // carries this call's tag (the group's merged-call count + 1, and S), so
+  // flags left by earlier calls never match and no flag is ever reset; the
+  // split holding the last ticket returns the ticket counter to zero and
+  // advances the count once every ticket is taken.
+  const uint32_t tk = lds.ticket;
+  const bool spread = !kCoherent && G >= 2 && S >= kSpreadSplits;
+  const uint32_t first = spread ? (uint32_t)(S - G) : (uint32_t)(S - 1);
+  const uint64_t tag = ((uint64_t)(epoch + 1u) << 32) | (uint32_t)S;
+  if (spread || tk < first) {
     // Publish: agent-scope stores write through to the level every L2 slice
     // reads (sc1), every thread waits for their acknowledgement, then one
     // thread raises the split's ready flag.
@@ -648,13 +747,13 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
     }
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    if (tid == 0) __hip_atomic_store(a.flags + grp * S + split, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return false;
+    if (tid == 0) __hip_atomic_store(a.flags + grp * S + split, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (tk < first) return false;
   }
 
-  // Alg. 2, "Combine", in the split holding the last ticket: its own partial
-  // stays in LDS; every other split has taken its ticket and is publishing,
-  // so thread t < S waits for split t's flag (agent-scope loads), then the
+  // Alg. 2, "Combine", in a merging split: its own partial stays in LDS;
+  // every other split has taken its ticket and is publishing (or has), so
+  // thread t < S waits for split t's flag (agent-scope loads), then the
   // partials are read with agent-scope loads and merged.
 #pragma unroll
   for (int k = 0; k < kItems; ++k) {
@@ -665,14 +764,26 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
     }
   }
   if (tid < S && tid != split) {
-    const uint32_t* fl = a.flags + grp * S + tid;
+    const uint64_t* fl = a.flags + grp * S + tid;
     uint32_t spins = 0;
-    while (__hip_atomic_load(fl, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u && ++spins < kFlagSpins)
+    while (__hip_atomic_load(fl, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != tag && ++spins < kFlagSpins)
       __builtin_amdgcn_s_sleep(1);
   }
   __syncthreads();
-  merge_tail<G, 64 * NW, kCoherent>(a, grp, S, split, ob, lds.own_o, lds.own_l, lds.w, lds.red);
-  return true;
+  if constexpr (!kCoherent && G >= 2) {
+    if (spread)
+      merge_head<G, 64 * NW>(a, grp, S, split, (int)(tk - first), ob, lds.own_o, lds.own_l, lds.w, lds.red);
+    else
+      merge_tail<G, 64 * NW, kCoherent>(a, grp, S, split, ob, lds.own_o, lds.own_l, lds.w, lds.red);
+  } else {
+    merge_tail<G, 64 * NW, kCoherent>(a, grp, S, split, ob, lds.own_o, lds.own_l, lds.w, lds.red);
+  }
+  const bool last = tk == (uint32_t)(S - 1);
+  if (last && tid == 0) {
+    __hip_atomic_store(a.counters + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(a.epochs + grp, epoch + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  return last;
 }
 
 }  // namespace

@@ -89,7 +89,8 @@ struct DecodeArgs {
   float* part_o;               // [B, Hkv, S, G, D]
   float* part_lse;             // [B, Hkv, S, G]
   uint32_t* counters;          // [B, Hkv] split tickets, zero between calls
-  uint32_t* flags;             // [B, Hkv, S] split partial published, zero between calls
+  uint32_t* epochs;            // [B, Hkv] merged calls so far (kept from call to call)
+  uint64_t* flags;             // [B, Hkv, S] split partial published: (epoch + 1) << 32 | S
   const uint16_t* k_new;       // fused step: [B, Hkv, D] token appended in the same launch
   const uint16_t* v_new;
 };

@@ -428,14 +428,20 @@ def test_decode_edge_cases():
 
 def test_decode_reused_workspace_many_splits():
     """Consecutive calls on one workspace with different queries, block sets
-    and split counts: each call's last split must merge only its own partials
-    and leave the merge counters at zero for the next call."""
+    and split counts (one merging split, and from 16 splits one per query
+    head): each call's merging splits must merge only that call's partials
+    (ready flags tagged with the call count and the split count, which
+    moves the flags' layout), leave the merge counters at zero and count the
+    merged calls of every group."""
     w, cap = small(g=4, L=2000, cap=2048, tag="reuse")
     lens = [2000, 1985]
     K, V = W.kv_cache(w, capacity=cap)
     K64, V64 = O.bf16_to_f64(K), O.bf16_to_f64(V)
     cache = make_cache(K, V, 16)
     ws = R.Workspace(dev())
+    # Sized once for the largest call (a growing workspace is reallocated and
+    # cleared, which would restart the call counts).
+    ws.get(R.lib().resa_decode_workspace_size(2, 2, 8, 125, 16, 128))
     st = O.DecodeState(K64, V64, lens, 16)
     calls = []
     for step, (s, S) in enumerate([(0.5, 7), (0.9, 32), (0.8, 64), (0.95, 3), (0.5, 128), (0.9, 1),
@@ -451,8 +457,9 @@ def test_decode_reused_workspace_many_splits():
         ro, rl = st.attend(O.bf16_to_f64(q), ri, w.sm_scale)
         assert max_abs_err(out.cpu().numpy(), ro) <= TOL
         assert max_abs_err(lse.cpu().numpy(), rl) <= TOL
-    counters = ws.buf[:16].view(torch.int32).cpu().numpy()
-    assert np.all(counters[:4] == 0)
+    words = ws.buf[:32].view(torch.int32).cpu().numpy()
+    assert np.all(words[:4] == 0)  # tickets
+    assert np.all(words[4:8] == 6)  # merged calls: every call but the single-split one
 
 
 def test_decode_deterministic():
