@@ -364,10 +364,12 @@ def oracle_select_idx(w, K64, lens, q, sparsity, min_blocks):
     return ri
 
 
-@pytest.mark.parametrize("g", [1, 4, 7, 8])
+@pytest.mark.parametrize("g", [1, 2, 4, 7, 8])
 @pytest.mark.parametrize("b", [16, 32, 64])
-@pytest.mark.parametrize("splits", [0, 1, 5])
+@pytest.mark.parametrize("splits", [0, 1, 5, 24])
 def test_decode_on_oracle_blocks(g, b, splits):
+    """Decode on the oracle's selection against the oracle's attention; 24
+    splits take the combine spread over g merging splits (one head each)."""
     w, cap = small(g=g, b=b, tag="dec")
     lens = [1000, 777]
     K, V = W.kv_cache(w, capacity=cap)
