@@ -38,12 +38,26 @@ struct Chunk {
   U4 k[4], v[4];
 };
 
+// The chunk's rows from row row0 on (wave-uniform) of the K and V arrays at
+// kp / vp (wave-uniform): non-temporal buffer loads over the chunk's 4 KB of
+// each, at the lane's offset loff (elements) into a row. The resource base
+// is a scalar sum and the offsets 32-bit (measured 0.3 us per launch faster
+// than 64-bit global addressing at 64K and 256K).
+constexpr int kPolicyNt = 2;  // buffer cache policy: non-temporal
 __device__ __forceinline__ void load_chunk(Chunk& ch, const uint16_t* kp, const uint16_t* vp,
-                                           const int (&krow)[4], int row0) {
+                                           const int (&krow)[4], int row0, int loff) {
+  constexpr int kBytes = kChunk * kHeadDim * 2;
+  const size_t base = (size_t)row0 * kHeadDim;
+  const __amdgpu_buffer_rsrc_t rk =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(kp + base), (short)0, kBytes, kBufWord3);
+  const __amdgpu_buffer_rsrc_t rv =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(vp + base), (short)0, kBytes, kBufWord3);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    ch.k[i] = ld16_stream(kp + (size_t)(row0 + krow[i]) * kHeadDim);
-    ch.v[i] = ld16_stream(vp + (size_t)(row0 + 4 * i) * kHeadDim);
+    ch.k[i] = __builtin_bit_cast(U4, __builtin_amdgcn_raw_buffer_load_b128(
+                                         rk, (uint32_t)((krow[i] * kHeadDim + loff) * 2), 0, kPolicyNt));
+    ch.v[i] = __builtin_bit_cast(U4, __builtin_amdgcn_raw_buffer_load_b128(
+                                         rv, (uint32_t)((4 * i * kHeadDim + loff) * 2), 0, kPolicyNt));
   }
 }
 
@@ -487,9 +501,10 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
   // Contiguous layout: chunk rows are counted from the group's first row;
   // paged layout: from the start of the pool (the page's row is staged).
   const bool paged = a.c.table != nullptr;
-  const size_t gbase = (paged ? 0 : grp * (size_t)a.c.capacity * kHeadDim) + (size_t)r * kHeadDim + col;
+  const size_t gbase = paged ? 0 : grp * (size_t)a.c.capacity * kHeadDim;
   const uint16_t* kp = a.c.k + gbase;
   const uint16_t* vp = a.c.v + gbase;
+  const int loff = r * kHeadDim + col;  // this lane's element offset into a chunk row group
   const float scale = a.scale_log2;
   const float ninf = -__builtin_inff();
   // The count and the length are requested last: the first use of either
@@ -591,7 +606,7 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
     for (int k = 0; k <= kDepth; ++k) {
       tring[k] = tok(cc + k * NW);
       if (cc + k * NW < ce) {  // no loads past the pass
-        load_chunk(ring[k], kp, vp, krow, row_of(cc + k * NW));
+        load_chunk(ring[k], kp, vp, krow, row_of(cc + k * NW), loff);
         patch(ring[k], tring[k]);
       }
     }
@@ -604,7 +619,7 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
           __builtin_amdgcn_sched_barrier(0);
           tring[k] = tok(cc + (kDepth + 1) * NW);
           if (cc + (kDepth + 1) * NW < ce) {
-            load_chunk(ring[k], kp, vp, krow, row_of(cc + (kDepth + 1) * NW));
+            load_chunk(ring[k], kp, vp, krow, row_of(cc + (kDepth + 1) * NW), loff);
             patch(ring[k], tring[k]);
           }
           __builtin_amdgcn_sched_barrier(0);
