@@ -41,9 +41,9 @@ struct Chunk {
 // The chunk's rows from row row0 on (wave-uniform) of the K and V arrays at
 // kp / vp (wave-uniform): non-temporal buffer loads over the chunk's 4 KB of
 // each, at the lane's offset loff (elements) into a row. The resource base
-// is a scalar sum and the offsets 32-bit (measured 0.3 us per launch faster
-// than 64-bit global addressing at 64K and 256K).
-constexpr int kPolicyNt = 2;  // buffer cache policy: non-temporal
+// is a scalar sum and the offsets 32-bit (measured 0.3 – 0.7 us per launch
+// faster than 64-bit global addressing at 64K and 256K, and 1 – 2 us faster
+// in the persistent step kernel).
 __device__ __forceinline__ void load_chunk(Chunk& ch, const uint16_t* kp, const uint16_t* vp,
                                            const int (&krow)[4], int row0, int loff) {
   constexpr int kBytes = kChunk * kHeadDim * 2;
@@ -210,8 +210,8 @@ __device__ void merge_tail(const DecodeArgs& a, size_t grp, int S, int own, size
   constexpr int kLse = (kMaxSplits * G + NT - 1) / NT;
   const int tid = tid_of<kOpaque>();
   const float ninf = -__builtin_inff();
-  const float* pl = a.part_lse + grp * S * (size_t)G;
-  const float* po = a.part_o + grp * S * (size_t)(G * kHeadDim);
+  const float* pl = wave_uniform(a.part_lse + grp * S * (size_t)G);
+  const float* po = wave_uniform(a.part_o + grp * S * (size_t)(G * kHeadDim));
   const __amdgpu_buffer_rsrc_t rl = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<float*>(pl), (short)0, S * G * 4, kBufWord3);
   const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(
@@ -329,8 +329,8 @@ __device__ void merge_head(const DecodeArgs& a, size_t grp, int S, int own, int 
   constexpr int kOut = 0x7fffffff;  // an offset past every buffer
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float ninf = -__builtin_inff();
-  const float* pl = a.part_lse + grp * S * (size_t)G;
-  const float* po = a.part_o + grp * S * (size_t)(G * kHeadDim);
+  const float* pl = wave_uniform(a.part_lse + grp * S * (size_t)G);
+  const float* po = wave_uniform(a.part_o + grp * S * (size_t)(G * kHeadDim));
   const __amdgpu_buffer_rsrc_t rl = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<float*>(pl), (short)0, S * G * 4, kBufWord3);
   const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(
@@ -502,8 +502,8 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
   // paged layout: from the start of the pool (the page's row is staged).
   const bool paged = a.c.table != nullptr;
   const size_t gbase = paged ? 0 : grp * (size_t)a.c.capacity * kHeadDim;
-  const uint16_t* kp = a.c.k + gbase;
-  const uint16_t* vp = a.c.v + gbase;
+  const uint16_t* kp = wave_uniform(a.c.k + gbase);
+  const uint16_t* vp = wave_uniform(a.c.v + gbase);
   const int loff = r * kHeadDim + col;  // this lane's element offset into a chunk row group
   const float scale = a.scale_log2;
   const float ninf = -__builtin_inff();

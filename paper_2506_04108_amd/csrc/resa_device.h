@@ -12,6 +12,7 @@ constexpr int kChunk = 16;  // tokens handled per decode step of a wave
 constexpr int kMaxGroup = 8;  // query heads per kv head (RESA_MAX_GROUP)
 constexpr int kBufWord3 = 0x00020000;  // raw buffer resource word 3: 32-bit data format
 constexpr int kSc1 = 16;              // buffer cache policy: agent-scope coherent
+constexpr int kPolicyNt = 2;          // buffer cache policy: non-temporal (read-once data)
 // s_waitcnt immediate that waits for every outstanding vector memory
 // operation (vmcnt 0) and leaves expcnt and lgkmcnt alone (gfx9 encoding).
 constexpr int kWaitVmcnt0 = 0x0F70;
@@ -53,6 +54,15 @@ __device__ __forceinline__ int tid_of() {
 
 __device__ __forceinline__ U4 ld16(const void* p) {
   return *reinterpret_cast<const U4*>(p);
+}
+// A pointer that is the same in every lane of the wave, marked so for the
+// compiler (buffer resources built from it then stay in scalar registers).
+template <typename T>
+__device__ __forceinline__ T* wave_uniform(T* p) {
+  const uint64_t u = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+  return reinterpret_cast<T*>(((uint64_t)hi << 32) | lo);
 }
 __device__ __forceinline__ U4 ld16_stream(const void* p) {
   // Read-once data: non-temporal hint keeps it from displacing reused lines.

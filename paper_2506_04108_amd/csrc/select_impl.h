@@ -33,8 +33,12 @@ __device__ __forceinline__ uint32_t block_key(int m, int forced_from, float s) {
   return m >= forced_from ? 0xFFFFFFFFu : order_key(s);
 }
 
+// A buffer resource over a workgroup-uniform range (marked uniform for the
+// compiler: in the persistent step kernel the group index comes from LDS,
+// and a resource in vector registers would take a loop over the lanes).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, kBufWord3);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(wave_uniform(p)), (short)0,
+                                           (int)__builtin_amdgcn_readfirstlane(bytes), kBufWord3);
 }
 
 // Length of sequence bb seen by the selection. With an append fused in
