@@ -742,7 +742,7 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
   // split holding the last ticket returns the ticket counter to zero and
   // advances the count once every ticket is taken.
   const uint32_t tk = lds.ticket;
-  const bool spread = !kCoherent && G >= 2 && S >= kSpreadSplits;
+  const bool spread = !kCoherent && G >= 2 && S >= kSpreadSplits && S >= G;
   const uint32_t first = spread ? (uint32_t)(S - G) : (uint32_t)(S - 1);
   const uint64_t tag = ((uint64_t)(epoch + 1u) << 32) | (uint32_t)S;
   if (spread || tk < first) {
