@@ -480,6 +480,34 @@ def test_decode_deterministic():
     assert torch.equal(idx, idx2) and torch.equal(a, b) and torch.equal(la, lb)
 
 
+def test_decode_tagged_flags_many_calls():
+    """Forty calls on one workspace, cycling through split counts that move
+    the ready flags' layout (and through the single merger and the spread
+    combine): every call is bit-identical to the same call on a freshly
+    zeroed workspace, so no flag of an earlier call is ever taken for one of
+    the current call, and the per-group call counts advance once per call."""
+    w, cap = small(g=4, L=2000, cap=2048, B=3, H=2, tag="tags")
+    lens = [2000, 1500, 1999]
+    K, V = W.kv_cache(w, capacity=cap)
+    cache = make_cache(K, V, 16)
+    lt = i32(lens)
+    R.block_summarize(cache, lt)
+    ws = R.Workspace(dev())
+    ws.get(R.lib().resa_decode_workspace_size(3, 2, 8, 125, 16, 64))
+    splits = [16, 24, 3, 32, 33, 64, 17, 4]
+    for call in range(40):
+        q = W.decode_query(w, call)
+        idx, ns = R.select_blocks(cache, up(q), lt, 2000, 0.5, 4, 1)
+        S = splits[call % len(splits)]
+        a, la = R.sparse_decode(cache, up(q), lt, idx, ns, num_splits=S, workspace=ws)
+        b, lb = R.sparse_decode(cache, up(q), lt, idx, ns, num_splits=S, workspace=R.Workspace(dev()))
+        torch.cuda.synchronize()
+        assert torch.equal(a, b) and torch.equal(la, lb), (call, S)
+    words = ws.buf[:48].view(torch.int32).cpu().numpy()
+    assert np.all(words[:6] == 0)  # tickets
+    assert np.all(words[6:12] == 40)  # merged calls
+
+
 @pytest.mark.parametrize("b,n_local,M", [(16, 1, 40), (16, 0, 40), (32, 1, 40), (64, 0, 40),
                                          (16, 1, 12500), (16, 1, 33000)])
 def test_append_select_matches_separate(b, n_local, M):
