@@ -406,9 +406,12 @@ def test_decode_all_blocks_is_dense():
             assert max_abs_err(lse[bi, 4 * hi:4 * hi + 4].cpu().numpy(), rl) <= TOL
 
 
-def test_decode_edge_cases():
+@pytest.mark.parametrize("splits", [9, 20])
+def test_decode_edge_cases(splits):
     """Empty selection, a single valid token, unsorted ids, ids out of range,
-    and more splits than chunks (empty splits)."""
+    and more splits than chunks (empty splits; 20 splits take the combine
+    spread over the g merging splits, whose all-empty heads must give 0 and
+    -inf)."""
     w, cap = small(g=4, L=40, cap=64, B=4, H=1, tag="edge")
     lens = [40, 1, 33, 40]
     K, V = W.kv_cache(w, capacity=cap, garbage=1e4)
@@ -416,7 +419,7 @@ def test_decode_edge_cases():
     ids = {(0, 0): [], (1, 0): [0], (2, 0): [2, 0], (3, 0): [1, 7, -1, 2]}
     idx, ns = padded_idx(ids, 4, 1, 4)
     cache = make_cache(K, V, 16)
-    out, lse = R.sparse_decode(cache, up(q), i32(lens), i32(idx), i32(ns), num_splits=9)
+    out, lse = R.sparse_decode(cache, up(q), i32(lens), i32(idx), i32(ns), num_splits=splits)
     torch.cuda.synchronize()
     o, l = out.cpu().numpy(), lse.cpu().numpy()
     K64, V64, q64 = O.bf16_to_f64(K), O.bf16_to_f64(V), O.bf16_to_f64(q)
