@@ -511,9 +511,11 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
   // (a move into scalar registers) then waits for everything above at once.
   const int n_raw = ld_i32<true>(a.num_sel + grp);
   const int L0 = ld_i32<true>(lens + bb);
-  // Calls of this group merged so far (several splits): tags this call's
-  // ready flags.
-  const uint32_t epoch = S > 1 ? __hip_atomic_load(a.epochs + grp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+  // Calls of this group merged so far: tags this call's ready flags.
+  // Requested with the count and the length (unconditionally: behind a
+  // branch the compiler would move it into a scalar register, and so wait
+  // for it, right there); nothing uses it before the tail.
+  uint32_t epoch = __hip_atomic_load(a.epochs + grp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const bool app = append && L0 >= 0 && L0 < a.c.capacity;
   const int L = app ? L0 + 1 : L0;
   const int pos = app ? L0 : -1;
@@ -735,6 +737,7 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
   }
   if (tid == 0) lds.ticket = ticket;
   lds_sync();
+  __asm__ volatile("" : "+v"(epoch));
   // Merging splits: the one holding the last ticket, or with many splits
   // those holding the last G tickets, one query head each. A ready flag
   // carries this call's tag (the group's merged-call count + 1, and S), so
