@@ -737,6 +737,8 @@ __device__ __forceinline__ bool decode_split(const DecodeArgs& a, int bb, int hk
   }
   if (tid == 0) lds.ticket = ticket;
   lds_sync();
+  // The call count read at the start is first used here: it stays in a
+  // vector register until now, so no earlier instruction waits for it.
   __asm__ volatile("" : "+v"(epoch));
   // Merging splits: the one holding the last ticket, or with many splits
   // those holding the last G tickets, one query head each. A ready flag
