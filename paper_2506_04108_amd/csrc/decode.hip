@@ -39,10 +39,13 @@ hipError_t launch_g(const DecodeArgs& a, hipStream_t stream) {
 int32_t decode_auto_splits(int32_t batch, int32_t kv_heads, int32_t n_cap, int32_t block_size) {
   const int64_t groups = (int64_t)batch * kv_heads;
   const int64_t chunks = (int64_t)n_cap * (block_size / kChunk);
-  // About one workgroup per CU (256 CUs), with at least 4 chunks per wave:
-  // measured on MI355X, fewer and longer-running workgroups beat more splits.
+  // About one workgroup per CU (256 CUs), with at least one chunk per wave.
+  // Measured on MI355X: more splits than that lose to fewer, longer-running
+  // workgroups at 64K and 256K (4 and 32 splits); small groups gain from the
+  // full count (4K, batch 1: 16 splits 9.1 us against 11.5 us with 4, the
+  // earlier cap of four chunks per wave).
   int64_t s = (256 + groups - 1) / groups;
-  const int64_t most = chunks / (4 * kDecodeWaves);
+  const int64_t most = chunks / kDecodeWaves;
   if (s > most) s = most;
   if (s > 256) s = 256;
   if (s < 1) s = 1;
