@@ -652,7 +652,9 @@ int32_t rectify_chunk(int32_t batch, int32_t kv_heads, int32_t nqblk, int32_t ma
   if (target < 1) target = 1;
   int64_t chunk = (max_seq_len + target - 1) / target;
   chunk = (chunk + kMaxKeyTile - 1) / kMaxKeyTile * kMaxKeyTile;
-  if (chunk < 512) chunk = 512;
+  // Short caches still fill the chip (4K, batch 1: 32 splits of 128 keys,
+  // 30.4 against 34.0 us per call with a 512-key minimum).
+  if (chunk < 128) chunk = 128;
   // At most kMaxRectSplits splits, so the combine's weights fit in LDS.
   const int64_t least = ((int64_t)max_seq_len + kMaxRectSplits - 1) / kMaxRectSplits;
   if (chunk < least) chunk = (least + kMaxKeyTile - 1) / kMaxKeyTile * kMaxKeyTile;
