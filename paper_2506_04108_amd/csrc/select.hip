@@ -5,8 +5,7 @@
 namespace resa {
 namespace {
 
-constexpr int kSelThreads = 1024;                 // 16 waves
-constexpr int kSelWaves = kSelThreads / 64;
+constexpr int kSelThreads = 1024;                 // 16 waves (512 for short ranges)
 constexpr int kTopnThreads = 1024;
 
 // Exact top-n per (sequence, kv head): an MSD radix select over order-
@@ -141,8 +140,8 @@ __global__ __launch_bounds__(kTopnThreads) void k_topn(SelectArgs a) {
 // ticket use agent scope (write-through stores, coherent loads, a relaxed
 // atomic after the stores are acknowledged), so no cache writeback is needed
 // between workgroups.
-template <int NJ>
-__global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
+template <int NJ, int NT = kSelThreads>
+__global__ __launch_bounds__(NT) void k_select(SelectArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t s_hist[kBins2];
   __shared__ __attribute__((aligned(16))) float s_score[kMaxBlocksPerWg];
   __shared__ uint32_t s_lds32[32];
@@ -150,7 +149,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
   const int tid = threadIdx.x;
   const int hk = blockIdx.y, bb = blockIdx.z;
   const size_t grp = (size_t)bb * a.c.kv_heads + hk;
-  const RangeInfo ri = score_range<kSelWaves, 1, false, window_lists(NJ, kSelThreads)>(a, bb, hk, blockIdx.x, gridDim.x, s_hist, s_score);
+  const RangeInfo ri = score_range<NT / 64, 1, false, window_lists(NJ, NT)>(a, bb, hk, blockIdx.x, gridDim.x, s_hist, s_score);
   if (!a.fused) return;
   __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
@@ -158,7 +157,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelectArgs a) {
     s_misc[3] = __hip_atomic_fetch_add(a.counters + grp, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
   if (s_misc[3] != gridDim.x - 1) return;
-  select_tail<NJ, kSelThreads>(a, grp, ri.M, ri.forced_from, gridDim.x, ri.win, s_hist, s_lds32, s_misc,
+  select_tail<NJ, NT>(a, grp, ri.M, ri.forced_from, gridDim.x, ri.win, s_hist, s_lds32, s_misc,
                                reinterpret_cast<int32_t*>(s_score), bb, ri.sl.L, nullptr);
 }
 
@@ -168,9 +167,24 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   if (a.max_blocks_seq > 0) {
     dim3 grid((a.max_blocks_seq + a.blocks_per_wg - 1) / a.blocks_per_wg, a.c.kv_heads, a.c.batch);
     // Keys per thread of the fused top-n: the smallest instantiation that
-    // holds the longest group (every group's M <= max_blocks_seq).
+    // holds the longest group (every group's M <= max_blocks_seq). Short
+    // score ranges (at most 256 blocks, two 8-block tiles per wave at 8
+    // waves) of groups up to 4096 blocks run in 512-thread workgroups: there
+    // the top-n of the last workgroup dominates, and half the waves share
+    // the CU's SIMDs (4K batch 1 selection 9.9 -> 9.35 us, 32K batch 4
+    // 14.2 -> 13.9 us; 64K batch 8, with 1024-block ranges, is slower so).
     const int per = (a.max_blocks_seq + kSelThreads - 1) / kSelThreads;
-    if (per <= 4)
+    const int per_half = (a.max_blocks_seq + 511) / 512;
+    const bool half = a.blocks_per_wg <= 256 && per_half <= 8;
+    if (half && per_half <= 4)
+      hipLaunchKernelGGL((k_select<4, 512>), grid, dim3(512), 0, stream, a);
+    else if (half && per_half <= 5)
+      hipLaunchKernelGGL((k_select<5, 512>), grid, dim3(512), 0, stream, a);
+    else if (half && per_half <= 6)
+      hipLaunchKernelGGL((k_select<6, 512>), grid, dim3(512), 0, stream, a);
+    else if (half)
+      hipLaunchKernelGGL((k_select<8, 512>), grid, dim3(512), 0, stream, a);
+    else if (per <= 4)
       hipLaunchKernelGGL((k_select<4>), grid, dim3(kSelThreads), 0, stream, a);
     else if (per <= 5)
       hipLaunchKernelGGL((k_select<5>), grid, dim3(kSelThreads), 0, stream, a);
