@@ -193,11 +193,15 @@ def test_select_exact_ties_large(M):
     assert list(gi[0, 0, :gn[0, 0]]) == list(ri[0, 0])
 
 
-@pytest.mark.parametrize("M", [4097, 8193, 12000, 16400, 20000, 28000, 32768, 32800])
+@pytest.mark.parametrize("M", [2049, 2600, 3500, 4096, 4097, 8193, 12000, 16400, 20000, 28000, 32768,
+                               32800])
 def test_select_large_groups(M):
-    """Group sizes that take each per-thread key count of the fused selection
-    (4097 just past 4 keys per thread, up to its 32768-key budget); 32800
-    blocks exceed it, so scoring and the standalone top-n kernel run instead."""
+    """Group sizes that take each per-thread key count of the fused selection:
+    up to 4096 blocks in 128-block ranges the 512-thread workgroups (2049,
+    2600, 3500 and 4096 take 5, 6, 8 and 8 keys per thread), from 4097 the
+    1024-thread ones (just past 4 keys per thread, up to the 32768-key
+    budget); 32800 blocks exceed it, so scoring and the standalone top-n
+    kernel run instead."""
     w = W.TINY_4K.with_(batch=1, num_q_heads=4, num_kv_heads=1, seq_len=M * 16 - 5,
                         min_tokens=0, seed_tag=f"large{M}")
     cap = M * 16
