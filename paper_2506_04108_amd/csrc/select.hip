@@ -127,7 +127,8 @@ __global__ __launch_bounds__(kTopnThreads) void k_topn(SelectArgs a) {
 
 // Pooled query (Fig. 3), Quest scores (Eq. 4) and, when `fused`, the top-n
 // (Eq. 5) in one kernel. Grid (ceil(max_blocks_seq / blocks_per_wg), kv
-// heads, batch), about one 16-wave workgroup per CU. Each workgroup streams
+// heads, batch), about one workgroup per CU (16 waves; 8 for short ranges of
+// short groups, see launch_select). Each workgroup streams
 // the summaries of its block range (score_range): lane (r, c) handles dims [8c, 8c + 8) of
 // 8-block tiles, so each wave-wide load is four whole 256-byte summary rows,
 // and the next tile's loads are in flight while one is scored. Per dimension
@@ -211,12 +212,12 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
 int32_t select_fused_max_blocks() { return kMaxSelectBlocks; }
 
 int32_t select_blocks_per_wg(int32_t batch, int32_t kv_heads, int32_t max_blocks_seq) {
-  // About one 16-wave workgroup per CU (256 CUs) in all: a group's blocks are
-  // cut into equal ranges of whole 32-block words (so a word of the
-  // above-window bits belongs to one range), at least one 8-block scoring
-  // tile per wave (128 blocks: small groups spread over more workgroups,
-  // 4K batch 1 selection 11.2 -> 10.0 us against 256) and at most the LDS
-  // staging area.
+  // About one workgroup per CU (256 CUs) in all: a group's blocks are cut
+  // into equal ranges of whole 32-block words (so a word of the above-window
+  // bits belongs to one range), at least one 8-block scoring tile per wave
+  // of a 16-wave workgroup (128 blocks: small groups spread over more
+  // workgroups, 4K batch 1 selection 11.2 -> 10.0 us against 256) and at
+  // most the LDS staging area.
   const int64_t groups = (int64_t)batch * kv_heads;
   const int64_t per_group = (256 + groups - 1) / groups;
   int64_t bpw = ((int64_t)max_blocks_seq + per_group - 1) / per_group;
