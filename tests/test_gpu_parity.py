@@ -138,8 +138,12 @@ def test_select_vs_oracle_tiny4k(b):
     assert swaps <= 2
 
 
-def test_select_ragged_batch_and_sparsities():
-    w, cap = small(g=7, L=3000, cap=3072, B=3, H=2, tag="selr")
+@pytest.mark.parametrize("g", [1, 3, 5, 6, 7])
+def test_select_ragged_batch_and_sparsities(g):
+    """Ragged lengths (one sequence of 17 tokens) at several sparsities and
+    minimum budgets, for group sizes whose pooled query averages 1 to 7
+    heads."""
+    w, cap = small(g=g, L=3000, cap=3072, B=3, H=2, tag="selr")
     lens = [3000, 17, 2049]
     q = W.decode_query(w)
     for s, nm in ((0.8, 4), (0.95, 0), (0.0, 0), (1.0, 2)):
@@ -368,12 +372,13 @@ def oracle_select_idx(w, K64, lens, q, sparsity, min_blocks):
     return ri
 
 
-@pytest.mark.parametrize("g", [1, 2, 4, 7, 8])
+@pytest.mark.parametrize("g", [1, 2, 3, 4, 5, 6, 7, 8])
 @pytest.mark.parametrize("b", [16, 32, 64])
 @pytest.mark.parametrize("splits", [0, 1, 5, 24])
 def test_decode_on_oracle_blocks(g, b, splits):
-    """Decode on the oracle's selection against the oracle's attention; 24
-    splits take the combine spread over g merging splits (one head each)."""
+    """Decode on the oracle's selection against the oracle's attention, for
+    every group size the library instantiates (g = 1 .. 8); 24 splits take
+    the combine spread over g merging splits (one head each)."""
     w, cap = small(g=g, b=b, tag="dec")
     lens = [1000, 777]
     K, V = W.kv_cache(w, capacity=cap)
@@ -574,7 +579,8 @@ def test_append_select_matches_separate(b, n_local, M):
 
 # -------------------------------------------------------------------- rectify
 
-@pytest.mark.parametrize("g,f", [(4, 16), (4, 1), (7, 32), (8, 32), (2, 64)])
+@pytest.mark.parametrize("g,f", [(4, 16), (4, 1), (7, 32), (8, 32), (2, 64), (1, 16), (3, 32), (5, 16),
+                                 (6, 8)])
 def test_rectify_vs_oracle(g, f):
     w, cap = small(g=g, L=300, cap=320, tag="rect")
     lens = [300, 257]
