@@ -229,9 +229,10 @@ size_t resa_decode_workspace_size(int32_t batch, int32_t num_kv_heads,
 /*
  * Eq. 2 with Alg. 2 (App. A): block-sparse flash-decoding. For every
  * (sequence b, kv head i) the selected blocks block_idx[b, i, :num_sel[b, i]]
- * (ids in [0, M_b); any order; as written by resa_select_blocks) are split
- * into num_splits contiguous parts; each part runs an online softmax of the g
- * query heads over its blocks' valid tokens (t < L_b; others are excluded)
+ * (ids in [0, M_b); any order; as written by resa_select_blocks) are cut
+ * into 16-token chunks, dealt to num_splits parts one by one (part s takes
+ * chunks s, s + num_splits, ...); each part runs an online softmax of the g
+ * query heads over its chunks' valid tokens (t < L_b; others are excluded)
  * and the parts are merged by log-sum-exp. For query head h:
  *   out[b, h, :] = sum_t softmax_t(q_h . K_t * sm_scale) V_t     (fp32)
  *   lse[b, h]    = log sum_t exp(q_h . K_t * sm_scale)           (optional)
@@ -325,8 +326,11 @@ int resa_decode_step(const resa_kv_cache_t* c, const void* k_new, const void* v_
                      int32_t n_cap, int32_t num_splits, float sm_scale, float* out, float* lse,
                      void* workspace, size_t workspace_bytes, void* stream);
 
-/* Workspace bytes resa_dense_rectify needs: 0 when one key split covers
- * the window (long windows such as prefill), and then workspace may be NULL. */
+/* Workspace bytes resa_dense_rectify needs for any call whose max_seq_len
+ * is at most the one given (the size never decreases as max_seq_len grows,
+ * so a workspace sized once for the longest context serves every call): 0
+ * when one key split covers every such window (long windows such as
+ * prefill), and then workspace may be NULL. */
 size_t resa_rectify_workspace_size(int32_t batch, int32_t num_kv_heads,
                                    int32_t num_q_heads, int32_t f, int32_t max_seq_len);
 

@@ -679,7 +679,16 @@ size_t resa_rectify_workspace_size(int32_t batch, int32_t num_kv_heads, int32_t 
                                    int32_t f, int32_t max_seq_len) {
   if (batch < 1 || num_kv_heads < 1 || num_q_heads < num_kv_heads || f < 1 || max_seq_len < 1)
     return 0;
-  return rectify_layout(batch, num_kv_heads, num_q_heads / num_kv_heads, f, max_seq_len).total;
+  // Sized for the largest split count of any length up to max_seq_len, so a
+  // workspace sized once serves every shorter call (the layout of a call is
+  // never larger: its offsets grow with its own split count).
+  const int32_t group = num_q_heads / num_kv_heads;
+  const int32_t nq = resa::rectify_num_qblocks(group, f);
+  const int32_t most = resa::rectify_max_splits(batch, num_kv_heads, nq, max_seq_len);
+  if (most == 1) return 0;  // every such call has one split, written to out / lse directly
+  const size_t groups = (size_t)batch * num_kv_heads;
+  const size_t rows = (size_t)group * f;
+  return round256(groups * most * rows * 4) + groups * most * rows * RESA_HEAD_DIM * 4;
 }
 
 int resa_dense_rectify(const resa_kv_cache_t* c, const void* q_f, const void* k_f,

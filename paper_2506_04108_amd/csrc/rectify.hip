@@ -646,19 +646,37 @@ int32_t rectify_num_qblocks(int32_t group, int32_t f) {
   return (rows + per - 1) / per;
 }
 
-int32_t rectify_chunk(int32_t batch, int32_t kv_heads, int32_t nqblk, int32_t max_seq_len) {
+// Key splits per group the attention aims for: about 512 workgroups in all.
+static int64_t rectify_target_splits(int32_t batch, int32_t kv_heads, int32_t nqblk) {
   const int64_t wgs = (int64_t)batch * kv_heads * nqblk;
-  int64_t target = (512 + wgs - 1) / wgs;
-  if (target < 1) target = 1;
+  const int64_t target = (512 + wgs - 1) / wgs;
+  return target < 1 ? 1 : target;
+}
+// Short caches still fill the chip (4K, batch 1: 32 splits of 128 keys,
+// 30.4 against 34.0 us per call with a 512-key minimum).
+constexpr int kMinRectChunk = 128;
+
+int32_t rectify_chunk(int32_t batch, int32_t kv_heads, int32_t nqblk, int32_t max_seq_len) {
+  const int64_t target = rectify_target_splits(batch, kv_heads, nqblk);
   int64_t chunk = (max_seq_len + target - 1) / target;
   chunk = (chunk + kMaxKeyTile - 1) / kMaxKeyTile * kMaxKeyTile;
-  // Short caches still fill the chip (4K, batch 1: 32 splits of 128 keys,
-  // 30.4 against 34.0 us per call with a 512-key minimum).
-  if (chunk < 128) chunk = 128;
+  if (chunk < kMinRectChunk) chunk = kMinRectChunk;
   // At most kMaxRectSplits splits, so the combine's weights fit in LDS.
   const int64_t least = ((int64_t)max_seq_len + kMaxRectSplits - 1) / kMaxRectSplits;
   if (chunk < least) chunk = (least + kMaxKeyTile - 1) / kMaxKeyTile * kMaxKeyTile;
   return (int32_t)chunk;
+}
+
+int32_t rectify_max_splits(int32_t batch, int32_t kv_heads, int32_t nqblk, int32_t max_seq_len) {
+  // ceil(L / chunk) with chunk >= 128 and chunk >= ceil(L / target) (target
+  // <= 512 < kMaxRectSplits): at most min(ceil(L / 128), target), a bound
+  // that never decreases as L grows, while the split count itself can (the
+  // chunk is rounded up to whole 64-key tiles: 512 splits at L = 65536, 342
+  // at 65537 for one group and one query block).
+  const int64_t by_len = ((int64_t)max_seq_len + kMinRectChunk - 1) / kMinRectChunk;
+  const int64_t target = rectify_target_splits(batch, kv_heads, nqblk);
+  const int64_t s = by_len < target ? by_len : target;
+  return (int32_t)(s < 1 ? 1 : s);
 }
 
 hipError_t launch_rectify(const RectifyArgs& a, hipStream_t stream) {

@@ -150,5 +150,8 @@ int32_t step_hist_words(int32_t batch, int32_t kv_heads, int32_t max_blocks_seq)
 int32_t step_max_blocks();
 int32_t rectify_num_qblocks(int32_t group, int32_t f);
 int32_t rectify_chunk(int32_t batch, int32_t kv_heads, int32_t nqblk, int32_t max_seq_len);
+// An upper bound on the key splits of any call with lengths up to
+// max_seq_len, non-decreasing in max_seq_len (workspace sizing).
+int32_t rectify_max_splits(int32_t batch, int32_t kv_heads, int32_t nqblk, int32_t max_seq_len);
 
 }  // namespace resa

@@ -202,3 +202,44 @@ def test_product_never_imports_oracle():
             if fn.endswith((".py", ".cpp", ".hip", ".h")):
                 text = open(os.path.join(dirpath, fn)).read()
                 assert "import oracle" not in text and "from oracle" not in text, fn
+
+
+def test_workspace_sizes_grow_with_length():
+    """A workspace sized for a longer context serves every shorter one: the
+    selection, decode, fused-step and rectification sizes never decrease as
+    the length (or the selected-block capacity) grows (lengths 65536 /
+    65537 around the rectification's 128-key chunk minimum included), and
+    the automatic split count stays in [1, 256] with at least one 16-token
+    chunk per wave of four."""
+    lib = L.lib()
+    lengths = sorted(set([1, 15, 16, 17, 2047, 2048, 2049, 65536, 65537, 65600]
+                         + [int(1.03 ** i) + 16 * (i % 7) for i in range(470)]))
+    for batch, heads, g in ((1, 1, 1), (1, 8, 4), (2, 2, 7), (3, 4, 2), (8, 8, 4), (16, 8, 4), (64, 4, 8)):
+        for b in (16, 32, 64):
+            prev_sel = prev_step = 0
+            for ln in lengths:
+                sel = lib.resa_select_workspace_size(batch, heads, ln, b)
+                assert sel >= prev_sel, (batch, heads, b, ln)
+                prev_sel = sel
+                m = -(-ln // b)
+                n_cap = max(1, m // 10)
+                step = lib.resa_step_workspace_size(batch, heads, heads * g, ln, b, n_cap, 0)
+                assert step >= prev_step, (batch, heads, b, ln)
+                prev_step = step
+            prev_dec = 0
+            for n_cap in range(1, 3000, 7):
+                s = lib.resa_decode_num_splits(batch, heads, n_cap, b)
+                chunks = n_cap * (b // 16)
+                assert 1 <= s <= 256
+                assert s == 1 or s <= chunks // 4, (batch, heads, n_cap, b, s)
+                dec = lib.resa_decode_workspace_size(batch, heads, heads * g, n_cap, b, 0)
+                assert dec >= prev_dec, (batch, heads, n_cap, b)
+                prev_dec = dec
+        for f in (1, 16, 32, 300):
+            prev_rect = 0
+            for ln in lengths:
+                if ln < f:
+                    continue
+                r = lib.resa_rectify_workspace_size(batch, heads, heads * g, f, ln)
+                assert r >= prev_rect, (batch, heads, g, f, ln)
+                prev_rect = r

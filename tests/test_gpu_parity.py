@@ -664,6 +664,40 @@ def test_rectify_large_and_tiny_v(g, f, lens, cap):
             assert worst <= TOL
 
 
+def test_rectify_workspace_sized_for_longer_context():
+    """A workspace sized once (C ABI) for the longest context serves a shorter
+    call that splits its keys more finely: one group and one query row take
+    512 key splits of 128 keys at L = 65536, where a 65600-token call takes
+    342 splits of 192 keys; the call must succeed and match the oracle."""
+    import ctypes as C
+    g, f, L, Lmax = 1, 1, 65536, 65600
+    w, cap = small(g=g, L=L, cap=Lmax + 64, B=1, H=1, tag="rws")
+    K, V = W.kv_cache(w, capacity=cap)
+    cache = make_cache(K, V, 16, sentinel=False)
+    lt = i32([L])
+    R.block_summarize(cache, lt)
+    qf, kf, vf = W.rectify_inputs(w, 4, K[:, :, L - f:L], V[:, :, L - f:L], f)
+    lib = R.lib()
+    nbytes = lib.resa_rectify_workspace_size(1, 1, g, f, Lmax)
+    assert nbytes >= lib.resa_rectify_workspace_size(1, 1, g, f, L) > 0
+    ws = torch.zeros(nbytes, dtype=torch.uint8, device=dev())
+    q_d, k_d, v_d = up(qf), up(kf), up(vf)
+    out = torch.empty((1, g, f, 128), dtype=torch.float32, device=dev())
+    lse = torch.empty((1, g, f), dtype=torch.float32, device=dev())
+    d = cache.desc()
+    rc = lib.resa_dense_rectify(C.byref(d), q_d.data_ptr(), k_d.data_ptr(), v_d.data_ptr(), g, f,
+                                lt.data_ptr(), None, L, C.c_float(w.sm_scale), out.data_ptr(),
+                                lse.data_ptr(), 1, ws.data_ptr(), C.c_size_t(nbytes),
+                                C.c_void_p(torch.cuda.current_stream().cuda_stream))
+    assert rc == 0, lib.resa_last_error()
+    torch.cuda.synchronize()
+    st = O.DecodeState(O.bf16_to_f64(K), O.bf16_to_f64(V), [L], 16)
+    ro, rl = st.rectify(O.bf16_to_f64(qf), O.bf16_to_f64(kf), O.bf16_to_f64(vf), f, w.sm_scale)
+    eo, el = max_abs_err(out.cpu().numpy(), ro), max_abs_err(lse.cpu().numpy(), rl)
+    print(f"rectify on a workspace sized for {Lmax}: max |dO| {eo:.2e}, max |dlse| {el:.2e}")
+    assert eo <= TOL and el <= TOL
+
+
 def test_rectify_tiny4k_full():
     """The tiny 4K layer: f = 16 rows, causal over the whole 4096 cache."""
     w = W.TINY_4K
