@@ -905,3 +905,55 @@ def test_graph_replay_matches_eager():
     assert l2.cpu().tolist() == [x + steps for x in lens0]
     for name in ("k", "v", "kmin", "kmax"):
         assert torch.equal(getattr(c1, name), getattr(c2, name)), name
+
+
+def test_rectify_graph_replay_matches_eager():
+    """Rectification (row rewrite, summary refresh, key-split attention and
+    the split merge) recorded once in a HIP graph and replayed with new
+    re-encoded rows each time, with eager work and synchronisations between
+    the replays, gives bit-identical outputs, lse, caches and summaries to the
+    same calls made eagerly."""
+    g, f, B, H = 4, 32, 2, 2
+    w, cap = small(g=g, L=2000, cap=2048, B=B, H=H, tag="rgraph")
+    lens = [2000, 1500]
+    K, V = W.kv_cache(w, capacity=cap)
+    c1 = make_cache(K, V, 16, sentinel=False)
+    c2 = make_cache(K, V, 16, sentinel=False)
+    l1, l2 = i32(lens), i32(lens)
+    R.block_summarize(c1, l1)
+    R.block_summarize(c2, l2)
+    lib = R.lib()
+    nbytes = lib.resa_rectify_workspace_size(B, H, g * H, f, max(lens))
+    assert nbytes > 0  # several key splits: the merge kernel runs too
+    d = dev()
+    bf = torch.bfloat16
+    q_s = torch.zeros((B, g * H, f, 128), dtype=bf, device=d)
+    k_s = torch.zeros((B, H, f, 128), dtype=bf, device=d)
+    v_s = torch.zeros((B, H, f, 128), dtype=bf, device=d)
+    out2 = torch.empty((B, g * H, f, 128), dtype=torch.float32, device=d)
+    lse2 = torch.empty((B, g * H, f), dtype=torch.float32, device=d)
+    ws1, ws2 = R.Workspace(d), R.Workspace(d)
+    ws1.get(nbytes)
+    ws2.get(nbytes)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.graph(graph, stream=side):
+        R.dense_rectify(c2, q_s, k_s, v_s, l2, max(lens), out=out2, lse=lse2, workspace=ws2)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        base_k = np.stack([np.stack([K[bi, hi, lens[bi] - f:lens[bi]] for hi in range(H)]) for bi in range(B)])
+        base_v = np.stack([np.stack([V[bi, hi, lens[bi] - f:lens[bi]] for hi in range(H)]) for bi in range(B)])
+        qf, kf, vf = W.rectify_inputs(w, 20 + rep, base_k, base_v, f)
+        q_s.copy_(up(qf))
+        k_s.copy_(up(kf))
+        v_s.copy_(up(vf))
+        graph.replay()
+        torch.cuda.synchronize()
+        o1, s1 = R.dense_rectify(c1, up(qf), up(kf), up(vf), l1, max(lens), workspace=ws1)
+        torch.cuda.synchronize()
+        print(f"rectify graph replay {rep}: max |out| {float(out2.abs().max()):.3f}", flush=True)
+        assert torch.equal(o1, out2) and torch.equal(s1, lse2)
+        for name in ("k", "v", "kmin", "kmax"):
+            assert torch.equal(getattr(c1, name), getattr(c2, name)), name
