@@ -83,13 +83,15 @@ def test_paged_matches_contiguous(b, g):
     _same_cache(c1, c2, cur)
 
 
-def test_paged_prefill():
+@pytest.mark.parametrize("b", [16, 32, 64])
+def test_paged_prefill(b):
     """Whole-prompt prefill (f = L) into a paged cache through the
-    rectification call, then one decode step: identical to the contiguous
-    layout, rows and summaries included."""
-    w = W.LONG_64K.with_(batch=2, num_q_heads=8, num_kv_heads=2, seq_len=700, min_tokens=64,
-                         seed_tag="pagedprefill")
-    b, cap = 16, 768
+    rectification call (8-wave workgroups, 64-key tiles over pages of b
+    tokens), then one decode step: identical to the contiguous layout, rows
+    and summaries included."""
+    w = W.LONG_64K.with_(batch=2, num_q_heads=8, num_kv_heads=2, seq_len=700, min_tokens=4 * b,
+                         block_size=b, seed_tag=f"pagedprefill{b}")
+    cap = 768
     lens = [700, 700]
     _, _, c1, c2 = _pair(w, cap, lens, [701, 701], b, seed=3)
     base_k = np.zeros((2, 2, 700, 128), dtype=np.uint16)
